@@ -1,0 +1,398 @@
+"""Pins of the CPU oracle against what the paper and mathematics fix (no GPU needed).
+
+Each test checks the oracle against something other than itself: closed forms, invariants, special
+cases that reduce to a library routine (torch / numpy), or brute force on tiny inputs.
+"""
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from helpers import from_bits, rng, to_bits
+
+
+# ------------------------------------------------------------------------ rules of the method
+def test_window_rows_follow_static_eviction_setup():
+    # App. F: last 20% of the prompt, 10% beyond 24k tokens (rounded down).
+    assert [oracle.window_rows(T) for T in (512, 2048, 8192)] == [102, 409, 1638]
+    assert [oracle.window_rows(T) for T in (32768, 131072)] == [3276, 13107]
+    assert oracle.window_rows(24576) == 4915      # 20% at exactly 24k
+    assert oracle.window_rows(24577) == 2457      # 10% just above
+    assert oracle.window_rows(3) == 1
+
+
+def test_owner_layer_skips_first_two_layers():
+    # Sec. 3.4: pairs of adjacent layers share, the first two layers never do.
+    assert [oracle.owner_layer(l, 2, 2) for l in range(12)] == [0, 1, 2, 2, 4, 4, 6, 6, 8, 8, 10, 10]
+    got = [oracle.owner_layer(l, 4, 2) for l in range(12)]
+    assert got == [0, 1, 2, 2, 2, 2, 6, 6, 6, 6, 10, 10]
+    # Alg. 3's literal "l % 2" pairing is start = 0.
+    assert [oracle.owner_layer(l, 2, 0) for l in range(6)] == [0, 0, 2, 2, 4, 4]
+    assert [oracle.owner_layer(l, 1, 2) for l in range(5)] == list(range(5))
+
+
+@pytest.mark.parametrize("name", ["C1", "C2", "C3", "C4", "C5"])
+def test_workload_integers_follow_the_rules(name):
+    w = synth.get(name)
+    assert w.window == oracle.window_rows(w.T)
+    assert w.keep == oracle.keep_tokens(w.T, w.static_ratio, w.cluster)
+    C = -(-w.keep // w.cluster)
+    S = -(-C // w.fanout)
+    assert w.k_super == oracle.level1_keep(S, w.dynamic_ratio)
+    assert w.k_clusters == oracle.level2_keep(w.keep, w.dynamic_ratio, w.cluster, w.k_super * w.fanout)
+
+
+def test_workload_derived_sizes():
+    # cluster / super-cluster counts and owner-layer counts of the five workloads
+    exp = {"C1": (16, 4, 1), "C2": (64, 16, 7), "C3": (128, 16, 10), "C4": (307, 39, 10),
+           "C5": (512, 64, 10)}
+    for name, (C, S, n_own) in exp.items():
+        w = synth.get(name)
+        assert -(-w.keep // w.cluster) == C
+        assert -(-C // w.fanout) == S
+        owners = {oracle.owner_layer(l, w.share_period, w.share_start) for l in range(w.n_layers)}
+        assert len(owners) == n_own
+
+
+def test_hierarchy_ratios_match_table3():
+    # Table 3 (20% overall): level-1 keep ratio x level-2 keep ratio of the surviving clusters = 0.2
+    for r1, r2 in [(0.9, 0.22), (0.7, 0.28), (0.5, 0.40), (0.3, 0.67)]:
+        assert abs(r1 * r2 - 0.2) < 0.005
+    # Our level-2 budget is taken against the kept cache, so with half the coarse clusters kept the
+    # fine level keeps 0.2 / 0.5 = 0.4 of its candidates, up to rounding down to whole clusters.
+    C, f = 64, 4
+    k1 = oracle.level1_keep(C // f, 0.2)
+    k2 = oracle.level2_keep(C * 16, 0.2, 16, k1 * f)
+    assert k1 * f == C // 2 and 0 <= 0.4 * k1 * f - k2 < 1
+
+
+# ------------------------------------------------------------------------ static scoring (A2)
+def _rand_bits(shape, dtype, seed, scale=1.0):
+    return to_bits(rng(seed).standard_normal(shape) * scale, dtype)
+
+
+def _torch_scores(qw, k, sm, causal):
+    """Brute force: dense masked softmax with torch (fp64), column sums over rows and heads."""
+    q = torch.from_numpy(qw)  # [G][W][d]
+    kk = torch.from_numpy(k)  # [T][d]
+    G, W, _ = q.shape
+    T = kk.shape[0]
+    s = sm * (q @ kk.T)  # [G][W][T]
+    if causal:
+        pos = torch.arange(T - W, T).view(W, 1)
+        s = s.masked_fill(torch.arange(T).view(1, T) > pos, float("-inf"))
+    return torch.softmax(s, dim=-1).sum(dim=(0, 1)).numpy()
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16", "fp16"])
+@pytest.mark.parametrize("causal", [True, False])
+def test_token_scores_brute_force(dtype, causal):
+    G, W, T, d = 3, 5, 17, 8
+    qw = _rand_bits((G, W, d), dtype, 1)
+    k = _rand_bits((T, d), dtype, 2)
+    sm = 0.35
+    got = oracle.token_scores(qw, k, dtype, sm, causal)
+    ref = _torch_scores(from_bits(qw, dtype), from_bits(k, dtype), float(np.float32(sm)), causal)
+    np.testing.assert_allclose(got, ref, rtol=1e-12, atol=1e-15)
+
+
+def test_token_scores_rows_sum_to_one():
+    G, W, T, d = 2, 9, 40, 16
+    qw = _rand_bits((G, W, d), "bf16", 3, 2.0)
+    k = _rand_bits((T, d), "bf16", 4, 2.0)
+    got = oracle.token_scores(qw, k, "bf16", 1 / 4, True)
+    assert abs(got.sum() - G * W) < 1e-12 * G * W
+    assert np.all(got[:T - W + 1] > 0)
+
+
+def test_token_scores_uniform_keys_closed_form():
+    # Identical keys: every causal row is uniform over its prefix, p = 1/(pos+1).
+    G, W, T, d = 2, 4, 10, 4
+    qw = _rand_bits((G, W, d), "fp32", 5)
+    k = np.tile(np.float32([0.5, -1.0, 2.0, 0.25]), (T, 1))
+    got = oracle.token_scores(qw, k, "fp32", 0.5, True)
+    exp = []
+    for j in range(T):
+        s = sum(Fraction(1, p + 1) for p in range(T - W, T) if p >= j)
+        exp.append(float(G * s))
+    np.testing.assert_allclose(got, exp, rtol=1e-13)
+    # non-causal: uniform over all T keys
+    got_nc = oracle.token_scores(qw, k, "fp32", 0.5, False)
+    np.testing.assert_allclose(got_nc, np.full(T, G * W / T), rtol=1e-13)
+
+
+def test_token_scores_dominant_key_takes_all_mass():
+    G, W, T, d = 1, 3, 12, 4
+    q = np.float32([1, 0, 0, 0])
+    qw = np.tile(q, (G, W, 1)).astype(np.float32)
+    k = _rand_bits((T, d), "fp32", 6, 0.1)
+    k[2] = np.float32([400, 0, 0, 0])
+    got = oracle.token_scores(qw, k, "fp32", 1.0, True)
+    assert abs(got[2] - G * W) < 1e-9
+    assert got.sum() - got[2] < 1e-9
+
+
+def test_token_scores_scale_invariance():
+    # scaling q by 2 and the softmax scale by 1/2 leaves the scores unchanged (catches a dropped
+    # or doubly applied scale)
+    G, W, T, d = 2, 3, 9, 4
+    qw = _rand_bits((G, W, d), "fp32", 7)
+    k = _rand_bits((T, d), "fp32", 8)
+    a = oracle.token_scores(qw, k, "fp32", 0.5, True)
+    b = oracle.token_scores((qw * 2).astype(np.float32), k, "fp32", 0.25, True)
+    np.testing.assert_allclose(a, b, rtol=1e-13)
+
+
+def test_row_lse_matches_torch():
+    G, W, T, d = 1, 6, 30, 8
+    qw = _rand_bits((G, W, d), "bf16", 9)
+    k = _rand_bits((T, d), "bf16", 10)
+    _, lse = oracle.token_scores(qw, k, "bf16", 0.3, True, with_lse=True)
+    qf, kf = from_bits(qw, "bf16"), from_bits(k, "bf16")
+    sm = float(np.float32(0.3))
+    for t in range(W):
+        n = T - W + t + 1
+        ref = torch.logsumexp(torch.from_numpy(sm * kf[:n] @ qf[0, t]), 0).item()
+        assert abs(lse[0, t] - ref) < 1e-12
+        assert abs(oracle.row_lse(qw[0, t], t, W, k, "bf16", 0.3) - ref) < 1e-12
+
+
+# ------------------------------------------------------------------------ static top-k
+def _lexsort_topk(score, k):
+    order = np.lexsort((np.arange(len(score)), -np.asarray(score)))
+    return order[:k]
+
+
+def test_static_topk_matches_lexsort_with_ties():
+    r = rng(11)
+    for T, keep, local in [(50, 20, 5), (64, 64, 8), (33, 10, 0), (40, 6, 10)]:
+        score = r.integers(0, 6, T).astype(np.float64)  # many ties
+        kept = oracle.static_topk(score, keep, local)
+        loc = min(local, keep)
+        exp = np.sort(np.concatenate([_lexsort_topk(score[:T - loc], keep - loc), np.arange(T - loc, T)]))
+        np.testing.assert_array_equal(kept, exp)
+        assert np.all(np.diff(kept) > 0)
+
+
+def test_static_topk_identity_and_equal_scores():
+    np.testing.assert_array_equal(oracle.static_topk(np.ones(16), 16, 4), np.arange(16))
+    # all equal: lowest indices first, plus the recent window
+    np.testing.assert_array_equal(oracle.static_topk(np.zeros(20), 6, 2), [0, 1, 2, 3, 18, 19])
+
+
+# ------------------------------------------------------------------------ clusters (A3, A4)
+def test_cluster_bounds_match_numpy_with_partial_tail():
+    k = _rand_bits((37, 8), "bf16", 12)
+    kf = from_bits(k, "bf16")
+    for first, count in [(0, 16), (16, 16), (32, 16)]:
+        rmax, rmin = oracle.cluster_bounds(k, "bf16", first, count)
+        np.testing.assert_array_equal(rmax, kf[first:first + count].max(0))
+        np.testing.assert_array_equal(rmin, kf[first:first + count].min(0))
+
+
+def test_centroid_fp32_rounding_and_alpha_limits():
+    r = rng(13)
+    vals = from_bits(to_bits(r.standard_normal((500, 2)) * 10, "bf16"), "bf16")
+    for a in (0.6, 0.3, 0.9):
+        a32 = np.float32(a)
+        b32 = np.float32(1) - a32
+        for rmax, rmin in vals:
+            exp = np.float32(a32 * np.float32(rmax)) + np.float32(b32 * np.float32(rmin))
+            assert np.float32(oracle.centroid(rmax, rmin, a)) == np.float32(exp)
+    for rmax, rmin in vals[:50]:
+        assert oracle.centroid(rmax, rmin, 1.0) == np.float32(rmax)  # alpha = 1 -> r^max
+        assert oracle.centroid(rmax, rmin, 0.0) == np.float32(rmin)  # alpha = 0 -> r^min
+
+
+def test_super_bounds_equal_member_bounds():
+    L, B, H, Ts, d, s, f = 1, 1, 2, 80, 8, 8, 3     # C = 10, S = 4 with a tail of 1
+    k = _rand_bits((L, B, H, Ts, d), "fp16", 14)
+    cent, scent = oracle.build_clusters(k, "fp16", cluster=s, fanout=f, alpha=1.0)
+    kf = from_bits(k, "fp16")
+    C = 10
+    assert cent.shape[3] == C and scent.shape[3] == 4
+    for h in range(H):
+        cmax = np.stack([kf[0, 0, h, c * s:(c + 1) * s].max(0) for c in range(C)])
+        np.testing.assert_array_equal(cent[0, 0, h], cmax.astype(np.float32))
+        for sc in range(4):
+            np.testing.assert_array_equal(scent[0, 0, h, sc], cmax[sc * f:(sc + 1) * f].max(0).astype(np.float32))
+
+
+def test_linear_score_below_mp_bound_above_true_max():
+    # Eq. 2 and the linearisation: for alpha in [0,1], sum q_i (a r^max + (1-a) r^min) <=
+    # sum max(q_i r^max, q_i r^min) >= max_k q.k
+    r = rng(15)
+    for trial in range(50):
+        d, s = 16, 8
+        kf = from_bits(to_bits(r.standard_normal((s, d)) * 3, "bf16"), "bf16")
+        q = to_bits(r.standard_normal((1, d)), "bf16")
+        qf = from_bits(q, "bf16")[0]
+        rmax, rmin = kf.max(0), kf.min(0)
+        cent = np.float32([oracle.centroid(a, b, 0.6) for a, b in zip(rmax, rmin)])
+        lin = oracle.cluster_scores(q, cent[None], "bf16")[0]
+        mp = oracle.mp_bound(qf, rmax, rmin)
+        true_max = (kf @ qf).max()
+        tol = 1e-6 * np.abs(qf) @ np.maximum(np.abs(rmax), np.abs(rmin))
+        assert lin <= mp + tol
+        assert mp >= true_max - 1e-12
+
+
+def test_unit_cluster_score_is_dot_product():
+    # s = 1, alpha = 1: the representative is the key itself, the score is q.k (exact in fp64)
+    r = rng(16)
+    k = to_bits(r.standard_normal((20, 8)), "bf16")
+    q = to_bits(r.standard_normal((2, 8)), "bf16")
+    cent = np.float32([[oracle.centroid(x, x, 1.0) for x in row] for row in from_bits(k, "bf16")])
+    got = oracle.cluster_scores(q, cent, "bf16")
+    exp = from_bits(k, "bf16") @ from_bits(q, "bf16").sum(0)
+    np.testing.assert_array_equal(got, exp)
+
+
+# ------------------------------------------------------------------------ selection (A5-A7)
+def test_topk_matches_lexsort():
+    r = rng(17)
+    s = r.integers(0, 4, 30).astype(np.float64)
+    np.testing.assert_array_equal(oracle.topk(s, 12), _lexsort_topk(s, 12))
+
+
+def _select_case(seed, L=6, B=1, Hq=4, Hkv=2, Ts=200, d=16, s=8, f=4, dtype="bf16"):
+    r = rng(seed)
+    k = to_bits(r.standard_normal((L, B, Hkv, Ts, d)), dtype)
+    q = to_bits(r.standard_normal((L, B, Hq, d)), dtype)
+    cent, scent = oracle.build_clusters(k, dtype, cluster=s, fanout=f)
+    return k, q, cent, scent
+
+
+def test_full_budget_selects_every_cluster():
+    k, q, cent, scent = _select_case(18, Ts=200, s=8, f=4)  # C = 25, S = 7 (tail 1)
+    sel, _ = oracle.select_clusters(q, cent, scent, "bf16", Ts=200, cluster=8, fanout=4, k_super=7,
+                                    k_clusters=25)
+    assert np.all(sel == np.arange(25))
+
+
+def test_hierarchical_selection_matches_independent_ranking():
+    Ts, s, f, ks, kc = 200, 8, 4, 3, 5
+    k, q, cent, scent = _select_case(19, Ts=Ts, s=s, f=f)
+    sel, score = oracle.select_clusters(q, cent, scent, "bf16", Ts=Ts, cluster=s, fanout=f, k_super=ks,
+                                        k_clusters=kc)
+    G = 2
+    qf = from_bits(q, "bf16")
+    C = 25
+    for l in range(q.shape[0]):
+        for h in range(2):
+            qs = qf[l, 0, h * G:(h + 1) * G].sum(0)
+            s1 = scent[l, 0, h].astype(np.float64) @ qs
+            sup = np.sort(_lexsort_topk(s1, ks))
+            cand = np.array([c for x in sup for c in range(x * f, min(C, (x + 1) * f))])
+            s2 = cent[l, 0, h, cand].astype(np.float64) @ qs
+            exp = np.sort(cand[_lexsort_topk(s2, kc)])
+            np.testing.assert_array_equal(sel[l, 0, h], exp)
+            np.testing.assert_allclose(score[l, 0, h], cent[l, 0, h, exp].astype(np.float64) @ qs, rtol=1e-12)
+
+
+def test_index_sharing_copies_owner_selection():
+    Ts, s, f = 200, 8, 4
+    k, q, cent, scent = _select_case(20, L=8, Ts=Ts, s=s, f=f)
+    kw = dict(Ts=Ts, cluster=s, fanout=f, k_super=3, k_clusters=4)
+    shared, _ = oracle.select_clusters(q, cent, scent, "bf16", share_period=2, **kw)
+    alone, _ = oracle.select_clusters(q, cent, scent, "bf16", share_period=1, **kw)
+    for l in range(8):
+        o = oracle.owner_layer(l, 2, 2)
+        np.testing.assert_array_equal(shared[l], alone[o])
+    # owners outside the block: the caller's selection is kept
+    prev = np.full((3, 1, 2, 4), 7, np.int32)
+    sel, _ = oracle.select_clusters(q[3:6], cent[3:6], scent[3:6], "bf16", layer0=3, share_period=2,
+                                    sel_in=prev, **kw)
+    assert np.all(sel[0] == 7)                      # layer 3's owner is layer 2
+    np.testing.assert_array_equal(sel[1], alone[4])  # layer 4 owns
+    np.testing.assert_array_equal(sel[2], alone[4])  # layer 5 follows layer 4
+
+
+# ------------------------------------------------------------------------ attention (A9, A12)
+def _sdpa(q, k, v, sm):
+    """torch scaled_dot_product_attention in fp64 on the CPU: q [d], k/v [n][d]."""
+    out = torch.nn.functional.scaled_dot_product_attention(
+        torch.from_numpy(q)[None, None, None], torch.from_numpy(k)[None, None],
+        torch.from_numpy(v)[None, None], scale=sm)
+    return out[0, 0, 0].numpy()
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "fp16", "bf16"])
+def test_full_budget_sparse_equals_dense_equals_sdpa(dtype):
+    L, B, Hq, Hkv, Ts, d, s = 2, 1, 4, 2, 40, 8, 8   # C = 5
+    r = rng(21)
+    k = to_bits(r.standard_normal((L, B, Hkv, Ts, d)), dtype)
+    v = to_bits(r.standard_normal((L, B, Hkv, Ts, d)), dtype)
+    q = to_bits(r.standard_normal((L, B, Hq, d)), dtype)
+    sm = 1 / np.sqrt(d)
+    sel = np.tile(np.arange(5, dtype=np.int32), (L, B, Hkv, 1))
+    sp, lse_s = oracle.sparse_decode_attn(q, k, v, sel, dtype, cluster=s, sm_scale=sm)
+    dn, lse_d = oracle.dense_decode_attn(q, k, v, dtype, sm_scale=sm)
+    np.testing.assert_allclose(sp, dn, rtol=1e-13, atol=1e-14)
+    np.testing.assert_allclose(lse_s, lse_d, rtol=1e-13)
+    sm32 = float(np.float32(sm))
+    qf, kf, vf = (from_bits(x, dtype) for x in (q, k, v))
+    for l in range(L):
+        for h in range(Hq):
+            ref = _sdpa(qf[l, 0, h], kf[l, 0, h // 2], vf[l, 0, h // 2], sm32)
+            np.testing.assert_allclose(dn[l, 0, h], ref, rtol=1e-12, atol=1e-13)
+            lref = torch.logsumexp(torch.from_numpy(sm32 * kf[l, 0, h // 2] @ qf[l, 0, h]), 0).item()
+            assert abs(lse_d[l, 0, h] - lref) < 1e-12
+
+
+def test_sparse_attention_gathers_selected_clusters_with_partial_tail():
+    L, B, Hq, Hkv, Ts, d, s = 1, 1, 2, 1, 45, 8, 8   # C = 6, last cluster has 5 tokens
+    r = rng(22)
+    k = to_bits(r.standard_normal((L, B, Hkv, Ts, d)), "bf16")
+    v = to_bits(r.standard_normal((L, B, Hkv, Ts, d)), "bf16")
+    q = to_bits(r.standard_normal((L, B, Hq, d)), "bf16")
+    sel = np.array([[[[1, 3, 5]]]], np.int32)
+    out, _ = oracle.sparse_decode_attn(q, k, v, sel, "bf16", cluster=s, sm_scale=0.3)
+    rows = list(range(8, 16)) + list(range(24, 32)) + list(range(40, 45))
+    qf, kf, vf = (from_bits(x, "bf16") for x in (q, k, v))
+    for h in range(Hq):
+        ref = _sdpa(qf[0, 0, h], kf[0, 0, 0, rows], vf[0, 0, 0, rows], float(np.float32(0.3)))
+        np.testing.assert_allclose(out[0, 0, h], ref, rtol=1e-12, atol=1e-13)
+
+
+# ------------------------------------------------------------------------ whole static eviction
+def test_static_evict_identity_sharing_and_gather():
+    L, B, Hq, Hkv, T, W, d = 4, 1, 4, 2, 48, 9, 8
+    r = rng(23)
+    qw = to_bits(r.standard_normal((L, B, Hq, W, d)), "bf16")
+    k = to_bits(r.standard_normal((L, B, Hkv, T, d)), "bf16")
+    v = to_bits(r.standard_normal((L, B, Hkv, T, d)), "bf16")
+    kept, ko, vo = oracle.static_evict(qw, k, v, "bf16", keep=T, local_keep=4, sm_scale=0.35)
+    assert np.all(kept == np.arange(T))
+    np.testing.assert_array_equal(ko, k)
+    kept, ko, vo, sc = oracle.static_evict(qw, k, v, "bf16", keep=20, local_keep=4, sm_scale=0.35,
+                                           share_period=2, with_scores=True)
+    for l in range(L):
+        o = oracle.owner_layer(l, 2, 2)
+        np.testing.assert_array_equal(kept[l], kept[o])
+        for h in range(Hkv):
+            np.testing.assert_array_equal(ko[l, 0, h], k[l, 0, h, kept[l, 0, h]])
+            np.testing.assert_array_equal(vo[l, 0, h], v[l, 0, h, kept[l, 0, h]])
+    # owner layers: kept = recent window + best scores by lexsort
+    for l in (0, 1, 2):
+        for h in range(Hkv):
+            exp = np.sort(np.concatenate([_lexsort_topk(sc[l, 0, h, :T - 4], 16), np.arange(T - 4, T)]))
+            np.testing.assert_array_equal(kept[l, 0, h], exp)
+            assert abs(sc[l, 0, h].sum() - 2 * W) < 1e-11
+
+
+def test_planted_tokens_survive_static_eviction_tiny():
+    # Sanity on the tiny workload: sinks and heavy hitters are the most attended tokens.
+    w = synth.get("C1")
+    qw, k, v = synth.prefill_host(w, 0)
+    kept, _, _ = oracle.static_evict(qw[None], k[None], v[None], w.dtype, keep=w.keep,
+                                     local_keep=w.local_keep, sm_scale=float(1 / np.sqrt(w.head_dim)))
+    sp = synth.spec(w)
+    for h in range(w.n_kv_heads):
+        ks = set(kept[0, 0, h].tolist())
+        assert {0, 1, 2, 3} <= ks
+        hh = synth.hh_starts(sp, 0, 0, h)
+        assert sum(int(x) in ks for x in hh) >= 14
