@@ -1,0 +1,157 @@
+/* mpcache.h — C ABI of the MI355X (gfx950) MPCache hot path.
+ *
+ * Paper: "MPCache: MPC-Friendly KV Cache Eviction for Efficient Private LLM Inference",
+ * arXiv 2501.06807. The library computes, in plaintext, the data-parallel steps of the method:
+ *   - look-once static eviction at prefill (Sec. 3.2; Alg. 3 step 1);
+ *   - hierarchical cluster representatives alpha*r^max + (1-alpha)*r^min (Sec. 3.3, Eq. "sim");
+ *   - query-aware two-level cluster selection with cross-layer index sharing (Sec. 3.3, 3.4;
+ *     Alg. 3 step 2);
+ *   - gather + softmax attention over the selected clusters (Alg. 1 steps 3-4).
+ *
+ * Conventions shared by every entry point
+ *   - Tensor arguments are DEVICE pointers owned by the caller, contiguous row-major, with
+ *     16-byte aligned bases. Element type is `dims->dtype` unless a float/int32 type is stated.
+ *   - Shapes use: B batch, L = dims->n_layers (a block of consecutive layers starting at the
+ *     absolute layer dims->layer0), Hq / Hkv query / kv heads (q-head h reads kv-head h / G,
+ *     G = Hq / Hkv), d head dim, T prompt tokens, W window rows, Ts kept tokens,
+ *     s cluster size, C = ceil(Ts / s) clusters, f fan-out, S = ceil(C / f) super-clusters.
+ *   - Cross-layer sharing: owner(l) = l if period <= 1 or l < start, else
+ *     start + period * floor((l - start) / period), on absolute layer indices (Sec. 3.4: the
+ *     first two layers never share, so start = 2 follows the paper's text; start = 0 gives the
+ *     pairing of Alg. 3).
+ *   - The library allocates nothing and keeps no global state except a thread-local message for
+ *     the last error. Scratch memory is a caller-provided workspace of mpc_workspace_bytes()
+ *     bytes; it must be zero-filled once before its first use, and every completed call leaves
+ *     the parts that must start at zero zeroed again. Calls that share one workspace must not
+ *     overlap in time.
+ *   - Every call is asynchronous on `stream` (a hipStream_t; NULL = default stream). The
+ *     returned status covers argument validation and launch errors only; it never waits for the
+ *     GPU. On any status other than MPC_OK nothing has been enqueued.
+ *   - Supported: d in {64, 128}; G in {1, 2, 4, 8}; dtype fp32 / fp16 / bf16.
+ */
+#ifndef MPCACHE_H
+#define MPCACHE_H
+#include <stddef.h>
+#include <stdint.h>
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MPC_OK = 0,
+  MPC_EINVAL = 1,       /* null pointer, non-positive size, bad enum value                  */
+  MPC_ESHAPE = 2,       /* sizes inconsistent with each other (e.g. Hq % Hkv, k > candidates) */
+  MPC_EUNSUPPORTED = 3, /* valid but outside what the kernels implement (head dim, group)    */
+  MPC_EWORKSPACE = 4,   /* workspace missing or smaller than mpc_workspace_bytes()           */
+  MPC_EHIP = 5          /* a HIP launch failed                                              */
+} mpc_status;
+
+typedef enum { MPC_FP32 = 0, MPC_FP16 = 1, MPC_BF16 = 2 } mpc_dtype;
+
+typedef struct {
+  int32_t batch;      /* B                                                */
+  int32_t layer0;     /* absolute index of the first layer of the block   */
+  int32_t n_layers;   /* L, layers in this call                           */
+  int32_t n_q_heads;  /* Hq                                               */
+  int32_t n_kv_heads; /* Hkv                                              */
+  int32_t head_dim;   /* d                                                */
+  int32_t dtype;      /* mpc_dtype of q / k / v / out                     */
+} mpc_dims;
+
+typedef struct {
+  int32_t cluster_size; /* s: tokens per fine cluster                                        */
+  int32_t fanout;       /* f: fine clusters per super-cluster                                */
+  int32_t k_super;      /* level-1 budget, 1 <= k_super <= S                                  */
+  int32_t k_clusters;   /* level-2 budget; must not exceed the smallest possible candidate set */
+  float alpha;          /* weight of r^max in the representative (the paper uses 0.6)        */
+  int32_t share_period; /* layers per shared selection (1 = no sharing)                     */
+  int32_t share_start;  /* first layer that may share (2 in the paper)                       */
+} mpc_select_cfg;
+
+typedef struct {
+  int32_t window;       /* W: window query rows (positions T-W .. T-1)                        */
+  int32_t keep;         /* Ts: tokens kept per (layer, sequence, kv head)                      */
+  int32_t local_keep;   /* most recent tokens always kept (part of `keep`)                    */
+  float sm_scale;       /* softmax scale of the window attention (1/sqrt(d))                  */
+  int32_t causal;       /* 1: window row t attends to keys j <= T-W+t                          */
+  int32_t share_period; /* layers sharing one kept set (same rule as the selection)           */
+  int32_t share_start;
+} mpc_evict_cfg;
+
+enum { MPC_OP_STATIC_EVICT = 0, MPC_OP_SELECT = 1, MPC_OP_DECODE_ATTN = 2 };
+
+/* Workspace bytes needed by `op` (MPC_OP_*) for these dims. `T_or_Ts` is T for static eviction
+ * and Ts otherwise; `cfg` points to the op's config struct (mpc_evict_cfg / mpc_select_cfg) or is
+ * NULL for MPC_OP_DECODE_ATTN. Returns 0 when the op needs no workspace or the arguments are
+ * invalid. */
+size_t mpc_workspace_bytes(int32_t op, const mpc_dims* dims, int32_t T_or_Ts, const void* cfg);
+
+/* Look-once static eviction (Sec. 3.2; Alg. 3 step 1; window rule of App. F).
+ * For every owner layer and (b, kv head): score[j] = sum over the G query heads of the group and
+ * the W window rows t of softmax_j(sm_scale * q_t . k_j) (causal: j <= T-W+t); keep the last
+ * `local_keep` tokens plus the (keep - local_keep) best-scored older tokens (ties: lower position
+ * first); write the kept positions ascending. Non-owner layers reuse their owner's kept set; a
+ * layer whose owner precedes layer0 must arrive with that set already in `kept_idx`. Every layer
+ * then gathers its kept K/V rows.
+ *   q_win       [L][B][Hq][W][d]   window queries (read for owner layers only)
+ *   k, v        [L][B][Hkv][T][d]  prompt cache
+ *   kept_idx    [L][B][Hkv][keep]  int32 out (in for layers owned before layer0)
+ *   k_out,v_out [L][B][Hkv][keep][d] out
+ *   token_score [L][B][Hkv][T] float, optional out (NULL = not returned); owner layers only
+ *   row_lse     [L][B][Hq][W] float, optional out: natural log-sum-exp of each window row's
+ *               scaled scores (the softmax normaliser); owner layers only
+ *   ws          workspace of mpc_workspace_bytes(MPC_OP_STATIC_EVICT, dims, T, cfg) bytes.
+ * Accumulation: fp32 tensor-core dot products, softmax statistics and sums in fp64. */
+mpc_status mpc_static_evict(const mpc_dims* dims, int32_t T, const mpc_evict_cfg* cfg,
+                            const void* q_win, const void* k, const void* v, int32_t* kept_idx,
+                            void* k_out, void* v_out, float* token_score, float* row_lse,
+                            void* ws, size_t ws_bytes, void* stream);
+
+/* Cluster representatives (Sec. 3.3: r^max / r^min under Eq. 1, reordered form Eq. "sim";
+ * hierarchy of Sec. 3.3 / App. F). Fine cluster c covers kept tokens [c*s, min((c+1)*s, Ts));
+ * super-cluster u covers fine clusters [u*f, min((u+1)*f, C)). Each representative is
+ * fp32( fp32(alpha * r^max) + fp32((1-alpha)_fp32 * r^min) ) per channel. Owner layers only.
+ *   k_cache [L][B][Hkv][Ts][d];  cent [L][B][Hkv][C][d] float out;  scent [L][B][Hkv][S][d] float out */
+mpc_status mpc_build_clusters(const mpc_dims* dims, int32_t Ts, const mpc_select_cfg* cfg,
+                              const void* k_cache, float* cent, float* scent, void* stream);
+
+/* Query-aware dynamic selection of one decode step (Sec. 3.3; Alg. 3 step 2).
+ * Score of a representative c for kv head h: sum over the group's q-heads g and channels i of
+ * q_{g,i} * c_i, accumulated in fp64. Level 1 keeps the k_super best super-clusters, level 2 the
+ * k_clusters best fine clusters among their members (ties: lower index first); the selection is
+ * written in ascending cluster order. Non-owner layers receive their owner's selection; a layer
+ * whose owner precedes layer0 is left untouched (the caller copies it).
+ *   q [L][B][Hq][d];  cent / scent as produced by mpc_build_clusters;
+ *   sel [L][B][Hkv][k_clusters] int32 out;  sel_score same shape, float, optional (score rounded
+ *   to fp32). ws may be NULL (no workspace needed). Limits: S <= 1024, k_super * f <= 2048. */
+mpc_status mpc_select_clusters(const mpc_dims* dims, int32_t Ts, const mpc_select_cfg* cfg,
+                               const void* q, const float* cent, const float* scent,
+                               int32_t* sel, float* sel_score, void* ws, size_t ws_bytes,
+                               void* stream);
+
+/* Sparse attention over the selected clusters (Alg. 1 steps 3-4; Alg. 3 step 2):
+ * o_h = softmax(sm_scale * q_h K'^T) V' with K', V' the kept-cache rows of the clusters in
+ * sel[l][b][h / G] (tokens past Ts in a partial last cluster are skipped).
+ *   q [L][B][Hq][d];  k_cache, v_cache [L][B][Hkv][Ts][d];  sel [L][B][Hkv][k_clusters] int32
+ *   (every entry in [0, C));  out [L][B][Hq][d] (dtype);  lse [L][B][Hq] float, optional
+ *   (natural-log log-sum-exp of the scaled scores). fp32 accumulation.
+ *   ws: mpc_workspace_bytes(MPC_OP_DECODE_ATTN, dims, Ts, NULL) bytes (split-K partials and
+ *   counters); may be NULL when that is 0. */
+mpc_status mpc_sparse_decode_attn(const mpc_dims* dims, int32_t Ts, int32_t cluster_size,
+                                  const void* q, const void* k_cache, const void* v_cache,
+                                  const int32_t* sel, int32_t k_clusters, float sm_scale,
+                                  void* out, float* lse, void* ws, size_t ws_bytes, void* stream);
+
+/* Owner layer of absolute layer `l` under the sharing rule above. */
+int32_t mpc_owner_layer(int32_t l, int32_t period, int32_t start);
+
+/* Static text for a status code. */
+const char* mpc_status_string(mpc_status s);
+
+/* Human-readable reason of the last failed call on this thread ("" if none). */
+const char* mpc_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,168 @@
+"""ctypes binding of libmpcache.so: the four entry points of the C ABI with the same names.
+
+Argument marshalling only: shapes are read off torch CUDA tensors, pointers and the current
+stream are handed to the library, and a non-zero status raises MpcError. Every step of the path
+runs in the HIP kernels; there is no fallback.
+"""
+import ctypes
+import os
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libmpcache.so")
+
+MPC_OK, MPC_EINVAL, MPC_ESHAPE, MPC_EUNSUPPORTED, MPC_EWORKSPACE, MPC_EHIP = range(6)
+MPC_OP_STATIC_EVICT, MPC_OP_SELECT, MPC_OP_DECODE_ATTN = range(3)
+DTYPE_CODE = {torch.float32: 0, torch.float16: 1, torch.bfloat16: 2}
+
+
+class MpcDims(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in
+                ("batch", "layer0", "n_layers", "n_q_heads", "n_kv_heads", "head_dim", "dtype")]
+
+
+class MpcSelectCfg(ctypes.Structure):
+    _fields_ = [("cluster_size", ctypes.c_int32), ("fanout", ctypes.c_int32),
+                ("k_super", ctypes.c_int32), ("k_clusters", ctypes.c_int32),
+                ("alpha", ctypes.c_float), ("share_period", ctypes.c_int32),
+                ("share_start", ctypes.c_int32)]
+
+
+class MpcEvictCfg(ctypes.Structure):
+    _fields_ = [("window", ctypes.c_int32), ("keep", ctypes.c_int32),
+                ("local_keep", ctypes.c_int32), ("sm_scale", ctypes.c_float),
+                ("causal", ctypes.c_int32), ("share_period", ctypes.c_int32),
+                ("share_start", ctypes.c_int32)]
+
+
+class MpcError(RuntimeError):
+    def __init__(self, fn, status, msg):
+        super().__init__(f"{fn}: status {status} ({msg})")
+        self.status = status
+
+
+_LIB = None
+EXPORTS = ("mpc_workspace_bytes", "mpc_static_evict", "mpc_build_clusters", "mpc_select_clusters",
+           "mpc_sparse_decode_attn", "mpc_owner_layer", "mpc_status_string", "mpc_last_error")
+
+
+def lib():
+    """Loads libmpcache.so; raises if it has not been built (no fallback path exists)."""
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build()")
+        L = ctypes.CDLL(LIB_PATH)
+        P, V, I, F = ctypes.POINTER, ctypes.c_void_p, ctypes.c_int32, ctypes.c_float
+        L.mpc_workspace_bytes.argtypes = [I, P(MpcDims), I, V]
+        L.mpc_workspace_bytes.restype = ctypes.c_size_t
+        L.mpc_static_evict.argtypes = [P(MpcDims), I, P(MpcEvictCfg)] + [V] * 8 + [V, ctypes.c_size_t, V]
+        L.mpc_build_clusters.argtypes = [P(MpcDims), I, P(MpcSelectCfg), V, V, V, V]
+        L.mpc_select_clusters.argtypes = [P(MpcDims), I, P(MpcSelectCfg)] + [V] * 5 + [V, ctypes.c_size_t, V]
+        L.mpc_sparse_decode_attn.argtypes = [P(MpcDims), I, I, V, V, V, V, I, F, V, V, V, ctypes.c_size_t, V]
+        for fn in ("mpc_static_evict", "mpc_build_clusters", "mpc_select_clusters", "mpc_sparse_decode_attn"):
+            getattr(L, fn).restype = ctypes.c_int
+        L.mpc_owner_layer.argtypes = [I, I, I]
+        L.mpc_owner_layer.restype = I
+        L.mpc_status_string.argtypes = [ctypes.c_int]
+        L.mpc_status_string.restype = ctypes.c_char_p
+        L.mpc_last_error.argtypes = []
+        L.mpc_last_error.restype = ctypes.c_char_p
+        _LIB = L
+    return _LIB
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _check(fn, status):
+    if status != MPC_OK:
+        raise MpcError(fn, status, lib().mpc_last_error().decode())
+
+
+def dims_of(q_like, kv, layer0=0):
+    """mpc_dims from a query-like tensor [L][B][Hq][..][d] and a cache [L][B][Hkv][..][d]."""
+    if kv.dtype not in DTYPE_CODE:
+        raise TypeError(f"unsupported dtype {kv.dtype}")
+    return MpcDims(batch=kv.shape[1], layer0=layer0, n_layers=kv.shape[0], n_q_heads=q_like.shape[2],
+                   n_kv_heads=kv.shape[2], head_dim=kv.shape[-1], dtype=DTYPE_CODE[kv.dtype])
+
+
+def _contig(*ts):
+    for t in ts:
+        if t is not None and not (t.is_cuda and t.is_contiguous()):
+            raise ValueError("tensors must be contiguous CUDA tensors")
+
+
+def owner_layer(layer, period, start=2):
+    return lib().mpc_owner_layer(layer, period, start)
+
+
+def workspace_bytes(op, dims, T_or_Ts, cfg=None):
+    c = None if cfg is None else ctypes.byref(cfg)
+    return lib().mpc_workspace_bytes(op, ctypes.byref(dims), T_or_Ts, c)
+
+
+def workspace(nbytes, device="cuda"):
+    """A zero-filled workspace buffer (the counters in it must start at zero)."""
+    return torch.zeros(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+
+
+def mpc_static_evict(q_win, k, v, kept_idx, k_out, v_out, *, keep, local_keep, sm_scale, causal=True,
+                     layer0=0, share_period=1, share_start=2, token_score=None, row_lse=None, ws=None,
+                     stream=None):
+    """q_win [L][B][Hq][W][d], k/v [L][B][Hkv][T][d] -> kept_idx [L][B][Hkv][keep], k_out/v_out."""
+    _contig(q_win, k, v, kept_idx, k_out, v_out, token_score, row_lse, ws)
+    dims = dims_of(q_win, k, layer0)
+    T, W = k.shape[3], q_win.shape[3]
+    cfg = MpcEvictCfg(window=W, keep=keep, local_keep=local_keep, sm_scale=sm_scale, causal=int(causal),
+                      share_period=share_period, share_start=share_start)
+    if ws is None:
+        ws = workspace(workspace_bytes(MPC_OP_STATIC_EVICT, dims, T, cfg), k.device)
+    _check("mpc_static_evict", lib().mpc_static_evict(
+        ctypes.byref(dims), T, ctypes.byref(cfg), _ptr(q_win), _ptr(k), _ptr(v), _ptr(kept_idx), _ptr(k_out),
+        _ptr(v_out), _ptr(token_score), _ptr(row_lse), _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def select_cfg(cluster, fanout, k_super, k_clusters, alpha=0.6, share_period=1, share_start=2):
+    return MpcSelectCfg(cluster_size=cluster, fanout=fanout, k_super=k_super, k_clusters=k_clusters,
+                        alpha=alpha, share_period=share_period, share_start=share_start)
+
+
+def mpc_build_clusters(k_cache, cent, scent, cfg, *, layer0=0, stream=None):
+    """k_cache [L][B][Hkv][Ts][d] -> cent [L][B][Hkv][C][d], scent [L][B][Hkv][S][d] (float32)."""
+    _contig(k_cache, cent, scent)
+    dims = dims_of(k_cache, k_cache, layer0)
+    _check("mpc_build_clusters", lib().mpc_build_clusters(
+        ctypes.byref(dims), k_cache.shape[3], ctypes.byref(cfg), _ptr(k_cache), _ptr(cent), _ptr(scent),
+        _stream(stream)))
+
+
+def mpc_select_clusters(q, cent, scent, sel, cfg, *, Ts, sel_score=None, layer0=0, stream=None):
+    """q [L][B][Hq][d] -> sel [L][B][Hkv][k_clusters] (int32, ascending)."""
+    _contig(q, cent, scent, sel, sel_score)
+    dims = dims_of(q, cent, layer0)
+    dims.dtype = DTYPE_CODE[q.dtype]
+    _check("mpc_select_clusters", lib().mpc_select_clusters(
+        ctypes.byref(dims), Ts, ctypes.byref(cfg), _ptr(q), _ptr(cent), _ptr(scent), _ptr(sel), _ptr(sel_score),
+        None, 0, _stream(stream)))
+
+
+def mpc_sparse_decode_attn(q, k_cache, v_cache, sel, out, *, cluster_size, sm_scale, lse=None, ws=None,
+                           layer0=0, stream=None):
+    """q [L][B][Hq][d], k/v [L][B][Hkv][Ts][d], sel [L][B][Hkv][k] -> out [L][B][Hq][d]."""
+    _contig(q, k_cache, v_cache, sel, out, lse, ws)
+    dims = dims_of(q, k_cache, layer0)
+    Ts = k_cache.shape[3]
+    if ws is None:
+        ws = workspace(workspace_bytes(MPC_OP_DECODE_ATTN, dims, Ts), q.device)
+    _check("mpc_sparse_decode_attn", lib().mpc_sparse_decode_attn(
+        ctypes.byref(dims), Ts, cluster_size, _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(sel), sel.shape[-1],
+        sm_scale, _ptr(out), _ptr(lse), _ptr(ws), ws.numel(), _stream(stream)))

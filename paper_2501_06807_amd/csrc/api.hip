@@ -1,0 +1,302 @@
+// C ABI of the MPCache hot path: argument validation, workspace layout, kernel dispatch.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+
+#include "clusters.h"
+#include "common.h"
+#include "decode_attn.h"
+#include "evict.h"
+#include "select.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+mpc_status fail(mpc_status s, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return s;
+}
+
+mpc_status ok() {
+  g_err[0] = '\0';
+  return MPC_OK;
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+int elt_size(int dtype) { return dtype == MPC_FP32 ? 4 : 2; }
+
+int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+mpc_status check_dims(const mpc_dims* d) {
+  if (!d) return fail(MPC_EINVAL, "dims is NULL");
+  if (d->batch <= 0 || d->n_layers <= 0 || d->layer0 < 0 || d->n_q_heads <= 0 ||
+      d->n_kv_heads <= 0 || d->head_dim <= 0)
+    return fail(MPC_EINVAL, "dims must be positive (layer0 >= 0)");
+  if (d->dtype < MPC_FP32 || d->dtype > MPC_BF16) return fail(MPC_EINVAL, "bad dtype %d", d->dtype);
+  if (d->n_q_heads % d->n_kv_heads)
+    return fail(MPC_ESHAPE, "n_q_heads %d not a multiple of n_kv_heads %d", d->n_q_heads, d->n_kv_heads);
+  if (d->head_dim != 64 && d->head_dim != 128)
+    return fail(MPC_EUNSUPPORTED, "head_dim %d not in {64, 128}", d->head_dim);
+  if ((int64_t)d->n_layers * d->batch * d->n_q_heads > (1 << 24))
+    return fail(MPC_EUNSUPPORTED, "too many (layer, sequence, head) units");
+  return MPC_OK;
+}
+
+mpc_status launched(hipError_t e, const char* what) {
+  if (e != hipSuccess) return fail(MPC_EHIP, "%s launch failed: %s", what, hipGetErrorString(e));
+  return MPC_OK;
+}
+
+// Static eviction workspace: fp64 row bias per window row, then fp32 token scores.
+struct EvictWs {
+  size_t rowstat, score, total;
+};
+EvictWs evict_ws(const mpc_dims* d, int T, int W) {
+  EvictWs w;
+  w.rowstat = 0;
+  w.score = align256((size_t)d->n_layers * d->batch * d->n_q_heads * W * sizeof(double));
+  w.total = w.score + align256((size_t)d->n_layers * d->batch * d->n_kv_heads * T * sizeof(float));
+  return w;
+}
+
+// Decode workspace: split-K partials sized for the largest split count, then counters.
+struct DecodeWs {
+  int splits_max;
+  size_t counters, total;
+};
+DecodeWs decode_ws(const mpc_dims* d) {
+  const int units = d->n_layers * d->batch * d->n_kv_heads;
+  const int G = d->n_q_heads / d->n_kv_heads;
+  DecodeWs w;
+  w.splits_max = mpc::decode_splits(units, 1 << 30, d->head_dim, elt_size(d->dtype));
+  if (w.splits_max <= 1) {
+    w.counters = w.total = 0;
+    return w;
+  }
+  w.counters = align256((size_t)units * w.splits_max * G * (d->head_dim + 2) * sizeof(float));
+  w.total = w.counters + align256((size_t)units * sizeof(int32_t));
+  return w;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* mpc_status_string(mpc_status s) {
+  switch (s) {
+    case MPC_OK: return "ok";
+    case MPC_EINVAL: return "invalid argument";
+    case MPC_ESHAPE: return "inconsistent shape";
+    case MPC_EUNSUPPORTED: return "unsupported configuration";
+    case MPC_EWORKSPACE: return "workspace too small";
+    case MPC_EHIP: return "HIP error";
+  }
+  return "unknown status";
+}
+
+const char* mpc_last_error(void) { return g_err; }
+
+int32_t mpc_owner_layer(int32_t l, int32_t period, int32_t start) {
+  return mpc::owner_layer(l, period, start);
+}
+
+size_t mpc_workspace_bytes(int32_t op, const mpc_dims* dims, int32_t T_or_Ts, const void* cfg) {
+  if (check_dims(dims) != MPC_OK || T_or_Ts <= 0) return 0;
+  if (op == MPC_OP_STATIC_EVICT) {
+    const mpc_evict_cfg* c = (const mpc_evict_cfg*)cfg;
+    if (!c || c->window <= 0 || c->window > T_or_Ts) return 0;
+    return evict_ws(dims, T_or_Ts, c->window).total;
+  }
+  if (op == MPC_OP_DECODE_ATTN) return decode_ws(dims).total;
+  return 0;
+}
+
+mpc_status mpc_static_evict(const mpc_dims* dims, int32_t T, const mpc_evict_cfg* cfg,
+                            const void* q_win, const void* k, const void* v, int32_t* kept_idx,
+                            void* k_out, void* v_out, float* token_score, float* row_lse,
+                            void* ws, size_t ws_bytes, void* stream) {
+  mpc_status s = check_dims(dims);
+  if (s != MPC_OK) return s;
+  if (!cfg) return fail(MPC_EINVAL, "cfg is NULL");
+  if (T <= 0) return fail(MPC_EINVAL, "T must be positive");
+  if (!q_win || !k || !v || !kept_idx || !k_out || !v_out)
+    return fail(MPC_EINVAL, "a required tensor pointer is NULL");
+  if (!aligned16(q_win) || !aligned16(k) || !aligned16(v) || !aligned16(k_out) || !aligned16(v_out))
+    return fail(MPC_EINVAL, "tensor bases must be 16-byte aligned");
+  if (cfg->window <= 0 || cfg->window > T) return fail(MPC_ESHAPE, "window %d not in [1, T]", cfg->window);
+  if (cfg->keep <= 0 || cfg->keep > T) return fail(MPC_ESHAPE, "keep %d not in [1, T]", cfg->keep);
+  if (cfg->local_keep < 0) return fail(MPC_EINVAL, "local_keep must be >= 0");
+  if (!(cfg->sm_scale >= 0.f) || !std::isfinite(cfg->sm_scale)) return fail(MPC_EINVAL, "bad sm_scale");
+  if (cfg->causal != 0 && cfg->causal != 1) return fail(MPC_EINVAL, "causal must be 0 or 1");
+  if ((int64_t)T * dims->head_dim * elt_size(dims->dtype) >= ((int64_t)1 << 31))
+    return fail(MPC_EUNSUPPORTED, "T too large");
+  const EvictWs lay = evict_ws(dims, T, cfg->window);
+  if (!ws || ws_bytes < lay.total)
+    return fail(MPC_EWORKSPACE, "static eviction needs %zu workspace bytes", lay.total);
+
+  mpc::EvictArgs a{};
+  a.q_win = q_win;
+  a.k = k;
+  a.v = v;
+  a.kept = kept_idx;
+  a.k_out = k_out;
+  a.v_out = v_out;
+  a.rowstat = (double*)((char*)ws + lay.rowstat);
+  a.score = token_score ? token_score : (float*)((char*)ws + lay.score);
+  a.row_lse = row_lse;
+  a.B = dims->batch;
+  a.layer0 = dims->layer0;
+  a.n_layers = dims->n_layers;
+  a.Hq = dims->n_q_heads;
+  a.Hkv = dims->n_kv_heads;
+  a.T = T;
+  a.W = cfg->window;
+  a.keep = cfg->keep;
+  a.local_keep = cfg->local_keep;
+  a.causal = cfg->causal;
+  a.period = cfg->share_period;
+  a.start = cfg->share_start;
+  a.c64 = (double)cfg->sm_scale * 1.4426950408889634;
+  a.c_hi = (float)a.c64;
+  a.c_lo = (float)(a.c64 - (double)a.c_hi);
+  hipStream_t st = (hipStream_t)stream;
+  const int D = dims->head_dim, dt = dims->dtype;
+  if ((s = launched(mpc::launch_rowstats(a, dt, D, st), "row statistics")) != MPC_OK) return s;
+  if ((s = launched(mpc::launch_colsum(a, dt, D, st), "column sums")) != MPC_OK) return s;
+  if ((s = launched(mpc::launch_topk(a, st), "top-k")) != MPC_OK) return s;
+  if ((s = launched(mpc::launch_gather(a, dt, D, st), "gather")) != MPC_OK) return s;
+  return ok();
+}
+
+mpc_status mpc_build_clusters(const mpc_dims* dims, int32_t Ts, const mpc_select_cfg* cfg,
+                              const void* k_cache, float* cent, float* scent, void* stream) {
+  mpc_status s = check_dims(dims);
+  if (s != MPC_OK) return s;
+  if (!cfg) return fail(MPC_EINVAL, "cfg is NULL");
+  if (Ts <= 0 || cfg->cluster_size <= 0 || cfg->fanout <= 0)
+    return fail(MPC_EINVAL, "Ts, cluster_size and fanout must be positive");
+  if (!(cfg->alpha >= 0.f && cfg->alpha <= 1.f)) return fail(MPC_EINVAL, "alpha must be in [0, 1]");
+  if (!k_cache || !cent || !scent) return fail(MPC_EINVAL, "a required tensor pointer is NULL");
+  if (!aligned16(k_cache) || !aligned16(cent) || !aligned16(scent))
+    return fail(MPC_EINVAL, "tensor bases must be 16-byte aligned");
+  mpc::BuildArgs a{};
+  a.k = k_cache;
+  a.cent = cent;
+  a.scent = scent;
+  a.B = dims->batch;
+  a.layer0 = dims->layer0;
+  a.n_layers = dims->n_layers;
+  a.Hkv = dims->n_kv_heads;
+  a.Ts = Ts;
+  a.s = cfg->cluster_size;
+  a.f = cfg->fanout;
+  a.C = ceil_div(Ts, a.s);
+  a.S = ceil_div(a.C, a.f);
+  a.period = cfg->share_period;
+  a.start = cfg->share_start;
+  a.alpha = cfg->alpha;
+  a.beta = (float)(1.0 - (double)cfg->alpha);
+  if ((int64_t)a.n_layers * a.B * a.Hkv * a.S >= ((int64_t)1 << 31))
+    return fail(MPC_EUNSUPPORTED, "grid too large");
+  if ((s = launched(mpc::launch_build(a, dims->dtype, dims->head_dim, (hipStream_t)stream), "build")) != MPC_OK)
+    return s;
+  return ok();
+}
+
+mpc_status mpc_select_clusters(const mpc_dims* dims, int32_t Ts, const mpc_select_cfg* cfg,
+                               const void* q, const float* cent, const float* scent,
+                               int32_t* sel, float* sel_score, void* ws, size_t ws_bytes,
+                               void* stream) {
+  (void)ws;
+  (void)ws_bytes;
+  mpc_status s = check_dims(dims);
+  if (s != MPC_OK) return s;
+  if (!cfg) return fail(MPC_EINVAL, "cfg is NULL");
+  if (Ts <= 0 || cfg->cluster_size <= 0 || cfg->fanout <= 0 || cfg->k_super <= 0 || cfg->k_clusters <= 0)
+    return fail(MPC_EINVAL, "Ts, cluster_size, fanout and budgets must be positive");
+  if (!q || !cent || !scent || !sel) return fail(MPC_EINVAL, "a required tensor pointer is NULL");
+  const int C = ceil_div(Ts, cfg->cluster_size), S = ceil_div(C, cfg->fanout);
+  if (cfg->k_super > S) return fail(MPC_ESHAPE, "k_super %d > super-clusters %d", cfg->k_super, S);
+  const int tail = C - (S - 1) * cfg->fanout;
+  const int min_cand = cfg->k_super * cfg->fanout - (cfg->fanout - tail);
+  if (cfg->k_clusters > min_cand)
+    return fail(MPC_ESHAPE, "k_clusters %d exceeds the smallest candidate set %d", cfg->k_clusters, min_cand);
+  if (S > mpc::kSelMaxSuper || (int64_t)cfg->k_super * cfg->fanout > mpc::kSelMaxCand)
+    return fail(MPC_EUNSUPPORTED, "selection sizes beyond the kernel limits");
+  mpc::SelectArgs a{};
+  a.q = q;
+  a.cent = cent;
+  a.scent = scent;
+  a.sel = sel;
+  a.sel_score = sel_score;
+  a.B = dims->batch;
+  a.layer0 = dims->layer0;
+  a.n_layers = dims->n_layers;
+  a.Hq = dims->n_q_heads;
+  a.Hkv = dims->n_kv_heads;
+  a.C = C;
+  a.S = S;
+  a.f = cfg->fanout;
+  a.NC = cfg->k_super * cfg->fanout;
+  a.k_super = cfg->k_super;
+  a.k_clusters = cfg->k_clusters;
+  a.period = cfg->share_period;
+  a.start = cfg->share_start;
+  if ((s = launched(mpc::launch_select(a, dims->dtype, dims->head_dim, (hipStream_t)stream), "select")) != MPC_OK)
+    return s;
+  return ok();
+}
+
+mpc_status mpc_sparse_decode_attn(const mpc_dims* dims, int32_t Ts, int32_t cluster_size,
+                                  const void* q, const void* k_cache, const void* v_cache,
+                                  const int32_t* sel, int32_t k_clusters, float sm_scale,
+                                  void* out, float* lse, void* ws, size_t ws_bytes, void* stream) {
+  mpc_status s = check_dims(dims);
+  if (s != MPC_OK) return s;
+  if (Ts <= 0 || cluster_size <= 0 || k_clusters <= 0)
+    return fail(MPC_EINVAL, "Ts, cluster_size and k_clusters must be positive");
+  if (!q || !k_cache || !v_cache || !sel || !out) return fail(MPC_EINVAL, "a required tensor pointer is NULL");
+  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache))
+    return fail(MPC_EINVAL, "tensor bases must be 16-byte aligned");
+  if (!std::isfinite(sm_scale)) return fail(MPC_EINVAL, "bad sm_scale");
+  const int G = dims->n_q_heads / dims->n_kv_heads;
+  if (G != 1 && G != 2 && G != 4 && G != 8) return fail(MPC_EUNSUPPORTED, "group size %d not in {1,2,4,8}", G);
+  const int C = ceil_div(Ts, cluster_size);
+  if (k_clusters > C) return fail(MPC_ESHAPE, "k_clusters %d > clusters %d", k_clusters, C);
+  if (k_clusters > 1024) return fail(MPC_EUNSUPPORTED, "k_clusters above 1024");
+  if ((int64_t)k_clusters * cluster_size >= ((int64_t)1 << 30)) return fail(MPC_EUNSUPPORTED, "too many tokens");
+  const int units = dims->n_layers * dims->batch * dims->n_kv_heads;
+  const DecodeWs lay = decode_ws(dims);
+  const int splits = mpc::decode_splits(units, k_clusters * cluster_size, dims->head_dim, elt_size(dims->dtype));
+  if (splits > 1 && (!ws || ws_bytes < lay.total))
+    return fail(MPC_EWORKSPACE, "sparse decode attention needs %zu workspace bytes", lay.total);
+  mpc::DecodeArgs a{};
+  a.q = q;
+  a.k = k_cache;
+  a.v = v_cache;
+  a.sel = sel;
+  a.out = out;
+  a.lse = lse;
+  a.part = splits > 1 ? (float*)ws : nullptr;
+  a.counters = splits > 1 ? (int32_t*)((char*)ws + lay.counters) : nullptr;
+  a.Ts = Ts;
+  a.s = cluster_size;
+  a.k_sel = k_clusters;
+  a.Hq = dims->n_q_heads;
+  a.Hkv = dims->n_kv_heads;
+  a.splits = splits;
+  a.qscale = (float)((double)sm_scale * 1.4426950408889634);
+  if ((s = launched(mpc::launch_sparse_decode(a, dims->dtype, dims->head_dim, G, units, (hipStream_t)stream),
+                    "sparse decode attention")) != MPC_OK)
+    return s;
+  return ok();
+}
+
+}  // extern "C"

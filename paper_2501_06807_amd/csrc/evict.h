@@ -1,0 +1,31 @@
+// Launch interface of the static-eviction kernels.
+#pragma once
+#include "common.h"
+
+namespace mpc {
+
+constexpr int kRowBlock = 128;  // window rows per row-statistics workgroup (4 waves x 32)
+constexpr int kColWaveKeys = 64;  // keys per wave in the column-sum pass (2 MFMA column blocks)
+constexpr int kColBlockKeys = 4 * kColWaveKeys;
+
+struct EvictArgs {
+  const void* q_win;   // [L][B][Hq][W][d]
+  const void* k;       // [L][B][Hkv][T][d]
+  const void* v;
+  int32_t* kept;       // [L][B][Hkv][keep]
+  void* k_out;         // [L][B][Hkv][keep][d]
+  void* v_out;
+  float* score;        // [L][B][Hkv][T] accumulated attention (token_score or workspace)
+  double* rowstat;     // [L][B][Hq][W]: -(c * max + log2(sum)) per window row
+  float* row_lse;      // [L][B][Hq][W] natural log-sum-exp, optional
+  int B, layer0, n_layers, Hq, Hkv, T, W, keep, local_keep, causal, period, start;
+  float c_hi, c_lo;    // sm_scale * log2(e) as an unevaluated fp32 sum
+  double c64;          // the same in fp64
+};
+
+hipError_t launch_rowstats(const EvictArgs& a, int dtype, int D, hipStream_t st);
+hipError_t launch_colsum(const EvictArgs& a, int dtype, int D, hipStream_t st);
+hipError_t launch_topk(const EvictArgs& a, hipStream_t st);
+hipError_t launch_gather(const EvictArgs& a, int dtype, int D, hipStream_t st);
+
+}  // namespace mpc

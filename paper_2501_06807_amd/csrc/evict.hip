@@ -1,0 +1,476 @@
+// Look-once static eviction on gfx950: accumulated window attention, top-k, gather.
+//
+// The accumulated attention of key j is A[j] = sum over the group's window rows t of
+// softmax_j(sm_scale * q_t . k_j). It needs every row's normaliser before any column can be
+// summed, so it takes two passes over the scores, both on the matrix cores
+// (v_mfma_f32_32x32x{16,16,2}_{bf16,f16,f32}):
+//   pass 1 (k_rowstats): window rows stay in registers as the B operand, key tiles stream
+//     through LDS as the A operand; each lane owns one query column of the 32x32 output, so the
+//     row max and row sum are in-lane reductions. Output per row: the fp64 bias
+//     -(c * max + log2(sum)), c = sm_scale * log2(e).
+//   pass 2 (k_colsum): keys stay in registers as the B operand, window-row tiles (all query heads
+//     of the group) stream through LDS as the A operand; each lane owns one key column, so the
+//     column sum is in-lane. p = exp2(c * s + bias) is formed with c and the bias as unevaluated
+//     fp32 pairs (two FMAs), summed over 16 rows in fp32 and accumulated across tiles in fp64.
+// The top-k is a 4-pass, 8-bit LDS radix select on the fp32 score bits followed by an ordered
+// block compaction; the gather copies kept rows with 16-byte lanes.
+#include "evict.h"
+
+namespace mpc {
+namespace {
+
+typedef float f32x16 __attribute__((__vector_size__(16 * sizeof(float))));
+typedef __bf16 bf16x8 __attribute__((__vector_size__(8 * sizeof(__bf16))));
+typedef _Float16 f16x8 __attribute__((__vector_size__(8 * sizeof(_Float16))));
+
+// Matrix-core operation per element type: reduction length K per instruction, KL elements per
+// lane. Lane l feeds row (l % 32) of A / column (l % 32) of B with the k-slice
+// [ks * K + (l / 32) * KL, + KL); any k-permutation works as long as A and B share it.
+template <class DT>
+struct Mma;
+template <>
+struct Mma<BF16> {
+  static constexpr int K = 16, KL = 8;
+  using Op = bf16x8;
+  __device__ static f32x16 run(Op a, Op b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+  }
+  __device__ static Op load(const void* p) { return __builtin_bit_cast(Op, *(const uint4*)p); }
+};
+template <>
+struct Mma<F16> {
+  static constexpr int K = 16, KL = 8;
+  using Op = f16x8;
+  __device__ static f32x16 run(Op a, Op b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+  }
+  __device__ static Op load(const void* p) { return __builtin_bit_cast(Op, *(const uint4*)p); }
+};
+template <>
+struct Mma<F32> {
+  static constexpr int K = 2, KL = 1;
+  using Op = float;
+  __device__ static f32x16 run(Op a, Op b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+  }
+  __device__ static Op load(const void* p) { return *(const float*)p; }
+};
+
+// Row of the 32x32 output held in accumulator register r of `lane` (the column is lane % 32).
+__device__ __forceinline__ int acc_row(int r, int lane) {
+  return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+}
+
+// 32-row tiles of a [rows][D] matrix staged through LDS with 16-byte chunks; the row stride is
+// padded by 16 bytes to spread the 32 rows of a fragment read over the LDS banks.
+template <class DT, int D>
+struct Tile {
+  static constexpr int RB = D * DT::kElt;
+  static constexpr int RS = RB + 16;
+  static constexpr int CH = RB / 16;
+  static constexpr int CHUNKS = 32 * CH;
+  static constexpr int PER = (CHUNKS + 255) / 256;
+  static constexpr int BYTES = 32 * RS;
+};
+
+template <class DT, int D>
+__global__ __launch_bounds__(256) void k_rowstats(EvictArgs a) {
+  using M = Mma<DT>;
+  using TL = Tile<DT, D>;
+  constexpr int KS = D / M::K;
+  __shared__ __align__(16) unsigned char s_k[2][TL::BYTES];
+
+  const int n_rb = (a.W + kRowBlock - 1) / kRowBlock;
+  const int rb = blockIdx.x % n_rb;
+  const int qunit = blockIdx.x / n_rb;  // (l * B + b) * Hq + hq
+  const int l = qunit / (a.B * a.Hq);
+  if (owner_layer(a.layer0 + l, a.period, a.start) != a.layer0 + l) return;
+  const int b = (qunit / a.Hq) % a.B, hq = qunit % a.Hq;
+  const int G = a.Hq / a.Hkv;
+  const size_t kvunit = ((size_t)l * a.B + b) * a.Hkv + hq / G;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, c32 = lane & 31, hl = lane >> 5;
+
+  const int t = rb * kRowBlock + w * 32 + c32;
+  const bool tvalid = t < a.W;
+  const int tc = tvalid ? t : a.W - 1;
+  const int pos = a.T - a.W + tc;
+  typename M::Op qf[KS];
+  const char* qrow = (const char*)a.q_win + ((size_t)qunit * a.W + tc) * TL::RB;
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) qf[ks] = M::load(qrow + (ks * M::K + hl * M::KL) * DT::kElt);
+
+  const char* kh = (const char*)a.k + kvunit * a.T * TL::RB;
+  const int last_row = min(a.W - 1, rb * kRowBlock + kRowBlock - 1);
+  const int jend = a.causal ? min(a.T, a.T - a.W + last_row + 1) : a.T;
+  const int ntile = (jend + 31) / 32;
+
+  uint4 pre[TL::PER];
+  auto fetch = [&](int tile) {
+#pragma unroll
+    for (int i = 0; i < TL::PER; ++i) {
+      const int ch = tid + i * 256;
+      const int row = ch / TL::CH, c16 = ch % TL::CH;
+      const int j = tile * 32 + row;
+      pre[i] = (ch < TL::CHUNKS && j < a.T) ? ldg16(kh + (size_t)j * TL::RB + c16 * 16) : make_uint4(0, 0, 0, 0);
+    }
+  };
+  auto stash = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < TL::PER; ++i) {
+      const int ch = tid + i * 256;
+      if (ch < TL::CHUNKS) *(uint4*)&s_k[buf][(ch / TL::CH) * TL::RS + (ch % TL::CH) * 16] = pre[i];
+    }
+  };
+  fetch(0);
+  stash(0);
+  __syncthreads();
+
+  float m = -INFINITY, bh = 0.f, bl = 0.f;
+  double ell = 0.0;
+  for (int it = 0; it < ntile; ++it) {
+    const int buf = it & 1;
+    if (it + 1 < ntile) fetch(it + 1);
+    f32x16 acc = {};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const typename M::Op af =
+          M::load(&s_k[buf][c32 * TL::RS + (ks * M::K + hl * M::KL) * DT::kElt]);
+      acc = M::run(af, qf[ks], acc);
+    }
+    const int j0 = it * 32;
+    float tmax = -INFINITY;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int j = j0 + acc_row(r, lane);
+      if (j < a.T && (!a.causal || j <= pos)) tmax = fmaxf(tmax, acc[r]);
+    }
+    if (tmax > m) {
+      if (ell > 0.0) ell *= exp2(((double)m - (double)tmax) * a.c64);
+      m = tmax;
+      const double nb = -a.c64 * (double)m;
+      bh = (float)nb;
+      bl = (float)(nb - (double)bh);
+    }
+    float ps = 0.f;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int j = j0 + acc_row(r, lane);
+      if (j < a.T && (!a.causal || j <= pos))
+        ps += fast_exp2(fmaf(a.c_hi, acc[r], bh) + fmaf(a.c_lo, acc[r], bl));
+    }
+    ell += (double)ps;
+    if (it + 1 < ntile) stash(buf ^ 1);
+    __syncthreads();
+  }
+  const float mo = __shfl_xor(m, 32);
+  const double eo = __shfl_xor(ell, 32);
+  const float mx = fmaxf(m, mo);
+  double L = 0.0;
+  if (ell > 0.0) L += ell * exp2(((double)m - (double)mx) * a.c64);
+  if (eo > 0.0) L += eo * exp2(((double)mo - (double)mx) * a.c64);
+  if (hl == 0 && tvalid) {
+    const double nb = -(a.c64 * (double)mx) - log2(L);
+    a.rowstat[(size_t)qunit * a.W + t] = nb;
+    if (a.row_lse) a.row_lse[(size_t)qunit * a.W + t] = (float)(-nb * 0.69314718055994531);
+  }
+}
+
+template <class DT, int D>
+__global__ __launch_bounds__(256) void k_colsum(EvictArgs a) {
+  using M = Mma<DT>;
+  using TL = Tile<DT, D>;
+  constexpr int KS = D / M::K;
+  constexpr int NB = kColWaveKeys / 32;
+  __shared__ __align__(16) unsigned char s_q[2][TL::BYTES];
+  __shared__ float s_bh[2][32], s_bl[2][32];
+
+  const int n_kb = (a.T + kColBlockKeys - 1) / kColBlockKeys;
+  const int kb = blockIdx.x % n_kb;
+  const int kvunit = blockIdx.x / n_kb;  // (l * B + b) * Hkv + h
+  const int l = kvunit / (a.B * a.Hkv);
+  if (owner_layer(a.layer0 + l, a.period, a.start) != a.layer0 + l) return;
+  const int b = (kvunit / a.Hkv) % a.B, h = kvunit % a.Hkv;
+  const int G = a.Hq / a.Hkv;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, c32 = lane & 31, hl = lane >> 5;
+
+  const int jw = kb * kColBlockKeys + w * kColWaveKeys;
+  const char* kh = (const char*)a.k + (size_t)kvunit * a.T * TL::RB;
+  typename M::Op kf[NB][KS];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    const int j = min(jw + nb * 32 + c32, a.T - 1);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      kf[nb][ks] = M::load(kh + (size_t)j * TL::RB + (ks * M::K + hl * M::KL) * DT::kElt);
+  }
+
+  const int j_lo = kb * kColBlockKeys;
+  const int t_start = a.causal ? (max(0, j_lo - (a.T - a.W)) & ~31) : 0;
+  const int n_t = (a.W - t_start + 31) / 32;
+  const int ntile = G * n_t;
+  const size_t qunit0 = ((size_t)l * a.B + b) * a.Hq + (size_t)h * G;
+
+  uint4 pre[TL::PER];
+  double pre_b = 0.0;
+  auto fetch = [&](int tile) {
+    const int g = tile / n_t, t0 = t_start + (tile % n_t) * 32;
+    const char* qb = (const char*)a.q_win + ((qunit0 + g) * a.W) * TL::RB;
+#pragma unroll
+    for (int i = 0; i < TL::PER; ++i) {
+      const int ch = tid + i * 256;
+      const int row = ch / TL::CH, c16 = ch % TL::CH;
+      const int t = t0 + row;
+      pre[i] = (ch < TL::CHUNKS && t < a.W) ? ldg16(qb + (size_t)t * TL::RB + c16 * 16) : make_uint4(0, 0, 0, 0);
+    }
+    if (tid < 32) {
+      const int t = t0 + tid;
+      pre_b = t < a.W ? a.rowstat[(qunit0 + g) * a.W + t] : 0.0;
+    }
+  };
+  auto stash = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < TL::PER; ++i) {
+      const int ch = tid + i * 256;
+      if (ch < TL::CHUNKS) *(uint4*)&s_q[buf][(ch / TL::CH) * TL::RS + (ch % TL::CH) * 16] = pre[i];
+    }
+    if (tid < 32) {
+      const float hi = (float)pre_b;
+      s_bh[buf][tid] = hi;
+      s_bl[buf][tid] = (float)(pre_b - (double)hi);
+    }
+  };
+  fetch(0);
+  stash(0);
+  __syncthreads();
+
+  double cacc[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) cacc[nb] = 0.0;
+  for (int it = 0; it < ntile; ++it) {
+    const int buf = it & 1;
+    if (it + 1 < ntile) fetch(it + 1);
+    const int t0 = t_start + (it % n_t) * 32;
+    float bhr[16], blr[16];
+    int trow[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int rr = acc_row(r, lane);
+      trow[r] = t0 + rr;
+      bhr[r] = s_bh[buf][rr];
+      blr[r] = s_bl[buf][rr];
+    }
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      f32x16 acc = {};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const typename M::Op af =
+            M::load(&s_q[buf][c32 * TL::RS + (ks * M::K + hl * M::KL) * DT::kElt]);
+        acc = M::run(af, kf[nb][ks], acc);
+      }
+      const int j = jw + nb * 32 + c32;
+      float ps = 0.f;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        if (trow[r] < a.W && (!a.causal || j <= a.T - a.W + trow[r]))
+          ps += fast_exp2(fmaf(a.c_hi, acc[r], bhr[r]) + fmaf(a.c_lo, acc[r], blr[r]));
+      }
+      cacc[nb] += (double)ps;
+    }
+    if (it + 1 < ntile) stash(buf ^ 1);
+    __syncthreads();
+  }
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    const double tot = cacc[nb] + __shfl_xor(cacc[nb], 32);
+    const int j = jw + nb * 32 + c32;
+    if (hl == 0 && j < a.T) a.score[(size_t)kvunit * a.T + j] = (float)tot;
+  }
+}
+
+// Exclusive prefix sum over the 1024 threads of a workgroup.
+__device__ int block_excl_scan(int v, int* wsum) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  int x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) wsum[w] = x;
+  __syncthreads();
+  if (w == 0) {
+    int s = lane < 16 ? wsum[lane] : 0;
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) {
+      const int y = __shfl_up(s, o);
+      if (lane >= o) s += y;
+    }
+    if (lane < 16) wsum[lane] = s;
+  }
+  __syncthreads();
+  const int res = (w > 0 ? wsum[w - 1] : 0) + x - v;
+  __syncthreads();
+  return res;
+}
+
+constexpr int kTopkThreads = 1024;
+
+__global__ __launch_bounds__(kTopkThreads) void k_topk(EvictArgs a) {
+  __shared__ uint32_t hist[kTopkThreads / 64][256];
+  __shared__ uint32_t tot[256];
+  __shared__ uint32_t s_prefix;
+  __shared__ int s_rem;
+  __shared__ int wsum[16];
+
+  const int unit = blockIdx.x;
+  const int l = unit / (a.B * a.Hkv);
+  if (owner_layer(a.layer0 + l, a.period, a.start) != a.layer0 + l) return;
+  const int tid = threadIdx.x, w = tid >> 6;
+  const int loc = min(a.local_keep, a.keep);
+  const int n_old = a.T - loc, n_sel = a.keep - loc;
+  const uint32_t* key = (const uint32_t*)(a.score + (size_t)unit * a.T);
+  int32_t* out = a.kept + (size_t)unit * a.keep;
+
+  // radix select: the n_sel-th largest key (non-negative floats order like their bits)
+  uint32_t prefix = 0, mask = 0;
+  int rem = n_sel;
+  if (n_sel > 0) {
+    for (int shift = 24; shift >= 0; shift -= 8) {
+      for (int i = tid; i < (kTopkThreads / 64) * 256; i += kTopkThreads) hist[i / 256][i % 256] = 0;
+      __syncthreads();
+      for (int j = tid; j < n_old; j += kTopkThreads) {
+        const uint32_t u = key[j];
+        if ((u & mask) == prefix) atomicAdd(&hist[w][(u >> shift) & 255u], 1u);
+      }
+      __syncthreads();
+      if (tid < 256) {
+        uint32_t s = 0;
+        for (int i = 0; i < kTopkThreads / 64; ++i) s += hist[i][tid];
+        tot[tid] = s;
+      }
+      __syncthreads();
+      if (tid == 0) {
+        uint32_t cum = 0;
+        int d = 255;
+        for (; d > 0; --d) {
+          if (cum + tot[d] >= (uint32_t)rem) break;
+          cum += tot[d];
+        }
+        s_prefix = prefix | ((uint32_t)d << shift);
+        s_rem = rem - (int)cum;
+      }
+      __syncthreads();
+      prefix = s_prefix;
+      rem = s_rem;
+      mask |= 255u << shift;
+      __syncthreads();
+    }
+  }
+  // ordered compaction: keys above the threshold, then the lowest-index ties up to `rem`
+  const int chk = (n_old + kTopkThreads - 1) / kTopkThreads;
+  const int j0 = min(n_old, tid * chk), j1 = min(n_old, j0 + chk);
+  int gt = 0, eq = 0;
+  if (n_sel > 0)
+    for (int j = j0; j < j1; ++j) {
+      const uint32_t u = key[j];
+      gt += u > prefix;
+      eq += u == prefix;
+    }
+  const int eq_before = block_excl_scan(eq, wsum);
+  const int take = n_sel > 0 ? max(0, min(eq, rem - eq_before)) : 0;
+  int off = block_excl_scan(gt + take, wsum);
+  if (n_sel > 0) {
+    int taken = 0;
+    for (int j = j0; j < j1; ++j) {
+      const uint32_t u = key[j];
+      if (u > prefix || (u == prefix && taken < take)) {
+        taken += u == prefix;
+        out[off++] = j;
+      }
+    }
+  }
+  for (int i = tid; i < loc; i += kTopkThreads) out[n_sel + i] = n_old + i;
+}
+
+template <int RB>
+__global__ __launch_bounds__(256) void k_gather(EvictArgs a) {
+  constexpr int CH = RB / 16;
+  constexpr int RPP = 256 / CH;
+  constexpr int ROWS = 64;
+  const int n_chunks = (a.keep + ROWS - 1) / ROWS;
+  const int chunk = blockIdx.x % n_chunks;
+  const size_t unit = blockIdx.x / n_chunks;
+  const int l = (int)(unit / ((size_t)a.B * a.Hkv));
+  const int o = owner_layer(a.layer0 + l, a.period, a.start) - a.layer0;
+  const int src_l = o >= 0 ? o : l;
+  const size_t src_unit = unit - (size_t)(l - src_l) * a.B * a.Hkv;
+  const int r_in = threadIdx.x / CH, c16 = threadIdx.x % CH;
+  const int end = min(a.keep, chunk * ROWS + ROWS);
+  for (int i = chunk * ROWS + r_in; i < end; i += RPP) {
+    int idx = a.kept[src_unit * a.keep + i];
+    if (src_l != l && c16 == 0) a.kept[unit * a.keep + i] = idx;
+    idx = min(max(idx, 0), a.T - 1);  // indices supplied by the caller are clamped into the cache
+    const size_t so = (unit * a.T + idx) * RB + c16 * 16;
+    const size_t dst = (unit * a.keep + i) * RB + c16 * 16;
+    *(uint4*)((char*)a.k_out + dst) = ldg16((const char*)a.k + so);
+    *(uint4*)((char*)a.v_out + dst) = ldg16((const char*)a.v + so);
+  }
+}
+
+template <class DT, int D>
+hipError_t launch_pass(const EvictArgs& a, bool rows, hipStream_t st) {
+  if (rows) {
+    const int n_rb = (a.W + kRowBlock - 1) / kRowBlock;
+    hipLaunchKernelGGL((k_rowstats<DT, D>), dim3(a.n_layers * a.B * a.Hq * n_rb), dim3(256), 0, st, a);
+  } else {
+    const int n_kb = (a.T + kColBlockKeys - 1) / kColBlockKeys;
+    hipLaunchKernelGGL((k_colsum<DT, D>), dim3(a.n_layers * a.B * a.Hkv * n_kb), dim3(256), 0, st, a);
+  }
+  return hipGetLastError();
+}
+
+template <class DT>
+hipError_t launch_pass_dt(const EvictArgs& a, int D, bool rows, hipStream_t st) {
+  if (D == 64) return launch_pass<DT, 64>(a, rows, st);
+  if (D == 128) return launch_pass<DT, 128>(a, rows, st);
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_pass_any(const EvictArgs& a, int dtype, int D, bool rows, hipStream_t st) {
+  switch (dtype) {
+    case MPC_FP32: return launch_pass_dt<F32>(a, D, rows, st);
+    case MPC_FP16: return launch_pass_dt<F16>(a, D, rows, st);
+    case MPC_BF16: return launch_pass_dt<BF16>(a, D, rows, st);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+hipError_t launch_rowstats(const EvictArgs& a, int dtype, int D, hipStream_t st) {
+  return launch_pass_any(a, dtype, D, true, st);
+}
+
+hipError_t launch_colsum(const EvictArgs& a, int dtype, int D, hipStream_t st) {
+  return launch_pass_any(a, dtype, D, false, st);
+}
+
+hipError_t launch_topk(const EvictArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL(k_topk, dim3(a.n_layers * a.B * a.Hkv), dim3(kTopkThreads), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather(const EvictArgs& a, int dtype, int D, hipStream_t st) {
+  const int rb = D * (dtype == MPC_FP32 ? 4 : 2);
+  const int blocks = a.n_layers * a.B * a.Hkv * ((a.keep + 63) / 64);
+  switch (rb) {
+    case 128: hipLaunchKernelGGL(k_gather<128>, dim3(blocks), dim3(256), 0, st, a); break;
+    case 256: hipLaunchKernelGGL(k_gather<256>, dim3(blocks), dim3(256), 0, st, a); break;
+    case 512: hipLaunchKernelGGL(k_gather<512>, dim3(blocks), dim3(256), 0, st, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace mpc

@@ -1,0 +1,24 @@
+// Launch interface of the two-level cluster selection kernel.
+#pragma once
+#include "common.h"
+
+namespace mpc {
+
+constexpr int kSelMaxSuper = 1024;  // S limit (LDS)
+constexpr int kSelMaxCand = 2048;   // k_super * fanout limit (LDS)
+
+struct SelectArgs {
+  const void* q;        // [L][B][Hq][d]
+  const float* cent;    // [L][B][Hkv][C][d]
+  const float* scent;   // [L][B][Hkv][S][d]
+  int32_t* sel;         // [L][B][Hkv][k_clusters]
+  float* sel_score;     // same or null
+  int B, layer0, n_layers, Hq, Hkv;
+  int C, S, f, NC, k_super, k_clusters;  // NC = k_super * f
+  int period, start;
+};
+
+size_t select_smem_bytes(int D, int S, int NC);
+hipError_t launch_select(const SelectArgs& a, int dtype, int D, hipStream_t st);
+
+}  // namespace mpc

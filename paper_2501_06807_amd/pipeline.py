@@ -1,0 +1,67 @@
+"""Preallocated prefill + decode path over the four C-ABI entry points."""
+import math
+
+import torch
+
+from . import _lib as L
+
+
+class MPCachePath:
+    """Buffers and calls for one workload: static eviction and cluster build at prefill, then
+    selection + sparse attention for every decode step, all layers of the block per call."""
+
+    def __init__(self, *, n_layers, batch, n_q_heads, n_kv_heads, head_dim, dtype, T, window, keep,
+                 local_keep, cluster, fanout, k_super, k_clusters, share_period, share_start=2,
+                 alpha=0.6, causal=True, layer0=0, device="cuda", keep_scores=False):
+        self.L, self.B, self.Hq, self.Hkv, self.d = n_layers, batch, n_q_heads, n_kv_heads, head_dim
+        self.dtype, self.T, self.W, self.keep = dtype, T, window, keep
+        self.local_keep, self.causal, self.layer0 = local_keep, causal, layer0
+        self.cluster, self.k_clusters = cluster, k_clusters
+        self.share_period, self.share_start = share_period, share_start
+        self.sm_scale = 1.0 / math.sqrt(head_dim)
+        self.C = -(-keep // cluster)
+        self.S = -(-self.C // fanout)
+        self.cfg = L.select_cfg(cluster, fanout, k_super, k_clusters, alpha, share_period, share_start)
+        dev = torch.device(device)
+        kv_shape = (n_layers, batch, n_kv_heads)
+        self.kept = torch.zeros(*kv_shape, keep, dtype=torch.int32, device=dev)
+        self.k_s = torch.empty(*kv_shape, keep, head_dim, dtype=dtype, device=dev)
+        self.v_s = torch.empty_like(self.k_s)
+        self.cent = torch.zeros(*kv_shape, self.C, head_dim, dtype=torch.float32, device=dev)
+        self.scent = torch.zeros(*kv_shape, self.S, head_dim, dtype=torch.float32, device=dev)
+        self.sel = torch.zeros(*kv_shape, k_clusters, dtype=torch.int32, device=dev)
+        self.sel_score = torch.zeros(*kv_shape, k_clusters, dtype=torch.float32, device=dev)
+        self.out = torch.empty(n_layers, batch, n_q_heads, head_dim, dtype=dtype, device=dev)
+        self.lse = torch.empty(n_layers, batch, n_q_heads, dtype=torch.float32, device=dev)
+        self.token_score = (torch.zeros(*kv_shape, T, dtype=torch.float32, device=dev)
+                            if keep_scores else None)
+        self.row_lse = (torch.zeros(n_layers, batch, n_q_heads, window, dtype=torch.float32, device=dev)
+                        if keep_scores else None)
+        qd = L.MpcDims(batch=batch, layer0=layer0, n_layers=n_layers, n_q_heads=n_q_heads,
+                       n_kv_heads=n_kv_heads, head_dim=head_dim, dtype=L.DTYPE_CODE[dtype])
+        ecfg = L.MpcEvictCfg(window=window, keep=keep, local_keep=local_keep, sm_scale=self.sm_scale,
+                             causal=int(causal), share_period=share_period, share_start=share_start)
+        self.ws_evict = L.workspace(L.workspace_bytes(L.MPC_OP_STATIC_EVICT, qd, T, ecfg), dev)
+        self.ws_decode = L.workspace(L.workspace_bytes(L.MPC_OP_DECODE_ATTN, qd, keep), dev)
+
+    def prefill(self, q_win, k, v, stream=None):
+        L.mpc_static_evict(q_win, k, v, self.kept, self.k_s, self.v_s, keep=self.keep,
+                           local_keep=self.local_keep, sm_scale=self.sm_scale, causal=self.causal,
+                           layer0=self.layer0, share_period=self.share_period,
+                           share_start=self.share_start, token_score=self.token_score,
+                           row_lse=self.row_lse, ws=self.ws_evict, stream=stream)
+        L.mpc_build_clusters(self.k_s, self.cent, self.scent, self.cfg, layer0=self.layer0, stream=stream)
+
+    def select(self, q, stream=None):
+        L.mpc_select_clusters(q, self.cent, self.scent, self.sel, self.cfg, Ts=self.keep,
+                              sel_score=self.sel_score, layer0=self.layer0, stream=stream)
+
+    def attend(self, q, stream=None):
+        L.mpc_sparse_decode_attn(q, self.k_s, self.v_s, self.sel, self.out, cluster_size=self.cluster,
+                                 sm_scale=self.sm_scale, lse=self.lse, ws=self.ws_decode,
+                                 layer0=self.layer0, stream=stream)
+
+    def decode(self, q, stream=None):
+        self.select(q, stream)
+        self.attend(q, stream)
+        return self.out
