@@ -1,0 +1,245 @@
+#!/usr/bin/env python3
+"""Benchmark of the MPCache hot path on one MI355X.
+
+One timed step = one full pass of the path over one batch of synthetic input already resident in
+HBM: look-once static eviction of the prompt cache (window scoring, top-k, gather), cluster
+representatives, then every decode step of the workload (two-level selection with layer sharing +
+sparse attention over all layers). The reported metric is the decode step's latency per layer
+(select + attention), measured with HIP events on the stream the kernels run on, with its
+effective HBM bandwidth against the 8 TB/s peak. Prefill figures are reported beside it.
+
+Prints one JSON line. Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload C4]
+"""
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "decode-step select+sparse-attn latency (µs/layer) & achieved HBM GB/s vs peak"
+HBM_PEAK_GBS = 8000.0
+MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "fp16": 2500.0, "fp32": 157.3}
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=3)
+    p.add_argument("--warmup", type=int, default=1)
+    p.add_argument("--workload", default="C4")
+    p.add_argument("--decode-steps", type=int, default=None, help="decode steps per pass (default: workload's)")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--copy-calibration", action="store_true",
+                   help="run a 1 GiB device copy first (reference kernel for HBM counter scaling)")
+    return p.parse_args()
+
+
+def source_digest(*names):
+    h = hashlib.sha256()
+    for n in names:
+        with open(os.path.join(ROOT, "paper_2501_06807_amd", "csrc", n), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel, workload, digest):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if it was taken on the
+    current kernel source; None otherwise."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("source_digest") != digest:
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def decode_bytes(w, owners, sel, C, S):
+    """Algorithmic bytes of one decode step: reads of representatives, queries, gathered K/V rows
+    and selections; writes of selections and outputs. Every byte is counted once."""
+    G, d, e = w.group, w.head_dim, w.elt
+    n_own = len(owners)
+    sel_read = n_own * w.batch * w.n_kv_heads * ((S + w.k_super * w.fanout) * d * 4 + G * d * e)
+    sel_write = w.n_layers * w.batch * w.n_kv_heads * w.k_clusters * 8
+    # exact gathered token count (a partial last cluster holds fewer rows)
+    last = w.keep - (C - 1) * w.cluster
+    n_tok = int(w.n_layers * w.batch * w.n_kv_heads * w.k_clusters * w.cluster
+                - (sel == C - 1).sum() * (w.cluster - last))
+    attn_read = n_tok * d * e * 2 + w.n_layers * w.batch * (w.n_q_heads * d * e + w.n_kv_heads * w.k_clusters * 4)
+    attn_write = w.n_layers * w.batch * w.n_q_heads * (d * e + 4)
+    return sel_read + sel_write, attn_read + attn_write
+
+
+def prefill_flops(w, n_owner):
+    """One causal pass of window scores q_t . k_j (2d flops each) over the owner layers."""
+    rows = sum(w.T - w.window + t + 1 for t in range(w.window))
+    return n_owner * w.batch * w.n_q_heads * rows * 2 * w.head_dim
+
+
+def cpu_baseline(w, n_steps_sample):
+    """The oracle's decode step (selection + sparse attention) on a sample of the workload: one
+    sharing block of layers (2..2+P-1), every sequence and head, `n_steps_sample` fresh queries."""
+    import oracle
+    import synth
+    layer0 = w.share_start
+    n_l = max(1, w.share_period)
+    ws = w.with_(n_layers=n_l)
+    ks, vs = [], []
+    for l in range(n_l):
+        k, v = synth.cache_host(w, layer0 + l)
+        ks.append(k)
+        vs.append(v)
+    import numpy as np
+    k, v = np.stack(ks), np.stack(vs)
+    cent, scent = oracle.build_clusters(k, w.dtype, cluster=w.cluster, fanout=w.fanout, layer0=layer0,
+                                        share_period=w.share_period, share_start=w.share_start)
+    sp = synth.spec(w, n_layers=layer0 + n_l)
+    qs = [synth.dq_host(sp, e, w.dtype)[layer0:] for e in range(n_steps_sample)]
+    sm = 1.0 / math.sqrt(w.head_dim)
+    t0 = time.perf_counter()
+    for q in qs:
+        sel, _ = oracle.select_clusters(q, cent, scent, w.dtype, Ts=w.keep, cluster=w.cluster, fanout=w.fanout,
+                                        k_super=w.k_super, k_clusters=w.k_clusters, layer0=layer0,
+                                        share_period=w.share_period, share_start=w.share_start)
+        oracle.sparse_decode_attn(q, k, v, sel, w.dtype, cluster=w.cluster, sm_scale=sm)
+    dt = time.perf_counter() - t0
+    return {"value": dt / (n_steps_sample * n_l) * 1e6, "unit": "us/layer", "cores": oracle.threads(),
+            "kind": "oracle",
+            "sample": f"{ws.name}: layers {layer0}..{layer0 + n_l - 1} (one sharing block), all {w.batch} "
+                      f"sequences x {w.n_kv_heads} kv heads, {n_steps_sample} decode steps "
+                      f"(selection + sparse attention), fp64, {dt:.2f} s total"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the path shards by "
+              f"(sequence, kv head) with no exchange, and no multi-GPU figure is measured here.",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    import paper_2501_06807_amd as M
+    import synth
+
+    w = synth.get(args.workload)
+    E = args.decode_steps or w.steps
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    if args.copy_calibration:
+        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    # inputs, generated on the device
+    sp = synth.spec(w)
+    rope = synth.rope_dev(w.T, w.head_dim, w.rope_base) if w.rope else None
+    q_win = synth.qwin_dev(sp, w.dtype, 0, w.n_layers, rope)
+    k, v = synth.kv_dev(sp, w.dtype, 0, w.n_layers, q_win, rope)
+    del rope
+    qs = [synth.dq_dev(sp, w.dtype, e) for e in range(E)]
+    path = M.MPCachePath(n_layers=w.n_layers, batch=w.batch, n_q_heads=w.n_q_heads, n_kv_heads=w.n_kv_heads,
+                         head_dim=w.head_dim, dtype=synth.torch_dtype(w.dtype), T=w.T, window=w.window,
+                         keep=w.keep, local_keep=w.local_keep, cluster=w.cluster, fanout=w.fanout,
+                         k_super=w.k_super, k_clusters=w.k_clusters, share_period=w.share_period,
+                         share_start=w.share_start)
+    torch.cuda.synchronize()
+
+    def one_pass(ev=None):
+        if ev:
+            ev["start"].record()
+        path.prefill(q_win, k, v)
+        if ev:
+            ev["prefill"].record()
+        for e in range(E):
+            if ev:
+                ev["sel"][e].record()
+            path.select(qs[e])
+            if ev:
+                ev["att"][e].record()
+            path.attend(qs[e])
+            if ev:
+                ev["end"][e].record()
+
+    for _ in range(args.warmup):
+        one_pass()
+    torch.cuda.synchronize()
+
+    mk = lambda: torch.cuda.Event(enable_timing=True)
+    evs = [dict(start=mk(), prefill=mk(), sel=[mk() for _ in range(E)], att=[mk() for _ in range(E)],
+                end=[mk() for _ in range(E)]) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        one_pass(evs[s])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    pre_ms = [ev["start"].elapsed_time(ev["prefill"]) for ev in evs]
+    sel_ms = [ev["sel"][e].elapsed_time(ev["att"][e]) for ev in evs for e in range(E)]
+    att_ms = [ev["att"][e].elapsed_time(ev["end"][e]) for ev in evs for e in range(E)]
+    dec_ms = [ev["sel"][e].elapsed_time(ev["end"][e]) for ev in evs for e in range(E)]
+    mean = lambda x: sum(x) / len(x)
+    dec_us = mean(dec_ms) * 1e3
+    att_us = mean(att_ms) * 1e3
+    sel_us = mean(sel_ms) * 1e3
+
+    owners = [l for l in range(w.n_layers) if M.owner_layer(l, w.share_period, w.share_start) == l]
+    sel_b, att_b = decode_bytes(w, owners, path.sel.cpu().numpy(), path.C, path.S)
+    step_b = sel_b + att_b
+    digest = source_digest("decode_attn.hip", "decode_attn.h", "common.h")
+    traffic = measured_traffic("sparse_decode", args.workload, digest)
+    att_gbs = att_b / (att_us * 1e-6) / 1e9
+    dec_gbs = step_b / (dec_us * 1e-6) / 1e9
+    fl = prefill_flops(w, len(owners))
+    pre_tflops = fl / (mean(pre_ms) * 1e-3) / 1e12
+
+    rec = {
+        "metric": METRIC,
+        "value": round(dec_us / w.n_layers, 4),
+        "unit": "us/layer",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall / args.steps * 1e3, 3),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic (seeded generator, device-resident before timing)",
+        "config": {"workload": f"{args.workload} {w.name}", "layers": w.n_layers, "batch": w.batch,
+                   "q_heads": w.n_q_heads, "kv_heads": w.n_kv_heads, "head_dim": w.head_dim, "prompt_tokens": w.T,
+                   "window_rows": w.window, "kept_tokens": w.keep, "cluster": w.cluster, "fanout": w.fanout,
+                   "k_super": w.k_super, "k_clusters": w.k_clusters, "share_period": w.share_period,
+                   "decode_steps_per_pass": E},
+        "decode_step": {"us": round(dec_us, 3), "select_us": round(sel_us, 3), "attention_us": round(att_us, 3),
+                        "algorithmic_bytes": step_b, "achieved_GBps": round(dec_gbs, 1),
+                        "frac_of_hbm_peak": round(dec_gbs / HBM_PEAK_GBS, 4)},
+        "roofline": {"kernel": "k_sparse_decode (gather + online-softmax attention, all layers per launch)",
+                     "bound": "hbm", "achieved": round(att_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(att_gbs / HBM_PEAK_GBS, 4), "traffic": traffic,
+                     "algorithmic_bytes_per_launch": att_b, "avg_launch_us": round(att_us, 3)},
+        "prefill": {"ms_per_pass": round(mean(pre_ms), 3), "owner_layers": len(owners),
+                    "ms_per_owner_layer": round(mean(pre_ms) / len(owners), 3),
+                    "algorithmic_TFLOP_per_pass": round(fl / 1e12, 3),
+                    "achieved_TFLOPs": round(pre_tflops, 1),
+                    "frac_of_mfma_peak": round(pre_tflops / MFMA_PEAK_TFLOPS[w.dtype], 4),
+                    "note": "static eviction (two score passes, top-k, gather) + cluster build, all layers"},
+    }
+    if not args.no_cpu_baseline:
+        rec["cpu_baseline"] = cpu_baseline(w, min(E, 64))
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,153 @@
+"""Full-size GPU runs (the launch configurations the benchmark times) checked on sampled outputs
+the oracle can compute one by one, and on properties that hold at any size.
+
+Inputs are generated on the device; the oracle's inputs for a sampled layer are regenerated on the
+host by the same generator (bit-identical, see test_gpu_synth.py).
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from gpu_util import assert_out_close, assert_sets_tie_equal, boundary_score, random_sel, say, to_f64
+
+pytestmark = pytest.mark.gpu
+
+FULL = ["C3", "C4", "C5"]
+
+
+def _path(w, T, keep_scores=False):
+    import paper_2501_06807_amd as M
+    return M.MPCachePath(n_layers=w.n_layers, batch=w.batch, n_q_heads=w.n_q_heads, n_kv_heads=w.n_kv_heads,
+                         head_dim=w.head_dim, dtype=synth.torch_dtype(w.dtype), T=T, window=w.window,
+                         keep=w.keep, local_keep=w.local_keep, cluster=w.cluster, fanout=w.fanout,
+                         k_super=w.k_super, k_clusters=w.k_clusters, share_period=w.share_period,
+                         share_start=w.share_start, keep_scores=keep_scores)
+
+
+def _owner(w, l):
+    return oracle.owner_layer(l, w.share_period, w.share_start) == l
+
+
+@pytest.mark.parametrize("name", FULL)
+def test_fullsize_static_eviction(name):
+    w = synth.get(name)
+    say(f"[full evict] {name} {w.name}")
+    sp = synth.spec(w)
+    rope = synth.rope_dev(w.T, w.head_dim, w.rope_base) if w.rope else None
+    q_win = synth.qwin_dev(sp, w.dtype, 0, w.n_layers, rope)
+    k, v = synth.kv_dev(sp, w.dtype, 0, w.n_layers, q_win, rope)
+    del rope
+    path = _path(w, w.T, keep_scores=True)
+    path.prefill(q_win, k, v)
+    torch.cuda.synchronize()
+    say("  prefill done")
+    G, loc = w.group, w.local_keep
+    owners = [l for l in range(w.n_layers) if _owner(w, l)]
+    sc = path.token_score[owners].double()
+    # every window row's softmax sums to one: the scores of a kv head sum to G * W
+    tot = sc.sum(-1)
+    assert torch.all((tot - G * w.window).abs() <= 1e-5 * G * w.window), tot.flatten()[:4]
+    kept = path.kept.long()
+    n_sel = w.keep - loc
+    assert torch.all(kept[..., 1:] > kept[..., :-1])
+    assert torch.all(kept[..., n_sel:] == torch.arange(w.T - loc, w.T, device="cuda"))
+    # the kept set is the top-(keep - local) of the GPU's own scores, ties to the lower position
+    s32 = path.token_score[owners][..., :w.T - loc]
+    chosen = torch.zeros_like(s32, dtype=torch.bool)
+    chosen.scatter_(-1, kept[owners][..., :n_sel], True)
+    min_in = torch.where(chosen, s32, torch.full_like(s32, float("inf"))).amin(-1, keepdim=True)
+    max_out = torch.where(chosen, torch.full_like(s32, -1.0), s32).amax(-1, keepdim=True)
+    assert torch.all(min_in >= max_out)
+    idx = torch.arange(w.T - loc, device="cuda").expand_as(s32)
+    last_in_tie = torch.where(chosen & (s32 == min_in), idx, torch.full_like(idx, -1)).amax(-1)
+    first_out_tie = torch.where(~chosen & (s32 == min_in), idx, torch.full_like(idx, w.T)).amin(-1)
+    assert torch.all(last_in_tie < first_out_tie)
+    # non-owner layers use their owner's kept set; every layer gathers its own rows
+    for l in range(w.n_layers):
+        o = oracle.owner_layer(l, w.share_period, w.share_start)
+        assert torch.equal(path.kept[l], path.kept[o])
+        gi = kept[l].unsqueeze(-1).expand(-1, -1, -1, w.head_dim)
+        assert torch.equal(path.k_s[l], torch.gather(k[l], 2, gi))
+        assert torch.equal(path.v_s[l], torch.gather(v[l], 2, gi))
+    say("  invariants ok")
+    # one owner layer regenerated on the host: sampled window rows against the oracle
+    l = owners[-1]
+    qw_h, k_h, _ = synth.prefill_host(w, l)
+    lse = path.row_lse[l].cpu().numpy()
+    sm = 1.0 / math.sqrt(w.head_dim)
+    rng = np.random.default_rng(11)
+    for _ in range(6):
+        b, hq, t = rng.integers(w.batch), rng.integers(w.n_q_heads), rng.integers(w.window)
+        ref = oracle.row_lse(qw_h[b, hq, t], int(t), w.window, k_h[b, hq // G], w.dtype, sm)
+        assert abs(lse[b, hq, t] - ref) <= 2e-6 * max(1.0, abs(ref)), (l, b, hq, t, lse[b, hq, t], ref)
+    if name == "C3":
+        # full oracle token scores for two heads of that layer
+        for h in (0, w.n_kv_heads - 1):
+            ref = oracle.token_scores(qw_h[0, h * G:(h + 1) * G], k_h[0, h], w.dtype, sm)
+            got = path.token_score[l, 0, h].cpu().numpy()
+            np.testing.assert_allclose(got, ref, rtol=2e-5)
+            kept_r = oracle.static_topk(ref, w.keep, loc)
+            bnd = boundary_score(ref[:w.T - loc], n_sel)
+            assert_sets_tie_equal(path.kept[l, 0, h].cpu().numpy(), kept_r, ref, bnd, f"C3 layer {l} head {h}")
+    say("  sampled rows ok")
+
+
+@pytest.mark.parametrize("name", FULL)
+def test_fullsize_decode(name):
+    w = synth.get(name)
+    say(f"[full decode] {name} {w.name}")
+    sp = synth.spec(w, T=w.keep, W=0, planting=False)
+    rope = synth.rope_dev(w.keep, w.head_dim, w.rope_base) if w.rope else None
+    path = _path(w, w.keep)
+    synth.kv_dev(sp, w.dtype, 0, w.n_layers, None, rope, out=(path.k_s, path.v_s))
+    del rope
+    import paper_2501_06807_amd as M
+    M.mpc_build_clusters(path.k_s, path.cent, path.scent, path.cfg)
+    q_sp = synth.spec(w)
+    q = synth.dq_dev(q_sp, w.dtype, 5)
+    path.select(q)
+    torch.cuda.synchronize()
+    say("  build + select done")
+    owners = [l for l in range(w.n_layers) if _owner(w, l)]
+    C = path.C
+    # sampled owner layer: host-regenerated cache -> oracle representatives and selection
+    l = owners[len(owners) // 2]
+    k_h, v_h = synth.cache_host(w, l)
+    cent_r, scent_r = oracle.build_clusters(k_h[None], w.dtype, cluster=w.cluster, fanout=w.fanout)
+    assert np.array_equal(path.cent[l].cpu().numpy(), cent_r[0])
+    assert np.array_equal(path.scent[l].cpu().numpy(), scent_r[0])
+    q_h = synth.dq_host(q_sp, 5, w.dtype)
+    sel_r, _ = oracle.select_clusters(q_h[l:l + 1], cent_r, scent_r, w.dtype, Ts=w.keep, cluster=w.cluster,
+                                      fanout=w.fanout, k_super=w.k_super, k_clusters=w.k_clusters)
+    sel_g = path.sel[l].cpu().numpy()
+    G = w.group
+    for b in range(w.batch):
+        for h in range(w.n_kv_heads):
+            if not np.array_equal(sel_g[b, h], sel_r[0, b, h]):
+                s_all = oracle.cluster_scores(q_h[l, b, h * G:(h + 1) * G], cent_r[0, b, h], w.dtype)
+                assert_sets_tie_equal(sel_g[b, h], sel_r[0, b, h], s_all, boundary_score(s_all[sel_r[0, b, h]],
+                                                                                          w.k_clusters),
+                                      f"layer {l} b {b} h {h}")
+    for l2 in range(w.n_layers):
+        assert torch.equal(path.sel[l2], path.sel[oracle.owner_layer(l2, w.share_period, w.share_start)])
+    say("  selection ok")
+    # attention at full size with a host-made selection; sampled units against the oracle
+    rng = np.random.default_rng(3)
+    sel = random_sel(rng, w.n_layers * w.batch * w.n_kv_heads, C, w.k_clusters).reshape(path.sel.shape)
+    path.sel.copy_(torch.from_numpy(sel))
+    path.attend(q)
+    torch.cuda.synchronize()
+    out = to_f64(path.out[l])
+    sm = 1.0 / math.sqrt(w.head_dim)
+    for b in range(w.batch):
+        for hq in rng.choice(w.n_q_heads, 4, replace=False):
+            h = hq // G
+            rows = np.concatenate([np.arange(c * w.cluster, min(w.keep, (c + 1) * w.cluster)) for c in sel[l, b, h]])
+            ref, lse_ref = oracle.attend(q_h[l, b, hq], rows, k_h[b, h], v_h[b, h], w.dtype, sm)
+            assert_out_close(out[b, hq][None], ref[None], w.dtype, f"layer {l} b {b} q-head {hq}")
+            assert abs(path.lse[l, b, hq].item() - lse_ref) <= 1e-5 * max(1.0, abs(lse_ref))
+    say("  attention ok")
