@@ -21,12 +21,12 @@
  *     pairing of Alg. 3).
  *   - The library allocates nothing and keeps no global state except a thread-local message for
  *     the last error. Scratch memory is a caller-provided workspace of mpc_workspace_bytes()
- *     bytes; it must be zero-filled once before its first use, and every completed call leaves
- *     the parts that must start at zero zeroed again. Calls that share one workspace must not
- *     overlap in time.
+ *     bytes (no initial contents needed). Calls that share one workspace must not overlap in
+ *     time.
  *   - Every call is asynchronous on `stream` (a hipStream_t; NULL = default stream). The
  *     returned status covers argument validation and launch errors only; it never waits for the
- *     GPU. On any status other than MPC_OK nothing has been enqueued.
+ *     GPU. A validation failure (MPC_EINVAL / ESHAPE / EUNSUPPORTED / EWORKSPACE) enqueues
+ *     nothing; after MPC_EHIP, kernels launched before the failing one may have been enqueued.
  *   - Supported: d in {64, 128}; G in {1, 2, 4, 8}; dtype fp32 / fp16 / bf16.
  */
 #ifndef MPCACHE_H
@@ -123,7 +123,7 @@ mpc_status mpc_build_clusters(const mpc_dims* dims, int32_t Ts, const mpc_select
  * whose owner precedes layer0 is left untouched (the caller copies it).
  *   q [L][B][Hq][d];  cent / scent as produced by mpc_build_clusters;
  *   sel [L][B][Hkv][k_clusters] int32 out;  sel_score same shape, float, optional (score rounded
- *   to fp32). ws may be NULL (no workspace needed). Limits: S <= 1024, k_super * f <= 2048. */
+ *   to fp32). ws may be NULL (no workspace needed). Limits: S <= 1024, k_super * f <= 1024. */
 mpc_status mpc_select_clusters(const mpc_dims* dims, int32_t Ts, const mpc_select_cfg* cfg,
                                const void* q, const float* cent, const float* scent,
                                int32_t* sel, float* sel_score, void* ws, size_t ws_bytes,
@@ -135,8 +135,9 @@ mpc_status mpc_select_clusters(const mpc_dims* dims, int32_t Ts, const mpc_selec
  *   q [L][B][Hq][d];  k_cache, v_cache [L][B][Hkv][Ts][d];  sel [L][B][Hkv][k_clusters] int32
  *   (every entry in [0, C));  out [L][B][Hq][d] (dtype);  lse [L][B][Hq] float, optional
  *   (natural-log log-sum-exp of the scaled scores). fp32 accumulation.
- *   ws: mpc_workspace_bytes(MPC_OP_DECODE_ATTN, dims, Ts, NULL) bytes (split-K partials and
- *   counters); may be NULL when that is 0. */
+ *   ws: mpc_workspace_bytes(MPC_OP_DECODE_ATTN, dims, Ts, NULL) bytes (split-K partials, used
+ *   when there are fewer (layer, sequence, kv head) units than compute units); may be NULL when
+ *   that is 0. */
 mpc_status mpc_sparse_decode_attn(const mpc_dims* dims, int32_t Ts, int32_t cluster_size,
                                   const void* q, const void* k_cache, const void* v_cache,
                                   const int32_t* sel, int32_t k_clusters, float sm_scale,

@@ -49,6 +49,10 @@ mpc_status check_dims(const mpc_dims* d) {
   return MPC_OK;
 }
 
+// Launch errors are read with hipGetLastError(); an error left by an unrelated earlier runtime call
+// on this thread is cleared first so that it is not reported as ours.
+void clear_stale_error() { (void)hipGetLastError(); }
+
 mpc_status launched(hipError_t e, const char* what) {
   if (e != hipSuccess) return fail(MPC_EHIP, "%s launch failed: %s", what, hipGetErrorString(e));
   return MPC_OK;
@@ -66,23 +70,13 @@ EvictWs evict_ws(const mpc_dims* d, int T, int W) {
   return w;
 }
 
-// Decode workspace: split-K partials sized for the largest split count, then counters.
-struct DecodeWs {
-  int splits_max;
-  size_t counters, total;
-};
-DecodeWs decode_ws(const mpc_dims* d) {
+// Decode workspace: split-K partials, sized for the largest split count any token budget gives.
+size_t decode_ws_bytes(const mpc_dims* d) {
   const int units = d->n_layers * d->batch * d->n_kv_heads;
   const int G = d->n_q_heads / d->n_kv_heads;
-  DecodeWs w;
-  w.splits_max = mpc::decode_splits(units, 1 << 30, d->head_dim, elt_size(d->dtype));
-  if (w.splits_max <= 1) {
-    w.counters = w.total = 0;
-    return w;
-  }
-  w.counters = align256((size_t)units * w.splits_max * G * (d->head_dim + 2) * sizeof(float));
-  w.total = w.counters + align256((size_t)units * sizeof(int32_t));
-  return w;
+  const mpc::DecodePlan p = mpc::decode_plan(units, 1 << 30, d->head_dim, elt_size(d->dtype));
+  if (p.splits <= 1) return 0;
+  return align256((size_t)units * p.splits * G * (d->head_dim + 2) * sizeof(float));
 }
 
 }  // namespace
@@ -114,7 +108,7 @@ size_t mpc_workspace_bytes(int32_t op, const mpc_dims* dims, int32_t T_or_Ts, co
     if (!c || c->window <= 0 || c->window > T_or_Ts) return 0;
     return evict_ws(dims, T_or_Ts, c->window).total;
   }
-  if (op == MPC_OP_DECODE_ATTN) return decode_ws(dims).total;
+  if (op == MPC_OP_DECODE_ATTN) return decode_ws_bytes(dims);
   return 0;
 }
 
@@ -137,6 +131,13 @@ mpc_status mpc_static_evict(const mpc_dims* dims, int32_t T, const mpc_evict_cfg
   if (cfg->causal != 0 && cfg->causal != 1) return fail(MPC_EINVAL, "causal must be 0 or 1");
   if ((int64_t)T * dims->head_dim * elt_size(dims->dtype) >= ((int64_t)1 << 31))
     return fail(MPC_EUNSUPPORTED, "T too large");
+  if (dims->n_layers > mpc::kMaxLayers)
+    return fail(MPC_EUNSUPPORTED, "static eviction takes at most %d layers per call", mpc::kMaxLayers);
+  if ((int64_t)dims->n_layers * dims->batch * dims->n_q_heads * ((cfg->window + mpc::kRowBlock - 1) / mpc::kRowBlock) >=
+          ((int64_t)1 << 31) ||
+      (int64_t)dims->n_layers * dims->batch * dims->n_kv_heads * ((T + mpc::kColBlockKeys - 1) / mpc::kColBlockKeys) >=
+          ((int64_t)1 << 31))
+    return fail(MPC_EUNSUPPORTED, "grid too large");
   const EvictWs lay = evict_ws(dims, T, cfg->window);
   if (!ws || ws_bytes < lay.total)
     return fail(MPC_EWORKSPACE, "static eviction needs %zu workspace bytes", lay.total);
@@ -163,14 +164,18 @@ mpc_status mpc_static_evict(const mpc_dims* dims, int32_t T, const mpc_evict_cfg
   a.causal = cfg->causal;
   a.period = cfg->share_period;
   a.start = cfg->share_start;
+  a.own = mpc::owner_table(dims->layer0, dims->n_layers, cfg->share_period, cfg->share_start);
   a.c64 = (double)cfg->sm_scale * 1.4426950408889634;
   a.c_hi = (float)a.c64;
   a.c_lo = (float)(a.c64 - (double)a.c_hi);
   hipStream_t st = (hipStream_t)stream;
   const int D = dims->head_dim, dt = dims->dtype;
-  if ((s = launched(mpc::launch_rowstats(a, dt, D, st), "row statistics")) != MPC_OK) return s;
-  if ((s = launched(mpc::launch_colsum(a, dt, D, st), "column sums")) != MPC_OK) return s;
-  if ((s = launched(mpc::launch_topk(a, st), "top-k")) != MPC_OK) return s;
+  clear_stale_error();
+  if (a.own.n > 0) {
+    if ((s = launched(mpc::launch_rowstats(a, dt, D, st), "row statistics")) != MPC_OK) return s;
+    if ((s = launched(mpc::launch_colsum(a, dt, D, st), "column sums")) != MPC_OK) return s;
+    if ((s = launched(mpc::launch_topk(a, st), "top-k")) != MPC_OK) return s;
+  }
   if ((s = launched(mpc::launch_gather(a, dt, D, st), "gather")) != MPC_OK) return s;
   return ok();
 }
@@ -203,8 +208,12 @@ mpc_status mpc_build_clusters(const mpc_dims* dims, int32_t Ts, const mpc_select
   a.start = cfg->share_start;
   a.alpha = cfg->alpha;
   a.beta = (float)(1.0 - (double)cfg->alpha);
+  if (a.n_layers > mpc::kMaxLayers) return fail(MPC_EUNSUPPORTED, "at most %d layers per call", mpc::kMaxLayers);
   if ((int64_t)a.n_layers * a.B * a.Hkv * a.S >= ((int64_t)1 << 31))
     return fail(MPC_EUNSUPPORTED, "grid too large");
+  a.own = mpc::owner_table(a.layer0, a.n_layers, a.period, a.start);
+  if (a.own.n == 0) return ok();
+  clear_stale_error();
   if ((s = launched(mpc::launch_build(a, dims->dtype, dims->head_dim, (hipStream_t)stream), "build")) != MPC_OK)
     return s;
   return ok();
@@ -249,6 +258,10 @@ mpc_status mpc_select_clusters(const mpc_dims* dims, int32_t Ts, const mpc_selec
   a.k_clusters = cfg->k_clusters;
   a.period = cfg->share_period;
   a.start = cfg->share_start;
+  if (a.n_layers > mpc::kMaxLayers) return fail(MPC_EUNSUPPORTED, "at most %d layers per call", mpc::kMaxLayers);
+  a.own = mpc::owner_table(a.layer0, a.n_layers, a.period, a.start);
+  if (a.own.n == 0) return ok();
+  clear_stale_error();
   if ((s = launched(mpc::launch_select(a, dims->dtype, dims->head_dim, (hipStream_t)stream), "select")) != MPC_OK)
     return s;
   return ok();
@@ -273,10 +286,11 @@ mpc_status mpc_sparse_decode_attn(const mpc_dims* dims, int32_t Ts, int32_t clus
   if (k_clusters > 1024) return fail(MPC_EUNSUPPORTED, "k_clusters above 1024");
   if ((int64_t)k_clusters * cluster_size >= ((int64_t)1 << 30)) return fail(MPC_EUNSUPPORTED, "too many tokens");
   const int units = dims->n_layers * dims->batch * dims->n_kv_heads;
-  const DecodeWs lay = decode_ws(dims);
-  const int splits = mpc::decode_splits(units, k_clusters * cluster_size, dims->head_dim, elt_size(dims->dtype));
-  if (splits > 1 && (!ws || ws_bytes < lay.total))
-    return fail(MPC_EWORKSPACE, "sparse decode attention needs %zu workspace bytes", lay.total);
+  const mpc::DecodePlan plan =
+      mpc::decode_plan(units, k_clusters * cluster_size, dims->head_dim, elt_size(dims->dtype));
+  const size_t need = decode_ws_bytes(dims);
+  if (plan.splits > 1 && (!ws || ws_bytes < need))
+    return fail(MPC_EWORKSPACE, "sparse decode attention needs %zu workspace bytes", need);
   mpc::DecodeArgs a{};
   a.q = q;
   a.k = k_cache;
@@ -284,16 +298,17 @@ mpc_status mpc_sparse_decode_attn(const mpc_dims* dims, int32_t Ts, int32_t clus
   a.sel = sel;
   a.out = out;
   a.lse = lse;
-  a.part = splits > 1 ? (float*)ws : nullptr;
-  a.counters = splits > 1 ? (int32_t*)((char*)ws + lay.counters) : nullptr;
+  a.part = plan.splits > 1 ? (float*)ws : nullptr;
   a.Ts = Ts;
   a.s = cluster_size;
+  a.C = C;
   a.k_sel = k_clusters;
   a.Hq = dims->n_q_heads;
   a.Hkv = dims->n_kv_heads;
-  a.splits = splits;
+  a.splits = plan.splits;
   a.qscale = (float)((double)sm_scale * 1.4426950408889634);
-  if ((s = launched(mpc::launch_sparse_decode(a, dims->dtype, dims->head_dim, G, units, (hipStream_t)stream),
+  clear_stale_error();
+  if ((s = launched(mpc::launch_sparse_decode(a, dims->dtype, dims->head_dim, G, units, plan.waves, (hipStream_t)stream),
                     "sparse decode attention")) != MPC_OK)
     return s;
   return ok();

@@ -10,6 +10,7 @@ struct BuildArgs {
   float* scent;    // [L][B][Hkv][S][d]
   int B, layer0, n_layers, Hkv, Ts, s, f, C, S, period, start;
   float alpha, beta;  // beta = fp32(1 - alpha)
+  OwnerTable own;
 };
 
 hipError_t launch_build(const BuildArgs& a, int dtype, int D, hipStream_t st);

@@ -20,10 +20,9 @@ __global__ __launch_bounds__(NW* kWave) void k_build(BuildArgs a) {
   __shared__ float s_max[NW][D], s_min[NW][D];
 
   const int sup = blockIdx.x % a.S;
-  const int unit = blockIdx.x / a.S;
-  const int l = unit / (a.B * a.Hkv);
-  const int abs_l = a.layer0 + l;
-  if (owner_layer(abs_l, a.period, a.start) != abs_l) return;
+  const int ou = blockIdx.x / a.S;  // (owner index * B + b) * Hkv + h
+  const int l = a.own.l[ou / (a.B * a.Hkv)];
+  const size_t unit = (size_t)l * a.B * a.Hkv + ou % (a.B * a.Hkv);
   const int tid = threadIdx.x, lane = tid % kWave, w = tid / kWave;
   const int rg = lane / LPR, li = lane % LPR;
   const char* kh = (const char*)a.k + (size_t)unit * a.Ts * D * DT::kElt;
@@ -106,7 +105,7 @@ hipError_t launch_dt(const BuildArgs& a, int D, int blocks, hipStream_t st) {
 }  // namespace
 
 hipError_t launch_build(const BuildArgs& a, int dtype, int D, hipStream_t st) {
-  const int blocks = a.n_layers * a.B * a.Hkv * a.S;
+  const int blocks = a.own.n * a.B * a.Hkv * a.S;
   switch (dtype) {
     case MPC_FP32: return launch_dt<F32>(a, D, blocks, st);
     case MPC_FP16: return launch_dt<F16>(a, D, blocks, st);

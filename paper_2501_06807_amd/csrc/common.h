@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "../../include/mpcache.h"
 
 namespace mpc {
@@ -114,6 +116,21 @@ __host__ __device__ __forceinline__ int owner_layer(int l, int period, int start
   return start + period * ((l - start) / period);
 }
 
+constexpr int kMaxLayers = 256;  // layers per call
+
+// Local indices of the owner layers of a block of layers, so that grids cover owner work only.
+struct OwnerTable {
+  int n;
+  int16_t l[kMaxLayers];
+};
+
+inline OwnerTable owner_table(int layer0, int n_layers, int period, int start) {
+  OwnerTable t{};
+  for (int l = 0; l < n_layers && l < kMaxLayers; ++l)
+    if (owner_layer(layer0 + l, period, start) == layer0 + l) t.l[t.n++] = (int16_t)l;
+  return t;
+}
+
 template <class T>
 __device__ __forceinline__ T wave_sum(T v) {
 #pragma unroll
@@ -122,5 +139,51 @@ __device__ __forceinline__ T wave_sum(T v) {
 }
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Data-parallel-primitive (DPP) lane moves: plain VALU operations, no LDS round trip.
+//   0x121..0x12F  row_ror:1..15   rotate right within each row of 16 lanes
+//   0x141         row_half_mirror reverse the order within each half-row of 8 lanes
+//   0x4E / 0xB1   quad_perm       lane ^ 2 / lane ^ 1 within each quad
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double x) {
+  const int lo = __builtin_amdgcn_update_dpp(0, __double2loint(x), CTRL, 0xF, 0xF, false);
+  const int hi = __builtin_amdgcn_update_dpp(0, __double2hiint(x), CTRL, 0xF, 0xF, false);
+  return __hiloint2double(hi, lo);
+}
+
+// Sum over aligned groups of N consecutive lanes; every lane of a group receives its group's sum.
+// Each step adds a lane permutation that pairs partial sums, so after log2(N) steps every lane
+// has seen all N inputs (rotations by 8, 4, 2, 1 within 16 lanes; mirror + quad swaps within 8).
+template <int N, class T>
+__device__ __forceinline__ T group_sum(T x) {
+  static_assert(N == 1 || N == 2 || N == 4 || N == 8 || N == 16 || N == 32 || N == 64, "group size");
+  auto mv = [](auto v, auto ctrl_tag) {
+    constexpr int C = decltype(ctrl_tag)::value;
+    if constexpr (sizeof(T) == 8) return dpp_f64<C>(v); else return dpp_f32<C>(v);
+  };
+  using I = int;
+  if constexpr (N == 2) {
+    x += mv(x, std::integral_constant<I, 0xB1>{});
+  } else if constexpr (N == 4) {
+    x += mv(x, std::integral_constant<I, 0x4E>{});
+    x += mv(x, std::integral_constant<I, 0xB1>{});
+  } else if constexpr (N == 8) {
+    x += mv(x, std::integral_constant<I, 0x141>{});
+    x += mv(x, std::integral_constant<I, 0x4E>{});
+    x += mv(x, std::integral_constant<I, 0xB1>{});
+  } else if constexpr (N >= 16) {
+    x += mv(x, std::integral_constant<I, 0x128>{});
+    x += mv(x, std::integral_constant<I, 0x124>{});
+    x += mv(x, std::integral_constant<I, 0x122>{});
+    x += mv(x, std::integral_constant<I, 0x121>{});
+    if constexpr (N >= 32) x += __shfl_xor(x, 16);
+    if constexpr (N == 64) x += __shfl_xor(x, 32);
+  }
+  return x;
+}
 
 }  // namespace mpc

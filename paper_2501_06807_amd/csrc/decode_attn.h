@@ -4,8 +4,8 @@
 
 namespace mpc {
 
-constexpr int kDecodeWaves = 8;          // waves per workgroup
-constexpr int kDecodeTargetBlocks = 1024; // split-K aims for at least this many workgroups
+constexpr int kNumCU = 256;      // compute units of an MI355X
+constexpr int kMaxSplits = 16;   // split-K limit (workspace bound)
 
 struct DecodeArgs {
   const void* q;       // [L][B][Hq][d]
@@ -15,13 +15,16 @@ struct DecodeArgs {
   void* out;           // [L][B][Hq][d]
   float* lse;          // [L][B][Hq] or null
   float* part;         // split-K partials [units][splits][G][d + 2]
-  int32_t* counters;   // [units], zero between calls
-  int Ts, s, k_sel, Hq, Hkv, splits;
+  int Ts, s, C, k_sel, Hq, Hkv, splits;  // C = ceil(Ts / s)
   float qscale;        // sm_scale * log2(e)
 };
 
-int decode_splits(int units, int n_slot, int D, int elt);
-hipError_t launch_sparse_decode(const DecodeArgs& a, int dtype, int D, int G, int units,
+struct DecodePlan {
+  int waves;   // waves per workgroup
+  int splits;  // workgroups per unit
+};
+DecodePlan decode_plan(int units, int n_slot, int D, int elt);
+hipError_t launch_sparse_decode(const DecodeArgs& a, int dtype, int D, int G, int units, int waves,
                                 hipStream_t st);
 
 }  // namespace mpc

@@ -2,7 +2,7 @@
 //
 // One work unit = (layer, sequence, kv head). Its token list is the concatenation of the
 // selected clusters' rows of the kept cache. A unit may be split over several workgroups
-// (split-K); each writes an (m, l, acc) partial and the last one to finish merges them.
+// (split-K); each writes an (m, l, acc) partial and a second launch merges them.
 //
 // Lane layout: a K/V row of d elements is read as 16-byte vectors by LPR consecutive lanes, so a
 // wave reads RPW = 64 / LPR rows per load instruction, fully coalesced. The G query heads of the
@@ -25,7 +25,6 @@ __global__ __launch_bounds__(NW* kWave) void k_sparse_decode(DecodeArgs a) {
   __shared__ int32_t s_sel[kMaxSel];
   __shared__ float s_m[NW][G], s_l[NW][G];
   __shared__ float s_acc[NW][G][D];
-  __shared__ int s_last;
 
   const int unit = blockIdx.x / a.splits;
   const int split = blockIdx.x % a.splits;
@@ -66,17 +65,14 @@ __global__ __launch_bounds__(NW* kWave) void k_sparse_decode(DecodeArgs a) {
     bool ok[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
+      // slot -> (selected cluster, row in cluster); ids come from the caller, so anything outside
+      // [0, C) or past the kept length contributes nothing (and loads row 0 harmlessly)
       const int sl = base + (u * NW + w) * RPW + rg;
-      int row = 0;
-      ok[u] = sl < hi;
-      if (ok[u]) {
-        // cluster ids come from the caller: anything outside [0, C) contributes nothing
-        const int c = s_sel[sl / a.s];
-        const long long r = (long long)c * a.s + sl % a.s;
-        ok[u] = c >= 0 && r < a.Ts;
-        row = ok[u] ? (int)r : 0;
-      }
-      const size_t off = ((size_t)row * D + li * EPL) * DT::kElt;
+      const int slc = min(sl, hi - 1);
+      const int c = s_sel[slc / a.s];
+      const int r = c * a.s + slc % a.s;
+      ok[u] = (sl < hi) & ((unsigned)c < (unsigned)a.C) & (r < a.Ts);
+      const size_t off = ((size_t)(ok[u] ? r : 0) * D + li * EPL) * DT::kElt;
       kr[u] = ldg16(kbase + off);
       vr[u] = ldg16(vbase + off);
     }
@@ -90,8 +86,7 @@ __global__ __launch_bounds__(NW* kWave) void k_sparse_decode(DecodeArgs a) {
         float p = 0.f;
 #pragma unroll
         for (int e = 0; e < EPL; ++e) p += qf[g][e] * kf[e];
-#pragma unroll
-        for (int o = LPR / 2; o > 0; o >>= 1) p += __shfl_xor(p, o);
+        p = group_sum<LPR>(p);
         sc[u][g] = ok[u] ? p : -INFINITY;
       }
     }
@@ -172,79 +167,85 @@ __global__ __launch_bounds__(NW* kWave) void k_sparse_decode(DecodeArgs a) {
       }
     }
   }
-  if (a.splits == 1) return;
+}
 
-  // split-K: the last workgroup of the unit to finish merges the partials
-  __threadfence();
-  __syncthreads();
-  if (tid == 0) s_last = atomicAdd(&a.counters[unit], 1) == a.splits - 1;
-  __syncthreads();
-  if (!s_last) return;
-  __threadfence();
-  for (int t = tid; t < G * D; t += NW * kWave) {
-    const int g = t / D, dim = t % D;
-    const float* p0 = a.part + ((size_t)unit * a.splits * G + g) * (D + 2);
-    const size_t stride = (size_t)G * (D + 2);
-    float M = -1e30f;
-    for (int i = 0; i < a.splits; ++i) M = fmaxf(M, __builtin_nontemporal_load(p0 + i * stride + D));
-    float L = 0.f, O = 0.f;
-    for (int i = 0; i < a.splits; ++i) {
-      const float* p = p0 + i * stride;
-      const float r = fast_exp2(__builtin_nontemporal_load(p + D) - M);
-      L += __builtin_nontemporal_load(p + D + 1) * r;
-      O += __builtin_nontemporal_load(p + dim) * r;
-    }
-    store_elt<DT>(a.out, (q_row0 + g) * D + dim, O / L);
-    if (dim == 0 && a.lse) a.lse[q_row0 + g] = (M + __log2f(L)) * 0.69314718055994531f;
+// Split-K merge: one workgroup per (unit, q-head of the group) combines the splits' partials.
+// Runs as its own launch, so the partials are visible without any cross-workgroup fence.
+template <class DT, int D, int G>
+__global__ __launch_bounds__(D) void k_merge(DecodeArgs a) {
+  const int unit = blockIdx.x / G, g = blockIdx.x % G, dim = threadIdx.x;
+  const size_t q_row = (size_t)(unit / a.Hkv) * a.Hq + (size_t)(unit % a.Hkv) * G + g;
+  const float* p0 = a.part + ((size_t)unit * a.splits * G + g) * (D + 2);
+  const size_t stride = (size_t)G * (D + 2);
+  float M = -1e30f;
+  for (int i = 0; i < a.splits; ++i) M = fmaxf(M, p0[i * stride + D]);
+  float L = 0.f, O = 0.f;
+  for (int i = 0; i < a.splits; ++i) {
+    const float* p = p0 + i * stride;
+    const float r = fast_exp2(p[D] - M);
+    L += p[D + 1] * r;
+    O += p[dim] * r;
   }
-  if (tid == 0) a.counters[unit] = 0;
+  store_elt<DT>(a.out, q_row * D + dim, O / L);
+  if (dim == 0 && a.lse) a.lse[q_row] = (M + __log2f(L)) * 0.69314718055994531f;
 }
 
 template <class DT, int D, int G>
-hipError_t launch_dt_d_g(const DecodeArgs& a, int units, hipStream_t st) {
-  constexpr int NW = kDecodeWaves, U = 4;
-  hipLaunchKernelGGL((k_sparse_decode<DT, D, G, NW, U>), dim3(units * a.splits), dim3(NW * kWave), 0,
-                     st, a);
+hipError_t launch_dt_d_g(const DecodeArgs& a, int units, int waves, hipStream_t st) {
+  if (waves == 16)
+    hipLaunchKernelGGL((k_sparse_decode<DT, D, G, 16, 4>), dim3(units * a.splits), dim3(16 * kWave), 0, st, a);
+  else
+    hipLaunchKernelGGL((k_sparse_decode<DT, D, G, 8, 4>), dim3(units * a.splits), dim3(8 * kWave), 0, st, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || a.splits == 1) return e;
+  hipLaunchKernelGGL((k_merge<DT, D, G>), dim3(units * G), dim3(D), 0, st, a);
   return hipGetLastError();
 }
 
 template <class DT, int D>
-hipError_t launch_dt_d(const DecodeArgs& a, int G, int units, hipStream_t st) {
+hipError_t launch_dt_d(const DecodeArgs& a, int G, int units, int waves, hipStream_t st) {
   switch (G) {
-    case 1: return launch_dt_d_g<DT, D, 1>(a, units, st);
-    case 2: return launch_dt_d_g<DT, D, 2>(a, units, st);
-    case 4: return launch_dt_d_g<DT, D, 4>(a, units, st);
-    case 8: return launch_dt_d_g<DT, D, 8>(a, units, st);
+    case 1: return launch_dt_d_g<DT, D, 1>(a, units, waves, st);
+    case 2: return launch_dt_d_g<DT, D, 2>(a, units, waves, st);
+    case 4: return launch_dt_d_g<DT, D, 4>(a, units, waves, st);
+    case 8: return launch_dt_d_g<DT, D, 8>(a, units, waves, st);
   }
   return hipErrorInvalidValue;
 }
 
 template <class DT>
-hipError_t launch_dt(const DecodeArgs& a, int D, int G, int units, hipStream_t st) {
-  if (D == 64) return launch_dt_d<DT, 64>(a, G, units, st);
-  if (D == 128) return launch_dt_d<DT, 128>(a, G, units, st);
+hipError_t launch_dt(const DecodeArgs& a, int D, int G, int units, int waves, hipStream_t st) {
+  if (D == 64) return launch_dt_d<DT, 64>(a, G, units, waves, st);
+  if (D == 128) return launch_dt_d<DT, 128>(a, G, units, waves, st);
   return hipErrorInvalidValue;
 }
 
 }  // namespace
 
-int decode_splits(int units, int n_slot, int D, int elt) {
-  const int lpr = D * elt / 16;
-  const int rows_per_pass = kDecodeWaves * (kWave / lpr);
-  int max_splits = n_slot / rows_per_pass;
-  if (max_splits < 1) max_splits = 1;
-  int s = (kDecodeTargetBlocks + units - 1) / units;
-  if (s > max_splits) s = max_splits;
-  if (s > 64) s = 64;
-  return s < 1 ? 1 : s;
+DecodePlan decode_plan(int units, int n_slot, int D, int elt) {
+  // One 8-wave workgroup per unit when there are at least as many units as CUs; otherwise the
+  // token list of each unit is split over several workgroups.
+  DecodePlan p;
+  p.waves = 8;
+  p.splits = 1;
+  if (units < kNumCU) {
+    const int lpr = D * elt / 16;
+    const int rows_per_pass = p.waves * (kWave / lpr);
+    int max_splits = n_slot / rows_per_pass;
+    if (max_splits < 1) max_splits = 1;
+    p.splits = (2 * kNumCU + units - 1) / units;
+    if (p.splits > max_splits) p.splits = max_splits;
+    if (p.splits > kMaxSplits) p.splits = kMaxSplits;
+  }
+  return p;
 }
 
-hipError_t launch_sparse_decode(const DecodeArgs& a, int dtype, int D, int G, int units,
+hipError_t launch_sparse_decode(const DecodeArgs& a, int dtype, int D, int G, int units, int waves,
                                 hipStream_t st) {
   switch (dtype) {
-    case MPC_FP32: return launch_dt<F32>(a, D, G, units, st);
-    case MPC_FP16: return launch_dt<F16>(a, D, G, units, st);
-    case MPC_BF16: return launch_dt<BF16>(a, D, G, units, st);
+    case MPC_FP32: return launch_dt<F32>(a, D, G, units, waves, st);
+    case MPC_FP16: return launch_dt<F16>(a, D, G, units, waves, st);
+    case MPC_BF16: return launch_dt<BF16>(a, D, G, units, waves, st);
   }
   return hipErrorInvalidValue;
 }

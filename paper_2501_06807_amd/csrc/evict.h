@@ -4,6 +4,7 @@
 
 namespace mpc {
 
+constexpr int kNumXcd = 8;       // accelerator dies; workgroup i runs on die i % 8
 constexpr int kRowBlock = 128;  // window rows per row-statistics workgroup (4 waves x 32)
 constexpr int kColWaveKeys = 64;  // keys per wave in the column-sum pass (2 MFMA column blocks)
 constexpr int kColBlockKeys = 4 * kColWaveKeys;
@@ -19,6 +20,7 @@ struct EvictArgs {
   double* rowstat;     // [L][B][Hq][W]: -(c * max + log2(sum)) per window row
   float* row_lse;      // [L][B][Hq][W] natural log-sum-exp, optional
   int B, layer0, n_layers, Hq, Hkv, T, W, keep, local_keep, causal, period, start;
+  OwnerTable own;      // owner layers of the block
   float c_hi, c_lo;    // sm_scale * log2(e) as an unevaluated fp32 sum
   double c64;          // the same in fp64
 };

@@ -61,6 +61,14 @@ __device__ __forceinline__ int acc_row(int r, int lane) {
   return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
 }
 
+// Workgroup ids are dealt round-robin over the dies; renumber them so that each die gets one
+// contiguous range of work items (all tiles of a head share that die's L2).
+__device__ __forceinline__ int xcd_remap(int bid, int n) {
+  const int q = n / kNumXcd, r = n % kNumXcd;
+  const int x = bid % kNumXcd, slot = bid / kNumXcd;
+  return x < r ? x * (q + 1) + slot : r * (q + 1) + (x - r) * q + slot;
+}
+
 // 32-row tiles of a [rows][D] matrix staged through LDS with 16-byte chunks; the row stride is
 // padded by 16 bytes to spread the 32 rows of a fragment read over the LDS banks.
 template <class DT, int D>
@@ -81,11 +89,12 @@ __global__ __launch_bounds__(256) void k_rowstats(EvictArgs a) {
   __shared__ __align__(16) unsigned char s_k[2][TL::BYTES];
 
   const int n_rb = (a.W + kRowBlock - 1) / kRowBlock;
-  const int rb = blockIdx.x % n_rb;
-  const int qunit = blockIdx.x / n_rb;  // (l * B + b) * Hq + hq
-  const int l = qunit / (a.B * a.Hq);
-  if (owner_layer(a.layer0 + l, a.period, a.start) != a.layer0 + l) return;
-  const int b = (qunit / a.Hq) % a.B, hq = qunit % a.Hq;
+  const int id = xcd_remap(blockIdx.x, gridDim.x);
+  const int rb = id % n_rb;
+  const int ou = id / n_rb;  // (owner index * B + b) * Hq + hq
+  const int l = a.own.l[ou / (a.B * a.Hq)];
+  const int b = (ou / a.Hq) % a.B, hq = ou % a.Hq;
+  const size_t qunit = ((size_t)l * a.B + b) * a.Hq + hq;
   const int G = a.Hq / a.Hkv;
   const size_t kvunit = ((size_t)l * a.B + b) * a.Hkv + hq / G;
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, c32 = lane & 31, hl = lane >> 5;
@@ -185,11 +194,12 @@ __global__ __launch_bounds__(256) void k_colsum(EvictArgs a) {
   __shared__ float s_bh[2][32], s_bl[2][32];
 
   const int n_kb = (a.T + kColBlockKeys - 1) / kColBlockKeys;
-  const int kb = blockIdx.x % n_kb;
-  const int kvunit = blockIdx.x / n_kb;  // (l * B + b) * Hkv + h
-  const int l = kvunit / (a.B * a.Hkv);
-  if (owner_layer(a.layer0 + l, a.period, a.start) != a.layer0 + l) return;
-  const int b = (kvunit / a.Hkv) % a.B, h = kvunit % a.Hkv;
+  const int id = xcd_remap(blockIdx.x, gridDim.x);
+  const int kb = id % n_kb;
+  const int ou = id / n_kb;  // (owner index * B + b) * Hkv + h
+  const int l = a.own.l[ou / (a.B * a.Hkv)];
+  const int b = (ou / a.Hkv) % a.B, h = ou % a.Hkv;
+  const size_t kvunit = ((size_t)l * a.B + b) * a.Hkv + h;
   const int G = a.Hq / a.Hkv;
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, c32 = lane & 31, hl = lane >> 5;
 
@@ -323,9 +333,9 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(EvictArgs a) {
   __shared__ int s_rem;
   __shared__ int wsum[16];
 
-  const int unit = blockIdx.x;
-  const int l = unit / (a.B * a.Hkv);
-  if (owner_layer(a.layer0 + l, a.period, a.start) != a.layer0 + l) return;
+  const int ou = blockIdx.x;  // (owner index * B + b) * Hkv + h
+  const int l = a.own.l[ou / (a.B * a.Hkv)];
+  const size_t unit = (size_t)l * a.B * a.Hkv + ou % (a.B * a.Hkv);
   const int tid = threadIdx.x, w = tid >> 6;
   const int loc = min(a.local_keep, a.keep);
   const int n_old = a.T - loc, n_sel = a.keep - loc;
@@ -422,10 +432,10 @@ template <class DT, int D>
 hipError_t launch_pass(const EvictArgs& a, bool rows, hipStream_t st) {
   if (rows) {
     const int n_rb = (a.W + kRowBlock - 1) / kRowBlock;
-    hipLaunchKernelGGL((k_rowstats<DT, D>), dim3(a.n_layers * a.B * a.Hq * n_rb), dim3(256), 0, st, a);
+    hipLaunchKernelGGL((k_rowstats<DT, D>), dim3(a.own.n * a.B * a.Hq * n_rb), dim3(256), 0, st, a);
   } else {
     const int n_kb = (a.T + kColBlockKeys - 1) / kColBlockKeys;
-    hipLaunchKernelGGL((k_colsum<DT, D>), dim3(a.n_layers * a.B * a.Hkv * n_kb), dim3(256), 0, st, a);
+    hipLaunchKernelGGL((k_colsum<DT, D>), dim3(a.own.n * a.B * a.Hkv * n_kb), dim3(256), 0, st, a);
   }
   return hipGetLastError();
 }
@@ -457,7 +467,7 @@ hipError_t launch_colsum(const EvictArgs& a, int dtype, int D, hipStream_t st) {
 }
 
 hipError_t launch_topk(const EvictArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL(k_topk, dim3(a.n_layers * a.B * a.Hkv), dim3(kTopkThreads), 0, st, a);
+  hipLaunchKernelGGL(k_topk, dim3(a.own.n * a.B * a.Hkv), dim3(kTopkThreads), 0, st, a);
   return hipGetLastError();
 }
 

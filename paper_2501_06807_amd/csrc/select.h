@@ -5,7 +5,7 @@
 namespace mpc {
 
 constexpr int kSelMaxSuper = 1024;  // S limit (LDS)
-constexpr int kSelMaxCand = 2048;   // k_super * fanout limit (LDS)
+constexpr int kSelMaxCand = 1024;   // k_super * fanout limit (LDS)
 
 struct SelectArgs {
   const void* q;        // [L][B][Hq][d]
@@ -16,6 +16,7 @@ struct SelectArgs {
   int B, layer0, n_layers, Hq, Hkv;
   int C, S, f, NC, k_super, k_clusters;  // NC = k_super * f
   int period, start;
+  OwnerTable own;  // owner layers of the block (one workgroup per owner head)
 };
 
 size_t select_smem_bytes(int D, int S, int NC);

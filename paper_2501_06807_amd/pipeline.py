@@ -1,4 +1,5 @@
 """Preallocated prefill + decode path over the four C-ABI entry points."""
+import ctypes
 import math
 
 import torch
@@ -44,6 +45,21 @@ class MPCachePath:
         self.ws_evict = L.workspace(L.workspace_bytes(L.MPC_OP_STATIC_EVICT, qd, T, ecfg), dev)
         self.ws_decode = L.workspace(L.workspace_bytes(L.MPC_OP_DECODE_ATTN, qd, keep), dev)
 
+        # argument tuples of the per-step calls, built once (only the query pointer and the stream
+        # change between decode steps)
+        self._qdims = qd
+        kvd = L.dims_of(self.out, self.k_s, layer0)
+        self._kvdims = kvd
+        P = lambda t: None if t is None else ctypes.c_void_p(t.data_ptr())
+        lib = L.lib()
+        self._select_fn = lib.mpc_select_clusters
+        self._select_args = (ctypes.byref(kvd), keep, ctypes.byref(self.cfg))
+        self._select_tail = (P(self.cent), P(self.scent), P(self.sel), P(self.sel_score), None, 0)
+        self._attend_fn = lib.mpc_sparse_decode_attn
+        self._attend_args = (ctypes.byref(kvd), keep, cluster)
+        self._attend_mid = (P(self.k_s), P(self.v_s), P(self.sel), k_clusters, self.sm_scale, P(self.out),
+                            P(self.lse), P(self.ws_decode), self.ws_decode.numel())
+
     def prefill(self, q_win, k, v, stream=None):
         L.mpc_static_evict(q_win, k, v, self.kept, self.k_s, self.v_s, keep=self.keep,
                            local_keep=self.local_keep, sm_scale=self.sm_scale, causal=self.causal,
@@ -53,13 +69,15 @@ class MPCachePath:
         L.mpc_build_clusters(self.k_s, self.cent, self.scent, self.cfg, layer0=self.layer0, stream=stream)
 
     def select(self, q, stream=None):
-        L.mpc_select_clusters(q, self.cent, self.scent, self.sel, self.cfg, Ts=self.keep,
-                              sel_score=self.sel_score, layer0=self.layer0, stream=stream)
+        """q: [L][B][Hq][d] contiguous CUDA tensor of the path's dtype."""
+        st = L._stream(stream)
+        L._check("mpc_select_clusters",
+                 self._select_fn(*self._select_args, ctypes.c_void_p(q.data_ptr()), *self._select_tail, st))
 
     def attend(self, q, stream=None):
-        L.mpc_sparse_decode_attn(q, self.k_s, self.v_s, self.sel, self.out, cluster_size=self.cluster,
-                                 sm_scale=self.sm_scale, lse=self.lse, ws=self.ws_decode,
-                                 layer0=self.layer0, stream=stream)
+        st = L._stream(stream)
+        L._check("mpc_sparse_decode_attn",
+                 self._attend_fn(*self._attend_args, ctypes.c_void_p(q.data_ptr()), *self._attend_mid, st))
 
     def decode(self, q, stream=None):
         self.select(q, stream)

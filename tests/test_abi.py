@@ -86,10 +86,11 @@ def test_decode_validation_and_workspace():
     s, _ = _status("mpc_sparse_decode_attn", ctypes.byref(d3), 256, 16, FAKE, FAKE, FAKE, FAKE, 4, 0.1,
                    FAKE, None, None, 0, None)
     assert s == L.MPC_EUNSUPPORTED  # group of 3
-    # few units -> split-K -> a workspace is required
+    # few units and enough tokens -> split-K -> a workspace is required (validation fails before
+    # any launch, so the fake pointers are never used)
     need = L.workspace_bytes(L.MPC_OP_DECODE_ATTN, d, 256)
     assert need > 0
-    s, msg = _status("mpc_sparse_decode_attn", ctypes.byref(d), 256, 16, FAKE, FAKE, FAKE, FAKE, 4, 0.1,
+    s, msg = _status("mpc_sparse_decode_attn", ctypes.byref(d), 256, 16, FAKE, FAKE, FAKE, FAKE, 16, 0.1,
                      FAKE, None, None, 0, None)
     assert s == L.MPC_EWORKSPACE and str(need) in msg
     # many units -> no split -> no workspace

@@ -132,6 +132,27 @@ def test_select_matches_oracle(name):
         say(f"  step {step}: tie swaps {swaps}")
 
 
+def test_select_many_heads_matches_oracle():
+    """At least 512 owner heads: the one-wave-per-head selection kernel; every head is checked."""
+    w = synth.get("C4").with_(n_layers=8, keep=2048, k_super=4, k_clusters=8)
+    say(f"[select many heads] C4 shape L=8 B=4 Hkv=32 Ts=2048 k_super=4 k_clusters=8")
+    k, _ = _cache(w, 0)
+    cent, scent = oracle.build_clusters(k, w.dtype, cluster=w.cluster, fanout=w.fanout, alpha=0.6,
+                                        share_period=w.share_period)
+    import paper_2501_06807_amd as M
+    cfg = M.select_cfg(w.cluster, w.fanout, w.k_super, w.k_clusters, 0.6, w.share_period)
+    q = _queries(w, 0, 7)
+    sel_ref, _ = oracle.select_clusters(q, cent, scent, w.dtype, Ts=w.keep, cluster=w.cluster, fanout=w.fanout,
+                                        k_super=w.k_super, k_clusters=w.k_clusters, share_period=w.share_period)
+    sel = torch.zeros(sel_ref.shape, dtype=torch.int32, device="cuda")
+    sc = torch.zeros(sel_ref.shape, dtype=torch.float32, device="cuda")
+    M.mpc_select_clusters(bits_to_torch(q, w.dtype), torch.from_numpy(cent).cuda(), torch.from_numpy(scent).cuda(),
+                          sel, cfg, Ts=w.keep, sel_score=sc)
+    torch.cuda.synchronize()
+    swaps = _check_selection(w, 0, q, cent, scent, sel.cpu().numpy(), sel_ref, sc.cpu().numpy())
+    say(f"  tie swaps {swaps}")
+
+
 @pytest.mark.parametrize("name", list(CASES))
 def test_sparse_attention_matches_oracle(name):
     w, layer0 = _workload(name)
