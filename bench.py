@@ -6,7 +6,8 @@ HBM: look-once static eviction of the prompt cache (window scoring, top-k, gathe
 representatives, then every decode step of the workload (two-level selection with layer sharing +
 sparse attention over all layers). The reported metric is the decode step's latency per layer
 (select + attention), measured with HIP events on the stream the kernels run on, with its
-effective HBM bandwidth against the 8 TB/s peak. Prefill figures are reported beside it.
+effective HBM bandwidth against the 8 TB/s peak. Prefill figures are reported beside it, and so is
+the decode step in the other mode (two kernels, or one launch of mpc_decode_step).
 
 Prints one JSON line. Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload C4]
 """
@@ -33,10 +34,17 @@ def parse():
     p.add_argument("--warmup", type=int, default=1)
     p.add_argument("--workload", default="C4")
     p.add_argument("--decode-steps", type=int, default=None, help="decode steps per pass (default: workload's)")
+    p.add_argument("--decode-mode", choices=("split", "fused"), default="split",
+                   help="timed decode step: selection and attention as two kernels (default) or one launch")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--copy-calibration", action="store_true",
                    help="run a 1 GiB device copy first (reference kernel for HBM counter scaling)")
     return p.parse_args()
+
+
+DECODE_STEP_SOURCES = ("fused.hip", "fused.h", "decode_dev.h", "select_dev.h", "decode_attn.h", "select.h",
+                       "common.h")
+SPARSE_DECODE_SOURCES = ("decode_attn.hip", "decode_attn.h", "decode_dev.h", "common.h")
 
 
 def source_digest(*names):
@@ -155,21 +163,29 @@ def main():
                          share_start=w.share_start)
     torch.cuda.synchronize()
 
+    fused = args.decode_mode == "fused"
+
+    def decode_steps(ev, split):
+        for e in range(E):
+            if ev:
+                ev["sel"][e].record()
+            if split:
+                path.select(qs[e])
+                if ev:
+                    ev["att"][e].record()
+                path.attend(qs[e])
+            else:
+                path.decode_fused(qs[e])
+            if ev:
+                ev["end"][e].record()
+
     def one_pass(ev=None):
         if ev:
             ev["start"].record()
         path.prefill(q_win, k, v)
         if ev:
             ev["prefill"].record()
-        for e in range(E):
-            if ev:
-                ev["sel"][e].record()
-            path.select(qs[e])
-            if ev:
-                ev["att"][e].record()
-            path.attend(qs[e])
-            if ev:
-                ev["end"][e].record()
+        decode_steps(ev, not fused)
 
     for _ in range(args.warmup):
         one_pass()
@@ -185,22 +201,49 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
 
-    pre_ms = [ev["start"].elapsed_time(ev["prefill"]) for ev in evs]
-    sel_ms = [ev["sel"][e].elapsed_time(ev["att"][e]) for ev in evs for e in range(E)]
-    att_ms = [ev["att"][e].elapsed_time(ev["end"][e]) for ev in evs for e in range(E)]
-    dec_ms = [ev["sel"][e].elapsed_time(ev["end"][e]) for ev in evs for e in range(E)]
     mean = lambda x: sum(x) / len(x)
+
+    def split_times(evs):
+        sel_ms = [ev["sel"][e].elapsed_time(ev["att"][e]) for ev in evs for e in range(E)]
+        att_ms = [ev["att"][e].elapsed_time(ev["end"][e]) for ev in evs for e in range(E)]
+        return mean(sel_ms) * 1e3, mean(att_ms) * 1e3
+
+    pre_ms = [ev["start"].elapsed_time(ev["prefill"]) for ev in evs]
+    dec_ms = [ev["sel"][e].elapsed_time(ev["end"][e]) for ev in evs for e in range(E)]
     dec_us = mean(dec_ms) * 1e3
-    att_us = mean(att_ms) * 1e3
-    sel_us = mean(sel_ms) * 1e3
+    # the decode step in the other mode, after the timed region (same prefilled state, same queries)
+    ev2 = [dict(sel=[mk() for _ in range(E)], att=[mk() for _ in range(E)], end=[mk() for _ in range(E)])
+           for _ in range(2)]
+    decode_steps(None, fused)
+    for ev in ev2:
+        decode_steps(ev, fused)
+    torch.cuda.synchronize()
+    if fused:
+        sel_us, att_us = split_times(ev2)
+        alt = {"mode": "split", "us": round(sel_us + att_us, 3)}
+    else:
+        sel_us, att_us = split_times(evs)
+        alt = {"mode": "fused", "us": round(mean([ev["sel"][e].elapsed_time(ev["end"][e]) for ev in ev2
+                                                  for e in range(E)]) * 1e3, 3)}
 
     owners = [l for l in range(w.n_layers) if M.owner_layer(l, w.share_period, w.share_start) == l]
     sel_b, att_b = decode_bytes(w, owners, path.sel.cpu().numpy(), path.C, path.S)
     step_b = sel_b + att_b
-    digest = source_digest("decode_attn.hip", "decode_attn.h", "common.h")
-    traffic = measured_traffic("sparse_decode", args.workload, digest)
     att_gbs = att_b / (att_us * 1e-6) / 1e9
     dec_gbs = step_b / (dec_us * 1e-6) / 1e9
+    if fused:
+        traffic = measured_traffic("decode_step", args.workload, source_digest(*DECODE_STEP_SOURCES))
+        roofline = {"kernel": "k_decode_step (two-level selection + gather + online-softmax attention, "
+                              "all layers, one launch)",
+                    "bound": "hbm", "achieved": round(dec_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": round(dec_gbs / HBM_PEAK_GBS, 4), "traffic": traffic,
+                    "algorithmic_bytes_per_launch": step_b, "avg_launch_us": round(dec_us, 3)}
+    else:
+        traffic = measured_traffic("sparse_decode", args.workload, source_digest(*SPARSE_DECODE_SOURCES))
+        roofline = {"kernel": "k_sparse_decode (gather + online-softmax attention, all layers per launch)",
+                    "bound": "hbm", "achieved": round(att_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": round(att_gbs / HBM_PEAK_GBS, 4), "traffic": traffic,
+                    "algorithmic_bytes_per_launch": att_b, "avg_launch_us": round(att_us, 3)}
     fl = prefill_flops(w, len(owners))
     pre_tflops = fl / (mean(pre_ms) * 1e-3) / 1e12
 
@@ -222,13 +265,14 @@ def main():
                    "window_rows": w.window, "kept_tokens": w.keep, "cluster": w.cluster, "fanout": w.fanout,
                    "k_super": w.k_super, "k_clusters": w.k_clusters, "share_period": w.share_period,
                    "decode_steps_per_pass": E},
-        "decode_step": {"us": round(dec_us, 3), "select_us": round(sel_us, 3), "attention_us": round(att_us, 3),
-                        "algorithmic_bytes": step_b, "achieved_GBps": round(dec_gbs, 1),
-                        "frac_of_hbm_peak": round(dec_gbs / HBM_PEAK_GBS, 4)},
-        "roofline": {"kernel": "k_sparse_decode (gather + online-softmax attention, all layers per launch)",
-                     "bound": "hbm", "achieved": round(att_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(att_gbs / HBM_PEAK_GBS, 4), "traffic": traffic,
-                     "algorithmic_bytes_per_launch": att_b, "avg_launch_us": round(att_us, 3)},
+        "decode_step": {"mode": args.decode_mode, "us": round(dec_us, 3), "algorithmic_bytes": step_b,
+                        "achieved_GBps": round(dec_gbs, 1), "frac_of_hbm_peak": round(dec_gbs / HBM_PEAK_GBS, 4)},
+        "decode_step_two_kernels": {"us": round(sel_us + att_us, 3), "select_us": round(sel_us, 3),
+                                    "attention_us": round(att_us, 3), "attention_algorithmic_bytes": att_b,
+                                    "attention_GBps": round(att_gbs, 1),
+                                    "attention_frac_of_hbm_peak": round(att_gbs / HBM_PEAK_GBS, 4)},
+        "decode_step_other_mode": alt,
+        "roofline": roofline,
         "prefill": {"ms_per_pass": round(mean(pre_ms), 3), "owner_layers": len(owners),
                     "ms_per_owner_layer": round(mean(pre_ms) / len(owners), 3),
                     "algorithmic_TFLOP_per_pass": round(fl / 1e12, 3),

@@ -78,12 +78,12 @@ typedef struct {
   int32_t share_start;
 } mpc_evict_cfg;
 
-enum { MPC_OP_STATIC_EVICT = 0, MPC_OP_SELECT = 1, MPC_OP_DECODE_ATTN = 2 };
+enum { MPC_OP_STATIC_EVICT = 0, MPC_OP_SELECT = 1, MPC_OP_DECODE_ATTN = 2, MPC_OP_DECODE_STEP = 3 };
 
 /* Workspace bytes needed by `op` (MPC_OP_*) for these dims. `T_or_Ts` is T for static eviction
- * and Ts otherwise; `cfg` points to the op's config struct (mpc_evict_cfg / mpc_select_cfg) or is
- * NULL for MPC_OP_DECODE_ATTN. Returns 0 when the op needs no workspace or the arguments are
- * invalid. */
+ * and Ts otherwise; `cfg` points to the op's config struct (mpc_evict_cfg for static eviction,
+ * mpc_select_cfg for selection and the decode step) or is NULL for MPC_OP_DECODE_ATTN. Returns 0
+ * when the op needs no workspace or the arguments are invalid. */
 size_t mpc_workspace_bytes(int32_t op, const mpc_dims* dims, int32_t T_or_Ts, const void* cfg);
 
 /* Look-once static eviction (Sec. 3.2; Alg. 3 step 1; window rule of App. F).
@@ -142,6 +142,22 @@ mpc_status mpc_sparse_decode_attn(const mpc_dims* dims, int32_t Ts, int32_t clus
                                   const void* q, const void* k_cache, const void* v_cache,
                                   const int32_t* sel, int32_t k_clusters, float sm_scale,
                                   void* out, float* lse, void* ws, size_t ws_bytes, void* stream);
+
+/* One decode step in one launch: mpc_select_clusters followed by mpc_sparse_decode_attn (same
+ * definitions, same results bit for bit), with the attention of a layer starting as soon as its
+ * owner's selection is published instead of after a kernel boundary.
+ *   q [L][B][Hq][d]; cent, scent from mpc_build_clusters; k_cache, v_cache [L][B][Hkv][Ts][d];
+ *   sel [L][B][Hkv][cfg->k_clusters] int32 out (in for layers owned before layer0);
+ *   sel_score optional; out [L][B][Hq][d]; lse optional.
+ *   ws: mpc_workspace_bytes(MPC_OP_DECODE_STEP, dims, Ts, cfg) bytes, zero-filled before its first
+ *   use; every completed call leaves it ready for the next (calls sharing it must not overlap).
+ * Blocks with fewer (layer, sequence, kv head) units than compute units run the two kernels one
+ * after the other instead (same results). */
+mpc_status mpc_decode_step(const mpc_dims* dims, int32_t Ts, const mpc_select_cfg* cfg,
+                           const void* q, const float* cent, const float* scent,
+                           const void* k_cache, const void* v_cache, float sm_scale, int32_t* sel,
+                           float* sel_score, void* out, float* lse, void* ws, size_t ws_bytes,
+                           void* stream);
 
 /* Owner layer of absolute layer `l` under the sharing rule above. */
 int32_t mpc_owner_layer(int32_t l, int32_t period, int32_t start);

@@ -1,4 +1,4 @@
-"""ctypes binding of libmpcache.so: the four entry points of the C ABI with the same names.
+"""ctypes binding of libmpcache.so: the entry points of the C ABI with the same names.
 
 Argument marshalling only: shapes are read off torch CUDA tensors, pointers and the current
 stream are handed to the library, and a non-zero status raises MpcError. Every step of the path
@@ -13,7 +13,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libmpcache.so")
 
 MPC_OK, MPC_EINVAL, MPC_ESHAPE, MPC_EUNSUPPORTED, MPC_EWORKSPACE, MPC_EHIP = range(6)
-MPC_OP_STATIC_EVICT, MPC_OP_SELECT, MPC_OP_DECODE_ATTN = range(3)
+MPC_OP_STATIC_EVICT, MPC_OP_SELECT, MPC_OP_DECODE_ATTN, MPC_OP_DECODE_STEP = range(4)
 DTYPE_CODE = {torch.float32: 0, torch.float16: 1, torch.bfloat16: 2}
 
 
@@ -44,7 +44,8 @@ class MpcError(RuntimeError):
 
 _LIB = None
 EXPORTS = ("mpc_workspace_bytes", "mpc_static_evict", "mpc_build_clusters", "mpc_select_clusters",
-           "mpc_sparse_decode_attn", "mpc_owner_layer", "mpc_status_string", "mpc_last_error")
+           "mpc_sparse_decode_attn", "mpc_decode_step", "mpc_owner_layer", "mpc_status_string",
+           "mpc_last_error")
 
 
 def lib():
@@ -61,7 +62,10 @@ def lib():
         L.mpc_build_clusters.argtypes = [P(MpcDims), I, P(MpcSelectCfg), V, V, V, V]
         L.mpc_select_clusters.argtypes = [P(MpcDims), I, P(MpcSelectCfg)] + [V] * 5 + [V, ctypes.c_size_t, V]
         L.mpc_sparse_decode_attn.argtypes = [P(MpcDims), I, I, V, V, V, V, I, F, V, V, V, ctypes.c_size_t, V]
-        for fn in ("mpc_static_evict", "mpc_build_clusters", "mpc_select_clusters", "mpc_sparse_decode_attn"):
+        L.mpc_decode_step.argtypes = [P(MpcDims), I, P(MpcSelectCfg)] + [V] * 5 + [F] + [V] * 4 + [
+            V, ctypes.c_size_t, V]
+        for fn in ("mpc_static_evict", "mpc_build_clusters", "mpc_select_clusters", "mpc_sparse_decode_attn",
+                   "mpc_decode_step"):
             getattr(L, fn).restype = ctypes.c_int
         L.mpc_owner_layer.argtypes = [I, I, I]
         L.mpc_owner_layer.restype = I
@@ -166,3 +170,21 @@ def mpc_sparse_decode_attn(q, k_cache, v_cache, sel, out, *, cluster_size, sm_sc
     _check("mpc_sparse_decode_attn", lib().mpc_sparse_decode_attn(
         ctypes.byref(dims), Ts, cluster_size, _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(sel), sel.shape[-1],
         sm_scale, _ptr(out), _ptr(lse), _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def mpc_decode_step(q, cent, scent, k_cache, v_cache, sel, out, cfg, *, sm_scale, sel_score=None, lse=None,
+                    ws=None, layer0=0, stream=None):
+    """Selection of every owner head then sparse attention of every head, in one call.
+
+    q [L][B][Hq][d], cent/scent as built, k/v [L][B][Hkv][Ts][d] -> sel [L][B][Hkv][k], out [L][B][Hq][d].
+    ws must come from workspace() (zero-filled) and be reused by later calls of the same shape.
+    """
+    _contig(q, cent, scent, k_cache, v_cache, sel, out, sel_score, lse, ws)
+    dims = dims_of(q, k_cache, layer0)
+    Ts = k_cache.shape[3]
+    if ws is None:
+        ws = workspace(workspace_bytes(MPC_OP_DECODE_STEP, dims, Ts, cfg), q.device)
+    _check("mpc_decode_step", lib().mpc_decode_step(
+        ctypes.byref(dims), Ts, ctypes.byref(cfg), _ptr(q), _ptr(cent), _ptr(scent), _ptr(k_cache), _ptr(v_cache),
+        sm_scale, _ptr(sel), _ptr(sel_score), _ptr(out), _ptr(lse), _ptr(ws), ws.numel(), _stream(stream)))
+    return ws

@@ -7,6 +7,7 @@
 #include "common.h"
 #include "decode_attn.h"
 #include "evict.h"
+#include "fused.h"
 #include "select.h"
 
 namespace {
@@ -79,6 +80,20 @@ size_t decode_ws_bytes(const mpc_dims* d) {
   return align256((size_t)units * p.splits * G * (d->head_dim + 2) * sizeof(float));
 }
 
+// Fused decode-step workspace: ticket counters, owner-head flags, then the split-K partials used
+// when the block is too small for the fused kernel.
+struct StepWs {
+  size_t flags, part, total;
+};
+StepWs step_ws(const mpc_dims* d, const mpc_select_cfg* cfg) {
+  StepWs w;
+  const mpc::OwnerTable own = mpc::owner_table(d->layer0, d->n_layers, cfg->share_period, cfg->share_start);
+  w.flags = align256(sizeof(mpc::FusedSync));
+  w.part = w.flags + align256((size_t)own.n * d->batch * d->n_kv_heads * sizeof(int));
+  w.total = w.part + decode_ws_bytes(d);
+  return w;
+}
+
 }  // namespace
 
 extern "C" {
@@ -109,6 +124,10 @@ size_t mpc_workspace_bytes(int32_t op, const mpc_dims* dims, int32_t T_or_Ts, co
     return evict_ws(dims, T_or_Ts, c->window).total;
   }
   if (op == MPC_OP_DECODE_ATTN) return decode_ws_bytes(dims);
+  if (op == MPC_OP_DECODE_STEP) {
+    if (!cfg) return 0;
+    return step_ws(dims, (const mpc_select_cfg*)cfg).total;
+  }
   return 0;
 }
 
@@ -219,12 +238,13 @@ mpc_status mpc_build_clusters(const mpc_dims* dims, int32_t Ts, const mpc_select
   return ok();
 }
 
-mpc_status mpc_select_clusters(const mpc_dims* dims, int32_t Ts, const mpc_select_cfg* cfg,
-                               const void* q, const float* cent, const float* scent,
-                               int32_t* sel, float* sel_score, void* ws, size_t ws_bytes,
-                               void* stream) {
-  (void)ws;
-  (void)ws_bytes;
+}  // extern "C"
+
+namespace {
+
+mpc_status prepare_select(const mpc_dims* dims, int32_t Ts, const mpc_select_cfg* cfg, const void* q,
+                          const float* cent, const float* scent, int32_t* sel, float* sel_score,
+                          mpc::SelectArgs* out) {
   mpc_status s = check_dims(dims);
   if (s != MPC_OK) return s;
   if (!cfg) return fail(MPC_EINVAL, "cfg is NULL");
@@ -239,6 +259,7 @@ mpc_status mpc_select_clusters(const mpc_dims* dims, int32_t Ts, const mpc_selec
     return fail(MPC_ESHAPE, "k_clusters %d exceeds the smallest candidate set %d", cfg->k_clusters, min_cand);
   if (S > mpc::kSelMaxSuper || (int64_t)cfg->k_super * cfg->fanout > mpc::kSelMaxCand)
     return fail(MPC_EUNSUPPORTED, "selection sizes beyond the kernel limits");
+  if (dims->n_layers > mpc::kMaxLayers) return fail(MPC_EUNSUPPORTED, "at most %d layers per call", mpc::kMaxLayers);
   mpc::SelectArgs a{};
   a.q = q;
   a.cent = cent;
@@ -258,19 +279,14 @@ mpc_status mpc_select_clusters(const mpc_dims* dims, int32_t Ts, const mpc_selec
   a.k_clusters = cfg->k_clusters;
   a.period = cfg->share_period;
   a.start = cfg->share_start;
-  if (a.n_layers > mpc::kMaxLayers) return fail(MPC_EUNSUPPORTED, "at most %d layers per call", mpc::kMaxLayers);
   a.own = mpc::owner_table(a.layer0, a.n_layers, a.period, a.start);
-  if (a.own.n == 0) return ok();
-  clear_stale_error();
-  if ((s = launched(mpc::launch_select(a, dims->dtype, dims->head_dim, (hipStream_t)stream), "select")) != MPC_OK)
-    return s;
-  return ok();
+  *out = a;
+  return MPC_OK;
 }
 
-mpc_status mpc_sparse_decode_attn(const mpc_dims* dims, int32_t Ts, int32_t cluster_size,
-                                  const void* q, const void* k_cache, const void* v_cache,
-                                  const int32_t* sel, int32_t k_clusters, float sm_scale,
-                                  void* out, float* lse, void* ws, size_t ws_bytes, void* stream) {
+mpc_status prepare_decode(const mpc_dims* dims, int32_t Ts, int32_t cluster_size, const void* q,
+                          const void* k_cache, const void* v_cache, const int32_t* sel, int32_t k_clusters,
+                          float sm_scale, void* out, float* lse, mpc::DecodeArgs* da, mpc::DecodePlan* plan) {
   mpc_status s = check_dims(dims);
   if (s != MPC_OK) return s;
   if (Ts <= 0 || cluster_size <= 0 || k_clusters <= 0)
@@ -286,11 +302,7 @@ mpc_status mpc_sparse_decode_attn(const mpc_dims* dims, int32_t Ts, int32_t clus
   if (k_clusters > 1024) return fail(MPC_EUNSUPPORTED, "k_clusters above 1024");
   if ((int64_t)k_clusters * cluster_size >= ((int64_t)1 << 30)) return fail(MPC_EUNSUPPORTED, "too many tokens");
   const int units = dims->n_layers * dims->batch * dims->n_kv_heads;
-  const mpc::DecodePlan plan =
-      mpc::decode_plan(units, k_clusters * cluster_size, dims->head_dim, elt_size(dims->dtype));
-  const size_t need = decode_ws_bytes(dims);
-  if (plan.splits > 1 && (!ws || ws_bytes < need))
-    return fail(MPC_EWORKSPACE, "sparse decode attention needs %zu workspace bytes", need);
+  *plan = mpc::decode_plan(units, k_clusters * cluster_size, dims->head_dim, elt_size(dims->dtype));
   mpc::DecodeArgs a{};
   a.q = q;
   a.k = k_cache;
@@ -298,18 +310,99 @@ mpc_status mpc_sparse_decode_attn(const mpc_dims* dims, int32_t Ts, int32_t clus
   a.sel = sel;
   a.out = out;
   a.lse = lse;
-  a.part = plan.splits > 1 ? (float*)ws : nullptr;
+  a.part = nullptr;
   a.Ts = Ts;
   a.s = cluster_size;
   a.C = C;
   a.k_sel = k_clusters;
   a.Hq = dims->n_q_heads;
   a.Hkv = dims->n_kv_heads;
-  a.splits = plan.splits;
+  a.splits = plan->splits;
   a.qscale = (float)((double)sm_scale * 1.4426950408889634);
+  *da = a;
+  return MPC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+mpc_status mpc_select_clusters(const mpc_dims* dims, int32_t Ts, const mpc_select_cfg* cfg,
+                               const void* q, const float* cent, const float* scent,
+                               int32_t* sel, float* sel_score, void* ws, size_t ws_bytes,
+                               void* stream) {
+  (void)ws;
+  (void)ws_bytes;
+  mpc::SelectArgs a{};
+  mpc_status s = prepare_select(dims, Ts, cfg, q, cent, scent, sel, sel_score, &a);
+  if (s != MPC_OK) return s;
+  if (a.own.n == 0) return ok();
+  clear_stale_error();
+  if ((s = launched(mpc::launch_select(a, dims->dtype, dims->head_dim, (hipStream_t)stream), "select")) != MPC_OK)
+    return s;
+  return ok();
+}
+
+mpc_status mpc_sparse_decode_attn(const mpc_dims* dims, int32_t Ts, int32_t cluster_size,
+                                  const void* q, const void* k_cache, const void* v_cache,
+                                  const int32_t* sel, int32_t k_clusters, float sm_scale,
+                                  void* out, float* lse, void* ws, size_t ws_bytes, void* stream) {
+  mpc::DecodeArgs a{};
+  mpc::DecodePlan plan{};
+  mpc_status s = prepare_decode(dims, Ts, cluster_size, q, k_cache, v_cache, sel, k_clusters, sm_scale, out,
+                                lse, &a, &plan);
+  if (s != MPC_OK) return s;
+  const size_t need = decode_ws_bytes(dims);
+  if (plan.splits > 1 && (!ws || ws_bytes < need))
+    return fail(MPC_EWORKSPACE, "sparse decode attention needs %zu workspace bytes", need);
+  if (plan.splits > 1) a.part = (float*)ws;
+  const int units = dims->n_layers * dims->batch * dims->n_kv_heads;
+  const int G = dims->n_q_heads / dims->n_kv_heads;
   clear_stale_error();
   if ((s = launched(mpc::launch_sparse_decode(a, dims->dtype, dims->head_dim, G, units, plan.waves, (hipStream_t)stream),
                     "sparse decode attention")) != MPC_OK)
+    return s;
+  return ok();
+}
+
+mpc_status mpc_decode_step(const mpc_dims* dims, int32_t Ts, const mpc_select_cfg* cfg,
+                           const void* q, const float* cent, const float* scent,
+                           const void* k_cache, const void* v_cache, float sm_scale, int32_t* sel,
+                           float* sel_score, void* out, float* lse, void* ws, size_t ws_bytes,
+                           void* stream) {
+  mpc::SelectArgs sa{};
+  mpc_status s = prepare_select(dims, Ts, cfg, q, cent, scent, sel, sel_score, &sa);
+  if (s != MPC_OK) return s;
+  mpc::DecodeArgs da{};
+  mpc::DecodePlan plan{};
+  s = prepare_decode(dims, Ts, cfg->cluster_size, q, k_cache, v_cache, sel, cfg->k_clusters, sm_scale, out, lse,
+                     &da, &plan);
+  if (s != MPC_OK) return s;
+  const StepWs lay = step_ws(dims, cfg);
+  if (!ws || ws_bytes < lay.total)
+    return fail(MPC_EWORKSPACE, "decode step needs %zu workspace bytes", lay.total);
+  const int units = dims->n_layers * dims->batch * dims->n_kv_heads;
+  const int G = dims->n_q_heads / dims->n_kv_heads;
+  hipStream_t st = (hipStream_t)stream;
+  clear_stale_error();
+  if (plan.splits > 1) {  // small block: the two kernels in sequence
+    da.part = (float*)((char*)ws + lay.part);
+    if (sa.own.n > 0 &&
+        (s = launched(mpc::launch_select(sa, dims->dtype, dims->head_dim, st), "select")) != MPC_OK)
+      return s;
+    if ((s = launched(mpc::launch_sparse_decode(da, dims->dtype, dims->head_dim, G, units, plan.waves, st),
+                      "sparse decode attention")) != MPC_OK)
+      return s;
+    return ok();
+  }
+  mpc::FusedArgs f{};
+  f.s = sa;
+  f.d = da;
+  f.sync = (mpc::FusedSync*)ws;
+  f.flags = (int*)((char*)ws + lay.flags);
+  const mpc::FusedPlan fp = mpc::fused_plan(sa, dims->head_dim);
+  f.total = fp.total;
+  if ((s = launched(mpc::launch_decode_step(f, fp, dims->dtype, dims->head_dim, G, st), "decode step")) != MPC_OK)
     return s;
   return ok();
 }

@@ -1,4 +1,4 @@
-"""Preallocated prefill + decode path over the four C-ABI entry points."""
+"""Preallocated prefill + decode path over the C-ABI entry points."""
 import ctypes
 import math
 
@@ -9,7 +9,10 @@ from . import _lib as L
 
 class MPCachePath:
     """Buffers and calls for one workload: static eviction and cluster build at prefill, then
-    selection + sparse attention for every decode step, all layers of the block per call."""
+    selection + sparse attention for every decode step, all layers of the block per call.
+
+    decode() runs them as two calls (mpc_select_clusters, mpc_sparse_decode_attn); decode_fused()
+    runs both in one launch (mpc_decode_step) with the same results."""
 
     def __init__(self, *, n_layers, batch, n_q_heads, n_kv_heads, head_dim, dtype, T, window, keep,
                  local_keep, cluster, fanout, k_super, k_clusters, share_period, share_start=2,
@@ -44,6 +47,7 @@ class MPCachePath:
                              causal=int(causal), share_period=share_period, share_start=share_start)
         self.ws_evict = L.workspace(L.workspace_bytes(L.MPC_OP_STATIC_EVICT, qd, T, ecfg), dev)
         self.ws_decode = L.workspace(L.workspace_bytes(L.MPC_OP_DECODE_ATTN, qd, keep), dev)
+        self.ws_step = L.workspace(L.workspace_bytes(L.MPC_OP_DECODE_STEP, qd, keep, self.cfg), dev)
 
         # argument tuples of the per-step calls, built once (only the query pointer and the stream
         # change between decode steps)
@@ -59,6 +63,10 @@ class MPCachePath:
         self._attend_args = (ctypes.byref(kvd), keep, cluster)
         self._attend_mid = (P(self.k_s), P(self.v_s), P(self.sel), k_clusters, self.sm_scale, P(self.out),
                             P(self.lse), P(self.ws_decode), self.ws_decode.numel())
+        self._step_fn = lib.mpc_decode_step
+        self._step_args = (ctypes.byref(kvd), keep, ctypes.byref(self.cfg))
+        self._step_tail = (P(self.cent), P(self.scent), P(self.k_s), P(self.v_s), self.sm_scale, P(self.sel),
+                           P(self.sel_score), P(self.out), P(self.lse), P(self.ws_step), self.ws_step.numel())
 
     def prefill(self, q_win, k, v, stream=None):
         L.mpc_static_evict(q_win, k, v, self.kept, self.k_s, self.v_s, keep=self.keep,
@@ -82,4 +90,10 @@ class MPCachePath:
     def decode(self, q, stream=None):
         self.select(q, stream)
         self.attend(q, stream)
+        return self.out
+
+    def decode_fused(self, q, stream=None):
+        st = L._stream(stream)
+        L._check("mpc_decode_step",
+                 self._step_fn(*self._step_args, ctypes.c_void_p(q.data_ptr()), *self._step_tail, st))
         return self.out

@@ -20,7 +20,7 @@ def test_library_exports_every_declared_function():
     lib = L.lib()
     names = declared_functions()
     assert {"mpc_static_evict", "mpc_build_clusters", "mpc_select_clusters",
-            "mpc_sparse_decode_attn"} <= set(names)
+            "mpc_sparse_decode_attn", "mpc_decode_step"} <= set(names)
     for n in names:
         assert hasattr(lib, n), n
 
@@ -96,6 +96,30 @@ def test_decode_validation_and_workspace():
     # many units -> no split -> no workspace
     big = _dims(n_layers=32, batch=4, n_q_heads=32, n_kv_heads=32)
     assert L.workspace_bytes(L.MPC_OP_DECODE_ATTN, big, 9824) == 0
+
+
+def test_decode_step_validation_and_workspace():
+    big = _dims(n_layers=32, batch=4, n_q_heads=32, n_kv_heads=32)
+    cfg = L.select_cfg(32, 8, 20, 15, share_period=4, share_start=2)
+    need = L.workspace_bytes(L.MPC_OP_DECODE_STEP, big, 9824, cfg)
+    owners = sum(1 for l in range(32) if oracle.owner_layer(l, 4, 2) == l)
+    assert owners == 10
+    assert need >= 16 + owners * 4 * 32 * 4  # counters + one flag per owner head
+    call = lambda d, c, ws, nb: _status(
+        "mpc_decode_step", ctypes.byref(d), 9824, ctypes.byref(c), FAKE, FAKE, FAKE, FAKE, FAKE, 0.088, FAKE,
+        None, FAKE, None, ws, nb, None)
+    s, msg = call(big, cfg, None, 0)
+    assert s == L.MPC_EWORKSPACE and str(need) in msg
+    assert call(big, cfg, FAKE, need - 1)[0] == L.MPC_EWORKSPACE
+    assert call(big, L.select_cfg(32, 8, 20, 161, share_period=4), FAKE, need)[0] == L.MPC_ESHAPE
+    assert call(big, L.select_cfg(32, 8, 40, 15, share_period=4), FAKE, need)[0] == L.MPC_ESHAPE
+    d3 = _dims(n_layers=32, batch=4, n_q_heads=96, n_kv_heads=32)
+    assert call(d3, cfg, FAKE, need)[0] == L.MPC_EUNSUPPORTED  # group of 3
+    # a small block also needs the split-K partials of the sequential fallback
+    small = _dims(n_layers=1, n_q_heads=8, n_kv_heads=8)
+    scfg = L.select_cfg(16, 4, 2, 4)
+    assert L.workspace_bytes(L.MPC_OP_DECODE_STEP, small, 256, scfg) >= \
+        L.workspace_bytes(L.MPC_OP_DECODE_ATTN, small, 256) > 0
 
 
 def test_static_evict_validation_and_workspace():

@@ -1,0 +1,127 @@
+"""GPU parity of the one-launch decode step (mpc_decode_step).
+
+The step must give bit for bit what mpc_select_clusters followed by mpc_sparse_decode_attn give,
+and both are checked against the oracle: the selection with the tie rule, the attention output
+recomputed by the oracle from the selection the GPU made. Cases are chosen so that the one-launch
+kernel runs (at least as many (layer, sequence, kv head) units as compute units) with per-head and
+per-wave selection, owners inside and before the block, and the sequential fallback of small blocks.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from gpu_util import assert_out_close, bits_to_torch, random_sel, say, to_f64
+from test_gpu_decode import _check_selection
+
+pytestmark = pytest.mark.gpu
+
+# name -> (workload, overrides, layer0)
+CASES = {
+    # 8 layers x 32 kv heads = 256 units; owners 0, 1, 2, 6 -> per-head selection items
+    "C3-L8": ("C3", dict(n_layers=8), 0),
+    # layers 3..10: layers 3-5 are owned by layer 2 (before the block) -> their selection is an input
+    "C3-L8@3": ("C3", dict(n_layers=8), 3),
+    # 512 owner heads -> one wave per head
+    "C4-L8": ("C4", dict(n_layers=8, keep=2048, k_super=4, k_clusters=8), 0),
+    # GQA group 4, 32 layers x 8 kv heads = 256 units
+    "C5-L32": ("C5", dict(keep=8192, k_super=8), 0),
+    # small blocks: the two kernels in sequence
+    "C1": ("C1", dict(), 0),
+    "C2": ("C2", dict(), 0),
+}
+
+
+def _setup(case):
+    name, kw, layer0 = CASES[case]
+    w = synth.get(name).with_(**kw)
+    ks, vs = [], []
+    for l in range(w.n_layers):
+        k, v = synth.cache_host(w, layer0 + l, T=w.keep)
+        ks.append(k)
+        vs.append(v)
+    k, v = np.stack(ks), np.stack(vs)
+    cent, scent = oracle.build_clusters(k, w.dtype, cluster=w.cluster, fanout=w.fanout, alpha=0.6, layer0=layer0,
+                                        share_period=w.share_period)
+    return w, layer0, k, v, cent, scent
+
+
+def _queries(w, layer0, step):
+    sp = synth.spec(w, n_layers=layer0 + w.n_layers)
+    return synth.dq_host(sp, step, w.dtype)[layer0:]
+
+
+def _sync_words(ws):
+    return ws[:16].view(torch.int32).cpu().tolist()  # ticket, done, epoch, error
+
+
+@pytest.mark.parametrize("case", list(CASES))
+def test_decode_step_equals_two_calls_and_oracle(case):
+    w, layer0, k, v, cent, scent = _setup(case)
+    import paper_2501_06807_amd as M
+    units = w.n_layers * w.batch * w.n_kv_heads
+    say(f"[step] {case}: L={w.n_layers}@{layer0} B={w.batch} Hq={w.n_q_heads} Hkv={w.n_kv_heads} Ts={w.keep} "
+        f"s={w.cluster} f={w.fanout} k_super={w.k_super} k_clusters={w.k_clusters} units={units}")
+    dt = synth.torch_dtype(w.dtype)
+    cfg = M.select_cfg(w.cluster, w.fanout, w.k_super, w.k_clusters, 0.6, w.share_period)
+    kd, vd = bits_to_torch(k, w.dtype), bits_to_torch(v, w.dtype)
+    cent_d, scent_d = torch.from_numpy(cent).cuda(), torch.from_numpy(scent).cuda()
+    shape_sel = (w.n_layers, w.batch, w.n_kv_heads, w.k_clusters)
+    shape_out = (w.n_layers, w.batch, w.n_q_heads, w.head_dim)
+    sm = 1.0 / math.sqrt(w.head_dim)
+    dims = M.dims_of(torch.empty(shape_out, dtype=dt), kd, layer0)
+    ws = M.workspace(M.workspace_bytes(M.MPC_OP_DECODE_STEP, dims, w.keep, cfg), "cuda")
+    ws_attn = M.workspace(M.workspace_bytes(M.MPC_OP_DECODE_ATTN, dims, w.keep), "cuda")
+    # layers owned before the block arrive with a selection made upstream (here: random, ascending)
+    C = -(-w.keep // w.cluster)
+    sel_in = random_sel(np.random.default_rng(11), w.n_layers * w.batch * w.n_kv_heads, C,
+                        w.k_clusters).reshape(shape_sel)
+    epoch = 0
+    for step in range(3):
+        q = _queries(w, layer0, step)
+        qd = bits_to_torch(q, w.dtype)
+        sel_ref, _ = oracle.select_clusters(q, cent, scent, w.dtype, Ts=w.keep, cluster=w.cluster, fanout=w.fanout,
+                                            k_super=w.k_super, k_clusters=w.k_clusters, layer0=layer0,
+                                            share_period=w.share_period, sel_in=sel_in)
+        outs = []
+        for fused in (False, True):
+            sel = torch.from_numpy(np.ascontiguousarray(sel_ref)).cuda()
+            for l in range(w.n_layers):
+                if oracle.owner_layer(layer0 + l, w.share_period, w.share_start) >= layer0:
+                    sel[l] = -7
+            sc = torch.zeros(shape_sel, dtype=torch.float32, device="cuda")
+            out = torch.full(shape_out, 3.0, dtype=dt, device="cuda")
+            lse = torch.zeros(shape_out[:-1], dtype=torch.float32, device="cuda")
+            if fused:
+                M.mpc_decode_step(qd, cent_d, scent_d, kd, vd, sel, out, cfg, sm_scale=sm, sel_score=sc, lse=lse,
+                                  ws=ws, layer0=layer0)
+            else:
+                M.mpc_select_clusters(qd, cent_d, scent_d, sel, cfg, Ts=w.keep, sel_score=sc, layer0=layer0)
+                M.mpc_sparse_decode_attn(qd, kd, vd, sel, out, cluster_size=w.cluster, sm_scale=sm, lse=lse,
+                                         ws=ws_attn, layer0=layer0)
+            torch.cuda.synchronize()
+            outs.append((sel.cpu(), sc.cpu(), out.cpu(), lse.cpu()))
+        (s0, c0, o0, l0), (s1, c1, o1, l1) = outs
+        assert torch.equal(s0, s1), "selection differs from the two-call path"
+        assert torch.equal(c0, c1), "selection scores differ from the two-call path"
+        assert torch.equal(o0.view(torch.int16 if dt != torch.float32 else torch.int32),
+                           o1.view(torch.int16 if dt != torch.float32 else torch.int32)), "output differs"
+        assert torch.equal(l0, l1), "lse differs"
+        # counters back at zero, no item gave up waiting; the epoch counts one-launch calls
+        sync = _sync_words(ws)
+        ran_fused = sync[2] == epoch + 1
+        assert sync[:2] == [0, 0] and sync[3] == 0 and (ran_fused or sync[2] == epoch), f"sync words {sync}"
+        assert ran_fused or units < 256, "a block with as many units as compute units must run in one launch"
+        epoch = sync[2]
+        # oracle: selection (tie rule) and attention over the selection the GPU made
+        sel_g = s1.numpy()
+        swaps = _check_selection(w, layer0, q, cent, scent, sel_g, sel_ref.copy(), c1.numpy())
+        ref, lse_ref = oracle.sparse_decode_attn(q, k, v, np.ascontiguousarray(sel_g), w.dtype, cluster=w.cluster,
+                                                 sm_scale=sm)
+        worst = assert_out_close(to_f64(o1), ref, w.dtype, case)
+        np.testing.assert_allclose(l1.numpy(), lse_ref, rtol=1e-5, atol=1e-5)
+        say(f"  step {step}: {'one launch' if ran_fused else 'two kernels'}, identical to two calls; "
+            f"tie swaps {swaps}; worst relative error {worst:.2e}")
