@@ -80,16 +80,18 @@ size_t decode_ws_bytes(const mpc_dims* d) {
   return align256((size_t)units * p.splits * G * (d->head_dim + 2) * sizeof(float));
 }
 
-// Fused decode-step workspace: ticket counters, owner-head flags, then the split-K partials used
-// when the block is too small for the fused kernel.
+// Fused decode-step workspace: the error word, per-owner-head state and consumer counts, then the
+// split-K partials used when the block is too small for the fused kernel.
 struct StepWs {
-  size_t flags, part, total;
+  size_t state, cons, part, total;
 };
 StepWs step_ws(const mpc_dims* d, const mpc_select_cfg* cfg) {
   StepWs w;
   const mpc::OwnerTable own = mpc::owner_table(d->layer0, d->n_layers, cfg->share_period, cfg->share_start);
-  w.flags = align256(sizeof(mpc::FusedSync));
-  w.part = w.flags + align256((size_t)own.n * d->batch * d->n_kv_heads * sizeof(int));
+  const size_t heads = align256((size_t)own.n * d->batch * d->n_kv_heads * sizeof(int));
+  w.state = align256(sizeof(mpc::FusedSync));
+  w.cons = w.state + heads;
+  w.part = w.cons + heads;
   w.total = w.part + decode_ws_bytes(d);
   return w;
 }
@@ -399,9 +401,9 @@ mpc_status mpc_decode_step(const mpc_dims* dims, int32_t Ts, const mpc_select_cf
   f.s = sa;
   f.d = da;
   f.sync = (mpc::FusedSync*)ws;
-  f.flags = (int*)((char*)ws + lay.flags);
+  f.state = (int*)((char*)ws + lay.state);
+  f.cons = (int*)((char*)ws + lay.cons);
   const mpc::FusedPlan fp = mpc::fused_plan(sa, dims->head_dim);
-  f.total = fp.total;
   if ((s = launched(mpc::launch_decode_step(f, fp, dims->dtype, dims->head_dim, G, st), "decode step")) != MPC_OK)
     return s;
   return ok();

@@ -5,26 +5,23 @@
 
 namespace mpc {
 
-// Ticket counters at the start of the fused workspace; zero before first use, left zero (with the
-// epoch advanced) by every completed launch. Owner-head flags follow.
+// Workspace of the fused kernel: a sticky error word, then per owner head a state word
+// (0 free, 1 being selected, 2 published) and a consumer count. Zero before first use; every
+// completed launch leaves the per-head words at zero again.
 struct FusedSync {
-  int ticket;
-  int done;
-  int epoch;
-  int error;  // bit 0: an attention item gave up waiting (never expected)
+  int error;  // bit 0: an attention unit gave up waiting for its selection (never expected)
 };
 
 struct FusedArgs {
   SelectArgs s;
   DecodeArgs d;
   FusedSync* sync;
-  int* flags;  // [owner heads]
-  int total;   // workgroups = tickets
+  int* state;  // [owner heads]
+  int* cons;   // [owner heads]
 };
 
 struct FusedPlan {
-  bool wave_select;
-  int total;
+  int units;
   size_t smem;
 };
 

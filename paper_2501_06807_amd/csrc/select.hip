@@ -29,7 +29,7 @@ template <class DT>
 hipError_t launch_wave(const SelectArgs& a, int D, hipStream_t st) {
   const int units = a.own.n * a.B * a.Hkv;
   const dim3 grid((units + kWaveHeads - 1) / kWaveHeads);
-  const size_t smem = kWaveHeads * dev::wave_region_bytes(a.S, a.NC);
+  const size_t smem = kWaveHeads * dev::wave_region_bytes(D, a.S, a.NC);
   if (D == 64)
     hipLaunchKernelGGL((k_select_wave<DT, 64>), grid, dim3(kWaveHeads * kWave), smem, st, a);
   else
