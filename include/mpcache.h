@@ -134,10 +134,12 @@ mpc_status mpc_select_clusters(const mpc_dims* dims, int32_t Ts, const mpc_selec
  * sel[l][b][h / G] (tokens past Ts in a partial last cluster are skipped).
  *   q [L][B][Hq][d];  k_cache, v_cache [L][B][Hkv][Ts][d];  sel [L][B][Hkv][k_clusters] int32
  *   (every entry in [0, C));  out [L][B][Hq][d] (dtype);  lse [L][B][Hq] float, optional
- *   (natural-log log-sum-exp of the scaled scores). fp32 accumulation.
- *   ws: mpc_workspace_bytes(MPC_OP_DECODE_ATTN, dims, Ts, NULL) bytes (split-K partials, used
- *   when there are fewer (layer, sequence, kv head) units than compute units); may be NULL when
- *   that is 0. */
+ *   (natural-log log-sum-exp of the scaled scores). fp32 accumulation; 16-bit types take exact
+ *   pairwise products summed in fp32. Limits: k_clusters <= 1024, Ts * d * element size <= 2 GiB.
+ *   ws: mpc_workspace_bytes(MPC_OP_DECODE_ATTN, dims, Ts, NULL) bytes (split-K partials and
+ *   per-unit arrival counters, used when there are fewer (layer, sequence, kv head) units than
+ *   twice the compute units), zero-filled before its first use; every completed call leaves the
+ *   counters at zero (calls sharing it must not overlap). May be NULL when that size is 0. */
 mpc_status mpc_sparse_decode_attn(const mpc_dims* dims, int32_t Ts, int32_t cluster_size,
                                   const void* q, const void* k_cache, const void* v_cache,
                                   const int32_t* sel, int32_t k_clusters, float sm_scale,
@@ -151,8 +153,8 @@ mpc_status mpc_sparse_decode_attn(const mpc_dims* dims, int32_t Ts, int32_t clus
  *   sel_score optional; out [L][B][Hq][d]; lse optional.
  *   ws: mpc_workspace_bytes(MPC_OP_DECODE_STEP, dims, Ts, cfg) bytes, zero-filled before its first
  *   use; every completed call leaves it ready for the next (calls sharing it must not overlap).
- * Blocks with fewer (layer, sequence, kv head) units than compute units run the two kernels one
- * after the other instead (same results). */
+ * Blocks whose attention is split over several workgroups per unit run the two kernels one after
+ * the other instead (same results). */
 mpc_status mpc_decode_step(const mpc_dims* dims, int32_t Ts, const mpc_select_cfg* cfg,
                            const void* q, const float* cent, const float* scent,
                            const void* k_cache, const void* v_cache, float sm_scale, int32_t* sel,

@@ -71,14 +71,22 @@ EvictWs evict_ws(const mpc_dims* d, int T, int W) {
   return w;
 }
 
-// Decode workspace: split-K partials, sized for the largest split count any token budget gives.
-size_t decode_ws_bytes(const mpc_dims* d) {
+// Decode workspace: split-K partials, sized for the largest split count any token budget gives,
+// then one arrival counter per unit (zero between launches).
+struct DecodeWs {
+  size_t cnt, total;
+};
+DecodeWs decode_ws(const mpc_dims* d) {
   const int units = d->n_layers * d->batch * d->n_kv_heads;
   const int G = d->n_q_heads / d->n_kv_heads;
   const mpc::DecodePlan p = mpc::decode_plan(units, 1 << 30, d->head_dim, elt_size(d->dtype));
-  if (p.splits <= 1) return 0;
-  return align256((size_t)units * p.splits * G * (d->head_dim + 2) * sizeof(float));
+  DecodeWs w{0, 0};
+  if (p.splits <= 1) return w;
+  w.cnt = align256((size_t)units * p.splits * G * (d->head_dim + 2) * sizeof(float));
+  w.total = w.cnt + align256((size_t)units * sizeof(int));
+  return w;
 }
+size_t decode_ws_bytes(const mpc_dims* d) { return decode_ws(d).total; }
 
 // Fused decode-step workspace: the error word, per-owner-head state and consumer counts, then the
 // split-K partials used when the block is too small for the fused kernel.
@@ -303,6 +311,8 @@ mpc_status prepare_decode(const mpc_dims* dims, int32_t Ts, int32_t cluster_size
   if (k_clusters > C) return fail(MPC_ESHAPE, "k_clusters %d > clusters %d", k_clusters, C);
   if (k_clusters > 1024) return fail(MPC_EUNSUPPORTED, "k_clusters above 1024");
   if ((int64_t)k_clusters * cluster_size >= ((int64_t)1 << 30)) return fail(MPC_EUNSUPPORTED, "too many tokens");
+  if ((int64_t)Ts * dims->head_dim * elt_size(dims->dtype) > ((int64_t)1 << 31))
+    return fail(MPC_EUNSUPPORTED, "a (layer, sequence, kv head) K/V block above 2 GiB");
   const int units = dims->n_layers * dims->batch * dims->n_kv_heads;
   *plan = mpc::decode_plan(units, k_clusters * cluster_size, dims->head_dim, elt_size(dims->dtype));
   mpc::DecodeArgs a{};
@@ -313,6 +323,7 @@ mpc_status prepare_decode(const mpc_dims* dims, int32_t Ts, int32_t cluster_size
   a.out = out;
   a.lse = lse;
   a.part = nullptr;
+  a.cnt = nullptr;
   a.Ts = Ts;
   a.s = cluster_size;
   a.C = C;
@@ -357,11 +368,14 @@ mpc_status mpc_sparse_decode_attn(const mpc_dims* dims, int32_t Ts, int32_t clus
   const size_t need = decode_ws_bytes(dims);
   if (plan.splits > 1 && (!ws || ws_bytes < need))
     return fail(MPC_EWORKSPACE, "sparse decode attention needs %zu workspace bytes", need);
-  if (plan.splits > 1) a.part = (float*)ws;
+  if (plan.splits > 1) {
+    a.part = (float*)ws;
+    a.cnt = (int*)((char*)ws + decode_ws(dims).cnt);
+  }
   const int units = dims->n_layers * dims->batch * dims->n_kv_heads;
   const int G = dims->n_q_heads / dims->n_kv_heads;
   clear_stale_error();
-  if ((s = launched(mpc::launch_sparse_decode(a, dims->dtype, dims->head_dim, G, units, plan.waves, (hipStream_t)stream),
+  if ((s = launched(mpc::launch_sparse_decode(a, dims->dtype, dims->head_dim, G, units, plan, (hipStream_t)stream),
                     "sparse decode attention")) != MPC_OK)
     return s;
   return ok();
@@ -389,10 +403,11 @@ mpc_status mpc_decode_step(const mpc_dims* dims, int32_t Ts, const mpc_select_cf
   clear_stale_error();
   if (plan.splits > 1) {  // small block: the two kernels in sequence
     da.part = (float*)((char*)ws + lay.part);
+    da.cnt = (int*)((char*)ws + lay.part + decode_ws(dims).cnt);
     if (sa.own.n > 0 &&
         (s = launched(mpc::launch_select(sa, dims->dtype, dims->head_dim, st), "select")) != MPC_OK)
       return s;
-    if ((s = launched(mpc::launch_sparse_decode(da, dims->dtype, dims->head_dim, G, units, plan.waves, st),
+    if ((s = launched(mpc::launch_sparse_decode(da, dims->dtype, dims->head_dim, G, units, plan, st),
                       "sparse decode attention")) != MPC_OK)
       return s;
     return ok();

@@ -128,6 +128,34 @@ __device__ __forceinline__ void store_elt<F16>(void* base, size_t i, float x) {
 
 __device__ __forceinline__ uint4 ldg16(const void* p) { return *(const uint4*)p; }
 
+// Device-coherent (agent-scope) accesses for data exchanged between workgroups of one launch:
+// they go through the coherent path of the per-die L2s without a cache write-back fence.
+__device__ __forceinline__ void st_coherent(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_coherent(const float* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Two-wide dot product of packed 16-bit pairs accumulated into fp32: c + a.lo * b.lo + a.hi * b.hi
+// (the products of 16-bit values are exact in fp32).
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
+template <class DT>
+__device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c);
+template <>
+__device__ __forceinline__ float dot2<BF16>(uint32_t a, uint32_t b, float c) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a), __builtin_bit_cast(bf16x2_t, b), c, false);
+}
+template <>
+__device__ __forceinline__ float dot2<F16>(uint32_t a, uint32_t b, float c) {
+  return __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2_t, a), __builtin_bit_cast(f16x2_t, b), c, false);
+}
+template <>
+__device__ __forceinline__ float dot2<F32>(uint32_t, uint32_t, float c) {
+  return c;  // not used: fp32 rows take the fused multiply-add path
+}
+
 // Owner layer of an absolute layer index (cross-layer index sharing).
 __host__ __device__ __forceinline__ int owner_layer(int l, int period, int start) {
   if (period <= 1 || l < start) return l;

@@ -15,6 +15,7 @@ struct DecodeArgs {
   void* out;           // [L][B][Hq][d]
   float* lse;          // [L][B][Hq] or null
   float* part;         // split-K partials [units][splits][G][d + 2]
+  int* cnt;            // split-K arrival counters [units], zero between launches
   int Ts, s, C, k_sel, Hq, Hkv, splits;  // C = ceil(Ts / s)
   float qscale;        // sm_scale * log2(e)
 };
@@ -24,7 +25,7 @@ struct DecodePlan {
   int splits;  // workgroups per unit
 };
 DecodePlan decode_plan(int units, int n_slot, int D, int elt);
-hipError_t launch_sparse_decode(const DecodeArgs& a, int dtype, int D, int G, int units, int waves,
+hipError_t launch_sparse_decode(const DecodeArgs& a, int dtype, int D, int G, int units, const DecodePlan& p,
                                 hipStream_t st);
 
 }  // namespace mpc

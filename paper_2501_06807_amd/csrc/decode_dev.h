@@ -15,6 +15,8 @@ __device__ __forceinline__ void attend_unit(const DecodeArgs& a, int unit, int s
   constexpr int EPL = DT::kVec;
   constexpr int LPR = D / EPL;
   constexpr int RPW = kWave / LPR;
+  constexpr bool kDot2 = DT::kElt == 2;
+  constexpr float kSlack = 8.f;
   static_assert(LPR <= kWave && kWave % LPR == 0, "row must fit a wave");
 
   __shared__ int32_t s_sel[kMaxSel];
@@ -34,13 +36,19 @@ __device__ __forceinline__ void attend_unit(const DecodeArgs& a, int unit, int s
 
   // unit = (l * B + b) * Hkv + h ; q-heads h*G .. h*G+G-1 of the same (l, b)
   const size_t q_row0 = (size_t)(unit / a.Hkv) * a.Hq + (size_t)(unit % a.Hkv) * G;
+  // 16-bit types: q stays packed and the dot products use the two-wide dot instructions (exact
+  // bf16 / fp16 products, fp32 sums), scaled afterwards; fp32: q pre-scaled, fused multiply-adds
+  uint4 qraw[G];
   float qf[G][EPL];
 #pragma unroll
   for (int g = 0; g < G; ++g) {
-    float t[EPL];
-    unpack<DT>(ldg16((const char*)a.q + ((q_row0 + g) * D + li * EPL) * DT::kElt), t);
+    qraw[g] = ldg16((const char*)a.q + ((q_row0 + g) * D + li * EPL) * DT::kElt);
+    if constexpr (!kDot2) {
+      float t[EPL];
+      unpack<DT>(qraw[g], t);
 #pragma unroll
-    for (int e = 0; e < EPL; ++e) qf[g][e] = t[e] * a.qscale;
+      for (int e = 0; e < EPL; ++e) qf[g][e] = t[e] * a.qscale;
+    }
   }
   __syncthreads();
 
@@ -59,46 +67,87 @@ __device__ __forceinline__ void attend_unit(const DecodeArgs& a, int unit, int s
     for (int e = 0; e < EPL; ++e) acc[g][e] = 0.f;
   }
 
-  for (int base = lo; base < hi; base += NW * RPW * U) {
-    uint4 kr[U], vr[U];
-    bool ok[U];
+  // slot cursors: slot = cluster position * s + row; each step of the loop advances every
+  // cursor by STEP slots without a division
+  constexpr int STEP = NW * RPW * U;
+  int cpos[U], crow[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int sl = lo + (u * NW + w) * RPW + rg;
+    cpos[u] = sl / a.s;
+    crow[u] = sl % a.s;
+  }
+  const int step_pos = STEP / a.s, step_row = STEP % a.s;
+
+  // gathers the U rows of every lane for the step at slot `base` and advances the cursors
+  auto fetch = [&](int base, uint4 (&kr)[U], uint4 (&vr)[U], bool (&ok)[U]) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      // slot -> (selected cluster, row in cluster); ids come from the caller, so anything outside
-      // [0, C) or past the kept length contributes nothing (and loads row 0 harmlessly)
+      // ids come from the caller, so anything outside [0, C) or past the kept length contributes
+      // nothing (and loads row 0 harmlessly)
       const int sl = base + (u * NW + w) * RPW + rg;
-      const int slc = min(sl, hi - 1);
-      const int c = s_sel[slc / a.s];
-      const int r = c * a.s + slc % a.s;
+      const int c = s_sel[min(cpos[u], a.k_sel - 1)];
+      const int r = c * a.s + crow[u];
       ok[u] = (sl < hi) & ((unsigned)c < (unsigned)a.C) & (r < a.Ts);
-      const size_t off = ((size_t)(ok[u] ? r : 0) * D + li * EPL) * DT::kElt;
+      const unsigned off = (unsigned)(ok[u] ? r : 0) * (unsigned)(D * DT::kElt) + (unsigned)(li * 16);
       kr[u] = ldg16(kbase + off);
       vr[u] = ldg16(vbase + off);
+      crow[u] += step_row;
+      cpos[u] += step_pos;
+      if (crow[u] >= a.s) {
+        crow[u] -= a.s;
+        ++cpos[u];
+      }
     }
+  };
+
+  for (int base = lo; base < hi; base += STEP) {
+    uint4 kr[U], vr[U];
+    bool ok[U];
+    fetch(base, kr, vr, ok);
     float sc[U][G];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       float kf[EPL];
-      unpack<DT>(kr[u], kf);
+      if constexpr (!kDot2) unpack<DT>(kr[u], kf);
 #pragma unroll
       for (int g = 0; g < G; ++g) {
         float p = 0.f;
+        if constexpr (kDot2) {
+          p = dot2<DT>(qraw[g].x, kr[u].x, p);
+          p = dot2<DT>(qraw[g].y, kr[u].y, p);
+          p = dot2<DT>(qraw[g].z, kr[u].z, p);
+          p = dot2<DT>(qraw[g].w, kr[u].w, p);
+        } else {
 #pragma unroll
-        for (int e = 0; e < EPL; ++e) p += qf[g][e] * kf[e];
+          for (int e = 0; e < EPL; ++e) p += qf[g][e] * kf[e];
+        }
         p = group_sum<LPR>(p);
+        if constexpr (kDot2) p *= a.qscale;
         sc[u][g] = ok[u] ? p : -INFINITY;
       }
     }
+    // The running maximum is refreshed only when a score exceeds it by more than kSlack (log2
+    // units): exponentials stay below 2^kSlack, and the rescale of l and acc is skipped by the
+    // whole wave in almost every step. Any reference maximum gives the same normalised result.
+    float mx[G];
+    bool up = false;
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-      float mx = m[g];
+      mx[g] = m[g];
 #pragma unroll
-      for (int u = 0; u < U; ++u) mx = fmaxf(mx, sc[u][g]);
-      const float r = fast_exp2(m[g] - mx);
-      l[g] *= r;
+      for (int u = 0; u < U; ++u) mx[g] = fmaxf(mx[g], sc[u][g]);
+      up |= mx[g] > m[g] + kSlack;
+    }
+    if (__any(up)) {
 #pragma unroll
-      for (int e = 0; e < EPL; ++e) acc[g][e] *= r;
-      m[g] = mx;
+      for (int g = 0; g < G; ++g) {
+        const float r = fast_exp2(m[g] - mx[g]);
+        l[g] *= r;
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) acc[g][e] *= r;
+        m[g] = mx[g];
+      }
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -158,13 +207,45 @@ __device__ __forceinline__ void attend_unit(const DecodeArgs& a, int unit, int s
       store_elt<DT>(a.out, (q_row0 + g) * D + dim, O / L);
       if (dim == 0 && a.lse) a.lse[q_row0 + g] = (M + __log2f(L)) * 0.69314718055994531f;
     } else {
+      // partial of this split, written device-coherently for the split that merges
       float* p = a.part + (((size_t)unit * a.splits + split) * G + g) * (D + 2);
-      p[dim] = O;
+      st_coherent(p + dim, O);
       if (dim == 0) {
-        p[D] = M;
-        p[D + 1] = L;
+        st_coherent(p + D, M);
+        st_coherent(p + D + 1, L);
       }
     }
+  }
+  if (a.splits == 1) return;
+
+  // Split-K: the last split of the unit to arrive merges all partials. Every split's partial
+  // stores have completed before its arrival is counted, and the merging split reads them with
+  // device-coherent loads, so no cache write-back fence is needed.
+  __shared__ int s_last;
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (tid == 0) {
+    const int c = __hip_atomic_fetch_add(&a.cnt[unit], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    s_last = c == a.splits - 1;
+    if (s_last) __hip_atomic_store(&a.cnt[unit], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  __syncthreads();
+  if (!s_last) return;
+  for (int t = tid; t < G * D; t += NW * kWave) {
+    const int g = t / D, dim = t % D;
+    const float* p0 = a.part + ((size_t)unit * a.splits * G + g) * (D + 2);
+    const size_t stride = (size_t)G * (D + 2);
+    float M = -1e30f;
+    for (int i = 0; i < a.splits; ++i) M = fmaxf(M, ld_coherent(p0 + i * stride + D));
+    float L = 0.f, O = 0.f;
+    for (int i = 0; i < a.splits; ++i) {
+      const float* p = p0 + i * stride;
+      const float r = fast_exp2(ld_coherent(p + D) - M);
+      L += ld_coherent(p + D + 1) * r;
+      O += ld_coherent(p + dim) * r;
+    }
+    store_elt<DT>(a.out, (q_row0 + g) * D + dim, O / L);
+    if (dim == 0 && a.lse) a.lse[q_row0 + g] = (M + __log2f(L)) * 0.69314718055994531f;
   }
 }
 
