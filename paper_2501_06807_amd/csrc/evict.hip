@@ -99,7 +99,8 @@ __global__ __launch_bounds__(256) void k_rowstats(EvictArgs a) {
   const size_t kvunit = ((size_t)l * a.B + b) * a.Hkv + hq / G;
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, c32 = lane & 31, hl = lane >> 5;
 
-  const int t = rb * kRowBlock + w * 32 + c32;
+  const int row_w0 = rb * kRowBlock + w * 32;  // first window row of this wave
+  const int t = row_w0 + c32;
   const bool tvalid = t < a.W;
   const int tc = tvalid ? t : a.W - 1;
   const int pos = a.T - a.W + tc;
@@ -147,11 +148,19 @@ __global__ __launch_bounds__(256) void k_rowstats(EvictArgs a) {
       acc = M::run(af, qf[ks], acc);
     }
     const int j0 = it * 32;
+    // a tile wholly inside the causal triangle and the key range needs no per-element mask
+    // (uniform over the wave: its smallest row bounds every row's last visible key)
+    const bool full = j0 + 31 < a.T && (!a.causal || j0 + 31 <= a.T - a.W + row_w0);
     float tmax = -INFINITY;
+    if (full) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int j = j0 + acc_row(r, lane);
-      if (j < a.T && (!a.causal || j <= pos)) tmax = fmaxf(tmax, acc[r]);
+      for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, acc[r]);
+    } else {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int j = j0 + acc_row(r, lane);
+        if (j < a.T && (!a.causal || j <= pos)) tmax = fmaxf(tmax, acc[r]);
+      }
     }
     if (tmax > m) {
       if (ell > 0.0) ell *= exp2(((double)m - (double)tmax) * a.c64);
@@ -161,11 +170,16 @@ __global__ __launch_bounds__(256) void k_rowstats(EvictArgs a) {
       bl = (float)(nb - (double)bh);
     }
     float ps = 0.f;
+    if (full) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int j = j0 + acc_row(r, lane);
-      if (j < a.T && (!a.causal || j <= pos))
-        ps += fast_exp2(fmaf(a.c_hi, acc[r], bh) + fmaf(a.c_lo, acc[r], bl));
+      for (int r = 0; r < 16; ++r) ps += fast_exp2(fmaf(a.c_hi, acc[r], bh) + fmaf(a.c_lo, acc[r], bl));
+    } else {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int j = j0 + acc_row(r, lane);
+        if (j < a.T && (!a.causal || j <= pos))
+          ps += fast_exp2(fmaf(a.c_hi, acc[r], bh) + fmaf(a.c_lo, acc[r], bl));
+      }
     }
     ell += (double)ps;
     if (it + 1 < ntile) stash(buf ^ 1);
@@ -279,11 +293,18 @@ __global__ __launch_bounds__(256) void k_colsum(EvictArgs a) {
         acc = M::run(af, kf[nb][ks], acc);
       }
       const int j = jw + nb * 32 + c32;
+      // every row of the tile valid and every key of the wave visible to its first row
+      const bool full = t0 + 31 < a.W && (!a.causal || jw + nb * 32 + 31 <= a.T - a.W + t0);
       float ps = 0.f;
+      if (full) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        if (trow[r] < a.W && (!a.causal || j <= a.T - a.W + trow[r]))
-          ps += fast_exp2(fmaf(a.c_hi, acc[r], bhr[r]) + fmaf(a.c_lo, acc[r], blr[r]));
+        for (int r = 0; r < 16; ++r) ps += fast_exp2(fmaf(a.c_hi, acc[r], bhr[r]) + fmaf(a.c_lo, acc[r], blr[r]));
+      } else {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          if (trow[r] < a.W && (!a.causal || j <= a.T - a.W + trow[r]))
+            ps += fast_exp2(fmaf(a.c_hi, acc[r], bhr[r]) + fmaf(a.c_lo, acc[r], blr[r]));
+        }
       }
       cacc[nb] += (double)ps;
     }
