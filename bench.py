@@ -164,67 +164,64 @@ def main():
     torch.cuda.synchronize()
 
     fused = args.decode_mode == "fused"
-
-    def decode_steps(ev, split):
-        for e in range(E):
-            if ev:
-                ev["sel"][e].record()
-            if split:
-                path.select(qs[e])
-                if ev:
-                    ev["att"][e].record()
-                path.attend(qs[e])
-            else:
-                path.decode_fused(qs[e])
-            if ev:
-                ev["end"][e].record()
+    step_fn = path.decode_fused if fused else path.decode
+    mk = lambda: torch.cuda.Event(enable_timing=True)
+    mean = lambda x: sum(x) / len(x)
 
     def one_pass(ev=None):
         if ev:
-            ev["start"].record()
+            ev[0].record()
         path.prefill(q_win, k, v)
         if ev:
-            ev["prefill"].record()
-        decode_steps(ev, not fused)
+            ev[1].record()
+        for e in range(E):
+            step_fn(qs[e])
+        if ev:
+            ev[2].record()
 
     for _ in range(args.warmup):
         one_pass()
     torch.cuda.synchronize()
 
-    mk = lambda: torch.cuda.Event(enable_timing=True)
-    evs = [dict(start=mk(), prefill=mk(), sel=[mk() for _ in range(E)], att=[mk() for _ in range(E)],
-                end=[mk() for _ in range(E)]) for _ in range(args.steps)]
+    # timed region: events only at the pass boundaries and after the prefill, so that the decode
+    # steps run back to back as a serving loop would issue them
+    evs = [(mk(), mk(), mk()) for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for s in range(args.steps):
         one_pass(evs[s])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    pre_ms = [a.elapsed_time(b) for a, b, _ in evs]
+    dec_us = mean([b.elapsed_time(c) / E for _, b, c in evs]) * 1e3
 
-    mean = lambda x: sum(x) / len(x)
+    # per-kernel breakdown on the same state and queries: HIP events around each launch on the
+    # launch stream (each interval includes that launch's dispatch gap)
+    def kernel_times():
+        ev = [(mk(), mk(), mk()) for _ in range(E)]
+        for e in range(E):
+            ev[e][0].record()
+            path.select(qs[e])
+            ev[e][1].record()
+            path.attend(qs[e])
+            ev[e][2].record()
+        torch.cuda.synchronize()
+        return (mean([a.elapsed_time(b) for a, b, _ in ev]) * 1e3, mean([b.elapsed_time(c) for _, b, c in ev]) * 1e3)
 
-    def split_times(evs):
-        sel_ms = [ev["sel"][e].elapsed_time(ev["att"][e]) for ev in evs for e in range(E)]
-        att_ms = [ev["att"][e].elapsed_time(ev["end"][e]) for ev in evs for e in range(E)]
-        return mean(sel_ms) * 1e3, mean(att_ms) * 1e3
+    def step_time(fn):
+        a, b = mk(), mk()
+        a.record()
+        for e in range(E):
+            fn(qs[e])
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / E * 1e3
 
-    pre_ms = [ev["start"].elapsed_time(ev["prefill"]) for ev in evs]
-    dec_ms = [ev["sel"][e].elapsed_time(ev["end"][e]) for ev in evs for e in range(E)]
-    dec_us = mean(dec_ms) * 1e3
-    # the decode step in the other mode, after the timed region (same prefilled state, same queries)
-    ev2 = [dict(sel=[mk() for _ in range(E)], att=[mk() for _ in range(E)], end=[mk() for _ in range(E)])
-           for _ in range(2)]
-    decode_steps(None, fused)
-    for ev in ev2:
-        decode_steps(ev, fused)
-    torch.cuda.synchronize()
-    if fused:
-        sel_us, att_us = split_times(ev2)
-        alt = {"mode": "split", "us": round(sel_us + att_us, 3)}
-    else:
-        sel_us, att_us = split_times(evs)
-        alt = {"mode": "fused", "us": round(mean([ev["sel"][e].elapsed_time(ev["end"][e]) for ev in ev2
-                                                  for e in range(E)]) * 1e3, 3)}
+    kernel_times()
+    sel_us, att_us = kernel_times()
+    other = path.decode if fused else path.decode_fused
+    step_time(other)
+    alt = {"mode": "split" if fused else "fused", "us": round(step_time(other), 3)}
 
     owners = [l for l in range(w.n_layers) if M.owner_layer(l, w.share_period, w.share_start) == l]
     sel_b, att_b = decode_bytes(w, owners, path.sel.cpu().numpy(), path.C, path.S)
@@ -267,10 +264,11 @@ def main():
                    "decode_steps_per_pass": E},
         "decode_step": {"mode": args.decode_mode, "us": round(dec_us, 3), "algorithmic_bytes": step_b,
                         "achieved_GBps": round(dec_gbs, 1), "frac_of_hbm_peak": round(dec_gbs / HBM_PEAK_GBS, 4)},
-        "decode_step_two_kernels": {"us": round(sel_us + att_us, 3), "select_us": round(sel_us, 3),
-                                    "attention_us": round(att_us, 3), "attention_algorithmic_bytes": att_b,
-                                    "attention_GBps": round(att_gbs, 1),
-                                    "attention_frac_of_hbm_peak": round(att_gbs / HBM_PEAK_GBS, 4)},
+        "kernels": {"select_us": round(sel_us, 3), "attention_us": round(att_us, 3),
+                    "attention_algorithmic_bytes": att_b, "attention_GBps": round(att_gbs, 1),
+                    "attention_frac_of_hbm_peak": round(att_gbs / HBM_PEAK_GBS, 4),
+                    "note": "HIP events around each launch of the two-kernel step; each interval includes "
+                            "its dispatch gap"},
         "decode_step_other_mode": alt,
         "roofline": roofline,
         "prefill": {"ms_per_pass": round(mean(pre_ms), 3), "owner_layers": len(owners),

@@ -11,6 +11,7 @@
 namespace mpc {
 
 constexpr int kWave = 64;
+constexpr int kNumCU = 256;  // compute units of an MI355X
 
 // Element-type tags. A 16-byte vector holds kVec elements.
 struct F32 {

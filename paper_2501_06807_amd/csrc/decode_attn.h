@@ -4,7 +4,6 @@
 
 namespace mpc {
 
-constexpr int kNumCU = 256;      // compute units of an MI355X
 constexpr int kMaxSplits = 16;   // split-K limit (workspace bound)
 
 struct DecodeArgs {

@@ -49,14 +49,15 @@ hipError_t launch_dt_nw(const SelectArgs& a, int D, int units, size_t smem, hipS
   return hipGetLastError();
 }
 
-// Few owner heads: one 8-wave workgroup per head shortens each head's chain. Many heads (at least
-// two per CU): one wave per head, so every head is in flight at once.
+// At most one owner head per CU: one 8-wave workgroup per head shortens each head's chain. More
+// heads: 4-wave workgroups, so that all of them are resident at once. Many heads (at least two
+// per CU): one wave per head.
 template <class DT>
 hipError_t launch_dt(const SelectArgs& a, int D, size_t smem, hipStream_t st) {
   const int units = a.own.n * a.B * a.Hkv;
   if (units >= 512 && a.S <= dev::kWaveMaxSuper && a.NC <= dev::kWaveMaxCand && (D == 64 || D == 128))
     return launch_wave<DT>(a, D, st);
-  if (units < 512) return launch_dt_nw<DT, 8>(a, D, units, smem, st);
+  if (units <= kNumCU) return launch_dt_nw<DT, 8>(a, D, units, smem, st);
   return launch_dt_nw<DT, 4>(a, D, units, smem, st);
 }
 

@@ -153,6 +153,27 @@ def test_select_many_heads_matches_oracle():
     say(f"  tie swaps {swaps}")
 
 
+def test_select_mid_heads_matches_oracle():
+    """Between one and two owner heads per CU: the 4-wave workgroup-per-head kernel."""
+    w = synth.get("C3").with_(n_layers=8, batch=3, keep=1024, k_super=2)
+    say("[select mid heads] C3 shape L=8 B=3 Hkv=32 Ts=1024 k_super=2 k_clusters=12 (384 owner heads)")
+    k, _ = _cache(w, 0)
+    cent, scent = oracle.build_clusters(k, w.dtype, cluster=w.cluster, fanout=w.fanout, alpha=0.6,
+                                        share_period=w.share_period)
+    import paper_2501_06807_amd as M
+    cfg = M.select_cfg(w.cluster, w.fanout, w.k_super, w.k_clusters, 0.6, w.share_period)
+    q = _queries(w, 0, 3)
+    sel_ref, _ = oracle.select_clusters(q, cent, scent, w.dtype, Ts=w.keep, cluster=w.cluster, fanout=w.fanout,
+                                        k_super=w.k_super, k_clusters=w.k_clusters, share_period=w.share_period)
+    sel = torch.zeros(sel_ref.shape, dtype=torch.int32, device="cuda")
+    sc = torch.zeros(sel_ref.shape, dtype=torch.float32, device="cuda")
+    M.mpc_select_clusters(bits_to_torch(q, w.dtype), torch.from_numpy(cent).cuda(), torch.from_numpy(scent).cuda(),
+                          sel, cfg, Ts=w.keep, sel_score=sc)
+    torch.cuda.synchronize()
+    swaps = _check_selection(w, 0, q, cent, scent, sel.cpu().numpy(), sel_ref, sc.cpu().numpy())
+    say(f"  tie swaps {swaps}")
+
+
 @pytest.mark.parametrize("name", list(CASES))
 def test_sparse_attention_matches_oracle(name):
     w, layer0 = _workload(name)
