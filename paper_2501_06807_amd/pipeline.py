@@ -87,6 +87,18 @@ class MPCachePath:
         L._check("mpc_sparse_decode_attn",
                  self._attend_fn(*self._attend_args, ctypes.c_void_p(q.data_ptr()), *self._attend_mid, st))
 
+    def attend_call(self, sel):
+        """A prepared attention call that reads the selection from `sel` (same shape as self.sel)
+        instead of self.sel: returns f(q, stream=None)."""
+        if sel.shape != self.sel.shape or sel.dtype != torch.int32 or not sel.is_contiguous():
+            raise ValueError("sel must be a contiguous int32 tensor shaped like the path's selection")
+        mid = (self._attend_mid[0], self._attend_mid[1], ctypes.c_void_p(sel.data_ptr())) + self._attend_mid[3:]
+
+        def call(q, stream=None):
+            L._check("mpc_sparse_decode_attn",
+                     self._attend_fn(*self._attend_args, ctypes.c_void_p(q.data_ptr()), *mid, L._stream(stream)))
+        return call
+
     def decode(self, q, stream=None):
         self.select(q, stream)
         self.attend(q, stream)
