@@ -15,7 +15,7 @@ namespace {
 
 template <class DT, int D, int G, int NW, int U>
 __global__ __launch_bounds__(NW* kWave) void k_sparse_decode(DecodeArgs a) {
-  dev::attend_unit<DT, D, G, NW, U, false>(a, blockIdx.x / a.splits, blockIdx.x % a.splits);
+  dev::attend<DT, D, G, NW, U, false>(a, blockIdx.x / a.splits, blockIdx.x % a.splits);
 }
 
 template <class DT, int D, int G>

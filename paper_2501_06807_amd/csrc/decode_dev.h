@@ -8,6 +8,72 @@ namespace dev {
 
 constexpr int kMaxSel = 1024;
 
+// Cross-wave merge of one unit's (m, l, acc) from LDS, then the output (one split) or the split-K
+// partial and, for the last split to arrive, the merge of all partials.
+template <class DT, int D, int G, int NW>
+__device__ __forceinline__ void finish_unit(const DecodeArgs& a, int unit, int split, size_t q_row0,
+                                            const float (*s_m)[G], const float (*s_l)[G],
+                                            const float (*s_acc)[G][D]) {
+  const int tid = threadIdx.x;
+  // merge the NW waves
+  for (int t = tid; t < G * D; t += NW * kWave) {
+    const int g = t / D, dim = t % D;
+    float M = -1e30f;
+#pragma unroll
+    for (int i = 0; i < NW; ++i) M = fmaxf(M, s_m[i][g]);
+    float L = 0.f, O = 0.f;
+#pragma unroll
+    for (int i = 0; i < NW; ++i) {
+      const float r = fast_exp2(s_m[i][g] - M);
+      L += s_l[i][g] * r;
+      O += s_acc[i][g][dim] * r;
+    }
+    if (a.splits == 1) {
+      store_elt<DT>(a.out, (q_row0 + g) * D + dim, O / L);
+      if (dim == 0 && a.lse) a.lse[q_row0 + g] = (M + __log2f(L)) * 0.69314718055994531f;
+    } else {
+      // partial of this split, written device-coherently for the split that merges
+      float* p = a.part + (((size_t)unit * a.splits + split) * G + g) * (D + 2);
+      st_coherent(p + dim, O);
+      if (dim == 0) {
+        st_coherent(p + D, M);
+        st_coherent(p + D + 1, L);
+      }
+    }
+  }
+  if (a.splits == 1) return;
+
+  // Split-K: the last split of the unit to arrive merges all partials. Every split's partial
+  // stores have completed before its arrival is counted, and the merging split reads them with
+  // device-coherent loads, so no cache write-back fence is needed.
+  __shared__ int s_last;
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (tid == 0) {
+    const int c = __hip_atomic_fetch_add(&a.cnt[unit], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    s_last = c == a.splits - 1;
+    if (s_last) __hip_atomic_store(&a.cnt[unit], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  __syncthreads();
+  if (!s_last) return;
+  for (int t = tid; t < G * D; t += NW * kWave) {
+    const int g = t / D, dim = t % D;
+    const float* p0 = a.part + ((size_t)unit * a.splits * G + g) * (D + 2);
+    const size_t stride = (size_t)G * (D + 2);
+    float M = -1e30f;
+    for (int i = 0; i < a.splits; ++i) M = fmaxf(M, ld_coherent(p0 + i * stride + D));
+    float L = 0.f, O = 0.f;
+    for (int i = 0; i < a.splits; ++i) {
+      const float* p = p0 + i * stride;
+      const float r = fast_exp2(ld_coherent(p + D) - M);
+      L += ld_coherent(p + D + 1) * r;
+      O += ld_coherent(p + dim) * r;
+    }
+    store_elt<DT>(a.out, (q_row0 + g) * D + dim, O / L);
+    if (dim == 0 && a.lse) a.lse[q_row0 + g] = (M + __log2f(L)) * 0.69314718055994531f;
+  }
+}
+
 // Attention of one work unit (or one split of it). COH_SEL: read the selection with
 // device-coherent loads (it was written by another workgroup of the same launch).
 template <class DT, int D, int G, int NW, int U, bool COH_SEL>
@@ -190,63 +256,199 @@ __device__ __forceinline__ void attend_unit(const DecodeArgs& a, int unit, int s
   }
   __syncthreads();
 
-  // merge the NW waves
-  for (int t = tid; t < G * D; t += NW * kWave) {
-    const int g = t / D, dim = t % D;
-    float M = -1e30f;
+  finish_unit<DT, D, G, NW>(a, unit, split, q_row0, s_m, s_l, s_acc);
+}
+
+// Groups of four query heads over 16-bit rows: the scores come from the matrix cores
+// (v_mfma_f32_16x16x32_{bf16,f16}: A = the group's four queries, each repeated on four rows,
+// B = 16 gathered key rows), so every lane receives the four head scores of one token with no
+// cross-lane reduction; p·V stays on the VALU in the row layout, each lane taking its row's
+// probabilities from the score lane with one cross-lane read per head. The reference maximum is
+// uniform over the wave (refreshed with a wave reduction only when a score exceeds it by more than
+// the slack), so the row layout's partial sums need no rescale when they meet.
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
+
+template <class DT>
+__device__ __forceinline__ f32x4_t mfma16(uint4 a, uint4 b, f32x4_t c);
+template <>
+__device__ __forceinline__ f32x4_t mfma16<BF16>(uint4 a, uint4 b, f32x4_t c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b), c,
+                                                 0, 0, 0);
+}
+template <>
+__device__ __forceinline__ f32x4_t mfma16<F16>(uint4 a, uint4 b, f32x4_t c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, a), __builtin_bit_cast(f16x8_t, b), c,
+                                                0, 0, 0);
+}
+
+__device__ __forceinline__ float wave_max(float x) {
 #pragma unroll
-    for (int i = 0; i < NW; ++i) M = fmaxf(M, s_m[i][g]);
-    float L = 0.f, O = 0.f;
+  for (int o = 32; o > 0; o >>= 1) x = fmaxf(x, __shfl_xor(x, o));
+  return x;
+}
+
+template <class DT, int D, int NW, bool COH_SEL>
+__device__ __forceinline__ void attend_unit_g4(const DecodeArgs& a, int unit, int split) {
+  constexpr int G = 4;
+  constexpr int EPL = 8;              // 16-bit elements per 16-byte vector
+  constexpr int LPR = D / EPL;        // lanes per row (row layout)
+  constexpr int RPW = kWave / LPR;    // rows per row-layout load
+  constexpr int UV = 16 / RPW;        // row-layout loads per 16 tokens
+  constexpr int KK = D / 32;          // matrix-core steps over d
+  constexpr int STEP = NW * 16;       // slots per workgroup step (16 per wave)
+  constexpr float kSlack = 8.f;
+  static_assert(DT::kElt == 2 && (D == 64 || D == 128), "16-bit rows, d = 64 or 128");
+
+  __shared__ int32_t s_sel[kMaxSel];
+  __shared__ float s_m[NW][G], s_l[NW][G];
+  __shared__ float s_acc[NW][G][D];
+
+  const int tid = threadIdx.x, lane = tid % kWave, w = tid / kWave;
+  const int tk = lane % 16, kq = lane / 16;    // score layout: token of the 16, quarter of a 32-wide k step
+  const int rg = lane / LPR, li = lane % LPR;  // row layout: row of the load, 16-byte column
+
+  for (int i = tid; i < a.k_sel; i += NW * kWave) {
+    const int32_t* src = a.sel + (size_t)unit * a.k_sel + i;
+    if constexpr (COH_SEL)
+      s_sel[i] = __hip_atomic_load(src, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    else
+      s_sel[i] = *src;
+  }
+  const size_t q_row0 = (size_t)(unit / a.Hkv) * a.Hq + (size_t)(unit % a.Hkv) * G;
+  uint4 qa[KK];  // A operand: row tk holds head tk % 4
 #pragma unroll
-    for (int i = 0; i < NW; ++i) {
-      const float r = fast_exp2(s_m[i][g] - M);
-      L += s_l[i][g] * r;
-      O += s_acc[i][g][dim] * r;
+  for (int kk = 0; kk < KK; ++kk)
+    qa[kk] = ldg16((const char*)a.q + ((q_row0 + tk % G) * D + kk * 32 + kq * 8) * DT::kElt);
+  __syncthreads();
+
+  const int n_slot = a.k_sel * a.s;
+  const int chunk = (n_slot + a.splits - 1) / a.splits;
+  const int lo = split * chunk, hi = min(n_slot, lo + chunk);
+  const char* kbase = (const char*)a.k + (size_t)unit * a.Ts * D * DT::kElt;
+  const char* vbase = (const char*)a.v + (size_t)unit * a.Ts * D * DT::kElt;
+
+  // slot cursors (cluster position, row), advanced by STEP slots per step without a division:
+  // [0] the score-layout token of this lane, [1 + u] its row-layout rows
+  int cpos[1 + UV], crow[1 + UV];
+#pragma unroll
+  for (int j = 0; j < 1 + UV; ++j) {
+    const int sl = lo + w * 16 + (j == 0 ? tk : (j - 1) * RPW + rg);
+    cpos[j] = sl / a.s;
+    crow[j] = sl % a.s;
+  }
+  const int step_pos = STEP / a.s, step_row = STEP % a.s;
+  // row of cursor j at step `base`; invalid slots read row 0 and are masked
+  auto row_of = [&](int j, int sl, bool& ok) {
+    const int c = s_sel[min(cpos[j], a.k_sel - 1)];
+    const int r = c * a.s + crow[j];
+    ok = (sl < hi) & ((unsigned)c < (unsigned)a.C) & (r < a.Ts);
+    crow[j] += step_row;
+    cpos[j] += step_pos;
+    if (crow[j] >= a.s) {
+      crow[j] -= a.s;
+      ++cpos[j];
     }
-    if (a.splits == 1) {
-      store_elt<DT>(a.out, (q_row0 + g) * D + dim, O / L);
-      if (dim == 0 && a.lse) a.lse[q_row0 + g] = (M + __log2f(L)) * 0.69314718055994531f;
-    } else {
-      // partial of this split, written device-coherently for the split that merges
-      float* p = a.part + (((size_t)unit * a.splits + split) * G + g) * (D + 2);
-      st_coherent(p + dim, O);
-      if (dim == 0) {
-        st_coherent(p + D, M);
-        st_coherent(p + D + 1, L);
+    return (unsigned)(ok ? r : 0) * (unsigned)(D * DT::kElt);
+  };
+
+  float m[G], l[G], acc[G][EPL];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    m[g] = -1e30f;
+    l[g] = 0.f;
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) acc[g][e] = 0.f;
+  }
+
+  for (int base = lo; base < hi; base += STEP) {
+    bool okk;
+    const unsigned koff = row_of(0, base + w * 16 + tk, okk);
+    uint4 kr[KK];
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) kr[kk] = ldg16(kbase + koff + (kk * 32 + kq * 8) * DT::kElt);
+    uint4 vr[UV];
+#pragma unroll
+    for (int u = 0; u < UV; ++u) {
+      bool okv;
+      const unsigned voff = row_of(1 + u, base + w * 16 + u * RPW + rg, okv);
+      vr[u] = ldg16(vbase + voff + li * 16);  // a masked row contributes p = 0
+    }
+    f32x4_t sacc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) sacc = mfma16<DT>(qa[kk], kr[kk], sacc);
+    float sc[G];
+    bool up = false;
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      sc[g] = okk ? sacc[g] * a.qscale : -INFINITY;
+      up |= sc[g] > m[g] + kSlack;
+    }
+    if (__any(up)) {
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const float mx = wave_max(fmaxf(m[g], sc[g]));
+        const float r = fast_exp2(m[g] - mx);
+        l[g] *= r;
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) acc[g][e] *= r;
+        m[g] = mx;
+      }
+    }
+    float p[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      p[g] = fast_exp2(sc[g] - m[g]);
+      l[g] += p[g];
+    }
+#pragma unroll
+    for (int u = 0; u < UV; ++u) {
+      float vf[EPL];
+      unpack<DT>(vr[u], vf);
+      const int src = u * RPW + rg;  // score lane of this row's token
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const float pg = __shfl(p[g], src);
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) acc[g][e] += pg * vf[e];
       }
     }
   }
-  if (a.splits == 1) return;
 
-  // Split-K: the last split of the unit to arrive merges all partials. Every split's partial
-  // stores have completed before its arrival is counted, and the merging split reads them with
-  // device-coherent loads, so no cache write-back fence is needed.
-  __shared__ int s_last;
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  if (tid == 0) {
-    const int c = __hip_atomic_fetch_add(&a.cnt[unit], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    s_last = c == a.splits - 1;
-    if (s_last) __hip_atomic_store(&a.cnt[unit], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
-  __syncthreads();
-  if (!s_last) return;
-  for (int t = tid; t < G * D; t += NW * kWave) {
-    const int g = t / D, dim = t % D;
-    const float* p0 = a.part + ((size_t)unit * a.splits * G + g) * (D + 2);
-    const size_t stride = (size_t)G * (D + 2);
-    float M = -1e30f;
-    for (int i = 0; i < a.splits; ++i) M = fmaxf(M, ld_coherent(p0 + i * stride + D));
-    float L = 0.f, O = 0.f;
-    for (int i = 0; i < a.splits; ++i) {
-      const float* p = p0 + i * stride;
-      const float r = fast_exp2(ld_coherent(p + D) - M);
-      L += ld_coherent(p + D + 1) * r;
-      O += ld_coherent(p + dim) * r;
+  // the wave's rows meet: acc over the row groups, l over the 16 token lanes (each group of 16
+  // lanes holds the same tokens' probabilities)
+#pragma unroll
+  for (int o = LPR; o < kWave; o <<= 1)
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) acc[g][e] += __shfl_xor(acc[g][e], o);
+#pragma unroll
+  for (int g = 0; g < G; ++g) l[g] = group_sum<16>(l[g]);
+  if (rg == 0) {
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) s_acc[w][g][li * EPL + e] = acc[g][e];
+      if (li == 0) {
+        s_m[w][g] = m[g];
+        s_l[w][g] = l[g];
+      }
     }
-    store_elt<DT>(a.out, (q_row0 + g) * D + dim, O / L);
-    if (dim == 0 && a.lse) a.lse[q_row0 + g] = (M + __log2f(L)) * 0.69314718055994531f;
   }
+  __syncthreads();
+  finish_unit<DT, D, G, NW>(a, unit, split, q_row0, s_m, s_l, s_acc);
+}
+
+// The attention path of a unit: matrix-core scores for four-head groups of 16-bit rows, the VALU
+// path otherwise.
+template <class DT, int D, int G, int NW, int U, bool COH_SEL>
+__device__ __forceinline__ void attend(const DecodeArgs& a, int unit, int split) {
+  if constexpr (G == 4 && DT::kElt == 2)
+    attend_unit_g4<DT, D, NW, COH_SEL>(a, unit, split);
+  else
+    attend_unit<DT, D, G, NW, U, COH_SEL>(a, unit, split);
 }
 
 }  // namespace dev

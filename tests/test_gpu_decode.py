@@ -199,7 +199,7 @@ def test_sparse_attention_matches_oracle(name):
 
 
 @pytest.mark.parametrize("dtype,Ts,s,G", [("bf16", 1000, 32, 4), ("fp16", 333, 16, 2), ("fp32", 200, 16, 1),
-                                          ("bf16", 77, 8, 8)])
+                                          ("bf16", 77, 8, 8), ("fp16", 500, 16, 4), ("bf16", 130, 64, 1)])
 def test_full_budget_equals_dense_attention_ragged(dtype, Ts, s, G):
     """Every cluster selected (partial last cluster included) = dense decode attention."""
     say(f"[dense] dtype={dtype} Ts={Ts} s={s} G={G}")
