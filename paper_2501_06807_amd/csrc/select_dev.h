@@ -101,27 +101,58 @@ __device__ __forceinline__ int count_above(const unsigned long long* key, int j0
   return c;
 }
 
-// rank[i] (number of entries with a larger composite key) for all entries: every thread takes an
-// (entry, slice) pair so that small sets still use all lanes; slice counts meet in LDS (rank[] must
-// start at zero).
-template <int NT>
-__device__ void rank_all(const unsigned long long* key, int n, int* rank) {
-  const int parts = n < NT ? min(NT / n, 8) : 1;
-  for (int t = threadIdx.x; t < n * parts; t += NT) {
-    const int i = t % n, part = t / n;
-    atomicAdd(&rank[i], count_above(key, part * n / parts, (part + 1) * n / parts, key[i]));
-  }
+// Top k of n entries by composite key, by one workgroup: top[r] = entry of rank r < k, bnd[0] /
+// bnd[1] = entries of rank k-1 / k (or -1). Small sets: every entry counts the keys above it.
+// Larger sets (a tournament): each slice of 32 entries keeps its local top k+1 in a list, then
+// the list entries count the list keys above them. An entry of global rank r <= k is in the list
+// (fewer than k+1 keys of its slice beat it) and so is every key above it, so its count is its
+// rank; an entry of rank > k finds at least k+1 list keys above it (a slice holding a key above
+// it that is not in the list contributes its whole top k+1). list_k / list_i hold
+// ceil(n / 32) * (k + 1) entries; ends with a barrier.
+constexpr int kSlice = 32;
+
+__host__ __device__ inline bool use_tournament(int n, int k) {
+  return n > 2 * kSlice && ((n + kSlice - 1) / kSlice) * (k + 1) * 2 <= n;
 }
 
-// top[r] = i for the entries of composite rank r < k; bnd[0] / bnd[1] = entries of rank k-1 / k.
 template <int NT>
-__device__ __forceinline__ void scatter_top(const int* rank, int n, int k, int* top, int* bnd) {
-  for (int i = threadIdx.x; i < n; i += NT) {
-    const int r = rank[i];
+__device__ void block_topk(const unsigned long long* ck, int n, int k, unsigned long long* list_k, int* list_i,
+                           int* top, int* bnd) {
+  const int tid = threadIdx.x;
+  if (!use_tournament(n, k)) {
+    for (int i = tid; i < n; i += NT) {
+      const int r = count_above(ck, 0, n, ck[i]);
+      if (r < k) top[r] = i;
+      if (r == k - 1) bnd[0] = i;
+      if (r == k) bnd[1] = i;
+    }
+    __syncthreads();
+    return;
+  }
+  const int m = (n + kSlice - 1) / kSlice * (k + 1);
+  for (int c = tid; c < m; c += NT) {  // slots a short slice leaves empty: key 0 beats nothing
+    list_k[c] = 0ull;
+    list_i[c] = -1;
+  }
+  __syncthreads();
+  for (int i = tid; i < n; i += NT) {
+    const int s0 = i / kSlice * kSlice;
+    const int r = count_above(ck, s0, min(n, s0 + kSlice), ck[i]);
+    if (r <= k) {
+      list_k[i / kSlice * (k + 1) + r] = ck[i];
+      list_i[i / kSlice * (k + 1) + r] = i;
+    }
+  }
+  __syncthreads();
+  for (int c = tid; c < m; c += NT) {
+    const int i = list_i[c];
+    if (i < 0) continue;
+    const int r = count_above(list_k, 0, m, list_k[c]);
     if (r < k) top[r] = i;
     if (r == k - 1) bnd[0] = i;
     if (r == k) bnd[1] = i;
   }
+  __syncthreads();
 }
 
 // When the images of the entries at composite ranks k-1 and k tie, the composite order inside that
@@ -148,14 +179,18 @@ __device__ void repair_top(const double* sc, const uint32_t* img, int n, int k, 
 // Position of top[j] among top[0, k) in ascending entry order (entries are distinct).
 __device__ __forceinline__ int ascending_pos(const int* top, int k, int j) {
   const int v = top[j];
-  int p = 0;
-  for (int u = 0; u < k; ++u) p += top[u] < v;
+  int p = 0, u = 0;
+  for (; u + 4 <= k; u += 4) {
+    const int t0 = top[u], t1 = top[u + 1], t2 = top[u + 2], t3 = top[u + 3];
+    p += (t0 < v) + (t1 < v) + (t2 < v) + (t3 < v);
+  }
+  for (; u < k; ++u) p += top[u] < v;
   return p;
 }
 
 // LDS carve-up of the one-workgroup-per-head selection (host and device).
 struct BlockLds {
-  size_t qsum, s1, s2, ck, img1, img2, rank1, rank2, top, cand, total;
+  size_t qsum, s1, s2, ck, img1, img2, list_k, list_i, top, cand, total;
 };
 __host__ __device__ inline BlockLds block_lds(int D, int S, int NC) {
   auto al = [](size_t x) { return (x + 15) & ~(size_t)15; };
@@ -167,9 +202,9 @@ __host__ __device__ inline BlockLds block_lds(int D, int S, int NC) {
   o.ck = al(o.s2 + (size_t)NC * 8);
   o.img1 = al(o.ck + (size_t)m * 8);
   o.img2 = al(o.img1 + (size_t)S * 4);
-  o.rank1 = al(o.img2 + (size_t)NC * 4);
-  o.rank2 = al(o.rank1 + (size_t)S * 4);
-  o.top = al(o.rank2 + (size_t)NC * 4);
+  o.list_k = al(o.img2 + (size_t)NC * 4);  // a tournament list is at most half its set
+  o.list_i = al(o.list_k + (size_t)m * 8);
+  o.top = al(o.list_i + (size_t)m * 4);
   o.cand = al(o.top + (size_t)m * 4);
   o.total = al(o.cand + (size_t)NC * 4);
   return o;
@@ -189,8 +224,8 @@ __device__ void select_block(const SelectArgs& a, int ou, unsigned char* smem) {
   unsigned long long* ck = (unsigned long long*)(smem + lay.ck);  // composite keys, level 1 then 2
   uint32_t* img1 = (uint32_t*)(smem + lay.img1);
   uint32_t* img2 = (uint32_t*)(smem + lay.img2);
-  int* rank1 = (int*)(smem + lay.rank1);
-  int* rank2 = (int*)(smem + lay.rank2);
+  unsigned long long* list_k = (unsigned long long*)(smem + lay.list_k);
+  int* list_i = (int*)(smem + lay.list_i);
   int* top = (int*)(smem + lay.top);
   int* cand = (int*)(smem + lay.cand);
   __shared__ int bnd1[2], bnd2[2];
@@ -214,8 +249,6 @@ __device__ void select_block(const SelectArgs& a, int ou, unsigned char* smem) {
     for (int g = 0; g < G; ++g) acc += (double)load_elt<DT>(a.q, q0 + (size_t)g * D + i);
     qsum[i] = acc;
   }
-  for (int i = tid; i < a.S; i += NT) rank1[i] = 0;
-  for (int i = tid; i < a.NC; i += NT) rank2[i] = 0;
   if (tid < 2) {
     bnd1[tid] = -1;
     bnd2[tid] = -1;
@@ -229,10 +262,7 @@ __device__ void select_block(const SelectArgs& a, int ou, unsigned char* smem) {
     tile_dot<D, PASS>(tile, a.S, r0, qsum, s1, img1, ck);
   }
   __syncthreads();
-  rank_all<NT>(ck, a.S, rank1);
-  __syncthreads();
-  scatter_top<NT>(rank1, a.S, a.k_super, top, bnd1);
-  __syncthreads();
+  block_topk<NT>(ck, a.S, a.k_super, list_k, list_i, top, bnd1);
   repair_top<NT>(s1, img1, a.S, a.k_super, bnd1, top);
   for (int j = tid; j < a.k_super; j += NT) {
     const int sup = top[j], p = ascending_pos(top, a.k_super, j);
@@ -249,10 +279,7 @@ __device__ void select_block(const SelectArgs& a, int ou, unsigned char* smem) {
     tile_dot<D, PASS>(tile, a.NC, r0, qsum, s2, img2, ck);
   }
   __syncthreads();
-  rank_all<NT>(ck, a.NC, rank2);
-  __syncthreads();
-  scatter_top<NT>(rank2, a.NC, a.k_clusters, top, bnd2);
-  __syncthreads();
+  block_topk<NT>(ck, a.NC, a.k_clusters, list_k, list_i, top, bnd2);
   repair_top<NT>(s2, img2, a.NC, a.k_clusters, bnd2, top);
   for (int j = tid; j < a.k_clusters; j += NT) {
     const int i = top[j], p = ascending_pos(top, a.k_clusters, j);
