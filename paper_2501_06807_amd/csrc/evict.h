@@ -5,7 +5,7 @@
 namespace mpc {
 
 constexpr int kNumXcd = 8;       // accelerator dies; workgroup i runs on die i % 8
-constexpr int kRowBlock = 128;  // window rows per row-statistics workgroup (4 waves x 32)
+constexpr int kRowBlock = 256;  // window rows per row-statistics workgroup (8 waves x 32)
 constexpr int kColWaveKeys = 64;  // keys per wave in the column-sum pass (2 MFMA column blocks)
 constexpr int kColBlockKeys = 4 * kColWaveKeys;
 

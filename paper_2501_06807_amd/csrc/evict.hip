@@ -71,20 +71,22 @@ __device__ __forceinline__ int xcd_remap(int bid, int n) {
 
 // 32-row tiles of a [rows][D] matrix staged through LDS with 16-byte chunks; the row stride is
 // padded by 16 bytes to spread the 32 rows of a fragment read over the LDS banks.
-template <class DT, int D>
+template <class DT, int D, int NT = 256>
 struct Tile {
   static constexpr int RB = D * DT::kElt;
   static constexpr int RS = RB + 16;
   static constexpr int CH = RB / 16;
   static constexpr int CHUNKS = 32 * CH;
-  static constexpr int PER = (CHUNKS + 255) / 256;
+  static constexpr int PER = (CHUNKS + NT - 1) / NT;  // chunks per thread (NT threads)
   static constexpr int BYTES = 32 * RS;
 };
 
+constexpr int kRowThreads = kRowBlock / 32 * kWave;  // one wave per 32 window rows
+
 template <class DT, int D>
-__global__ __launch_bounds__(256) void k_rowstats(EvictArgs a) {
+__global__ __launch_bounds__(kRowThreads) void k_rowstats(EvictArgs a) {
   using M = Mma<DT>;
-  using TL = Tile<DT, D>;
+  using TL = Tile<DT, D, kRowThreads>;
   constexpr int KS = D / M::K;
   __shared__ __align__(16) unsigned char s_k[2][TL::BYTES];
 
@@ -118,7 +120,7 @@ __global__ __launch_bounds__(256) void k_rowstats(EvictArgs a) {
   auto fetch = [&](int tile) {
 #pragma unroll
     for (int i = 0; i < TL::PER; ++i) {
-      const int ch = tid + i * 256;
+      const int ch = tid + i * kRowThreads;
       const int row = ch / TL::CH, c16 = ch % TL::CH;
       const int j = tile * 32 + row;
       pre[i] = (ch < TL::CHUNKS && j < a.T) ? ldg16(kh + (size_t)j * TL::RB + c16 * 16) : make_uint4(0, 0, 0, 0);
@@ -127,7 +129,7 @@ __global__ __launch_bounds__(256) void k_rowstats(EvictArgs a) {
   auto stash = [&](int buf) {
 #pragma unroll
     for (int i = 0; i < TL::PER; ++i) {
-      const int ch = tid + i * 256;
+      const int ch = tid + i * kRowThreads;
       if (ch < TL::CHUNKS) *(uint4*)&s_k[buf][(ch / TL::CH) * TL::RS + (ch % TL::CH) * 16] = pre[i];
     }
   };
@@ -453,7 +455,7 @@ template <class DT, int D>
 hipError_t launch_pass(const EvictArgs& a, bool rows, hipStream_t st) {
   if (rows) {
     const int n_rb = (a.W + kRowBlock - 1) / kRowBlock;
-    hipLaunchKernelGGL((k_rowstats<DT, D>), dim3(a.own.n * a.B * a.Hq * n_rb), dim3(256), 0, st, a);
+    hipLaunchKernelGGL((k_rowstats<DT, D>), dim3(a.own.n * a.B * a.Hq * n_rb), dim3(kRowThreads), 0, st, a);
   } else {
     const int n_kb = (a.T + kColBlockKeys - 1) / kColBlockKeys;
     hipLaunchKernelGGL((k_colsum<DT, D>), dim3(a.own.n * a.B * a.Hkv * n_kb), dim3(256), 0, st, a);
