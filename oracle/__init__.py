@@ -33,13 +33,14 @@ def lib():
             "mpcref_static_topk": ([I, V, I, I, V], ctypes.c_int),
             "mpcref_cluster_bounds": ([I, I, I, V, I, I, V, V], ctypes.c_int),
             "mpcref_centroid": ([D, D, F], F),
-            "mpcref_cluster_scores": ([I, I, I, V, I, V, V], ctypes.c_int),
+            "mpcref_cluster_scores": ([I, I, I, I, V, I, V, V], ctypes.c_int),
+            "mpcref_cluster_mean": ([I, I, I, V, I, I, V], ctypes.c_int),
             "mpcref_mp_bound": ([I, V, V, V, V], ctypes.c_int),
             "mpcref_topk": ([I, V, I, V], ctypes.c_int),
             "mpcref_attend": ([I, I, F, V, I, V, V, V, V, V], ctypes.c_int),
             "mpcref_static_evict": ([I] * 11 + [F, I, I, I] + [V] * 7, ctypes.c_int),
-            "mpcref_build_clusters": ([I] * 9 + [F, I, I] + [V] * 3, ctypes.c_int),
-            "mpcref_select_clusters": ([I] * 14 + [V] * 5, ctypes.c_int),
+            "mpcref_build_clusters": ([I] * 9 + [F, I, I, I] + [V] * 3, ctypes.c_int),
+            "mpcref_select_clusters": ([I] * 15 + [V] * 5, ctypes.c_int),
             "mpcref_sparse_decode_attn": ([I] * 8 + [V] * 4 + [I, F, V, V], ctypes.c_int),
             "mpcref_dense_decode_attn": ([I] * 7 + [V] * 3 + [F, V, V], ctypes.c_int),
             "mpcref_threads": ([], ctypes.c_int),
@@ -140,14 +141,30 @@ def centroid(rmax, rmin, alpha):
     return lib().mpcref_centroid(float(rmax), float(rmin), float(alpha))
 
 
-def cluster_scores(q_group, cent, dtype):
-    """q_group [G][d] (raw bits), cent [n][d] float32 -> fp64 scores [n]."""
+SIMILARITY = {"linear": 0, "maxprod": 1, "mean": 2}
+
+
+def rep_rows(similarity):
+    """Rows of d floats per representative: r^max and r^min for the max-product bound."""
+    return 2 if SIMILARITY[similarity] == 1 else 1
+
+
+def cluster_scores(q_group, cent, dtype, similarity="linear"):
+    """q_group [G][d] (raw bits), cent [n][R][d] (or [n][d] when R = 1) float32 -> fp64 scores [n]."""
     q_group, cent = _c(q_group), _c(cent, np.float32)
     G, d = q_group.shape
     n = cent.shape[0]
     out = np.empty(n, np.float64)
-    _ok(lib().mpcref_cluster_scores(G, d, DTYPE_CODE[dtype], _p(q_group), n, _p(cent), _p(out)),
-        "mpcref_cluster_scores")
+    _ok(lib().mpcref_cluster_scores(G, d, DTYPE_CODE[dtype], SIMILARITY[similarity], _p(q_group), n, _p(cent),
+                                    _p(out)), "mpcref_cluster_scores")
+    return out
+
+
+def cluster_mean(k, dtype, first, count):
+    k = _c(k)
+    n_tok, d = k.shape
+    out = np.empty(d, np.float64)
+    _ok(lib().mpcref_cluster_mean(n_tok, d, DTYPE_CODE[dtype], _p(k), first, count, _p(out)), "mpcref_cluster_mean")
     return out
 
 
@@ -195,29 +212,33 @@ def static_evict(q_win, k, v, dtype, *, keep, local_keep, sm_scale, causal=True,
 
 
 def build_clusters(k_cache, dtype, *, cluster, fanout, alpha=0.6, layer0=0, share_period=1,
-                   share_start=2):
+                   share_start=2, similarity="linear"):
+    """-> cent [L][B][Hkv][C][d], scent [L][B][Hkv][S][d]; with similarity="maxprod" the
+    representative is two rows (r^max, r^min): [..][C][2][d], [..][S][2][d]."""
     k_cache = _c(k_cache)
     L, B, Hkv, Ts, d = k_cache.shape
     C = -(-Ts // cluster)
     S = -(-C // fanout)
-    cent = np.zeros((L, B, Hkv, C, d), np.float32)
-    scent = np.zeros((L, B, Hkv, S, d), np.float32)
+    R = rep_rows(similarity)
+    rows = (R, d) if R > 1 else (d,)
+    cent = np.zeros((L, B, Hkv, C) + rows, np.float32)
+    scent = np.zeros((L, B, Hkv, S) + rows, np.float32)
     _ok(lib().mpcref_build_clusters(B, layer0, L, Hkv, d, DTYPE_CODE[dtype], Ts, cluster, fanout, alpha,
-                                    share_period, share_start, _p(k_cache), _p(cent), _p(scent)),
-        "mpcref_build_clusters")
+                                    share_period, share_start, SIMILARITY[similarity], _p(k_cache), _p(cent),
+                                    _p(scent)), "mpcref_build_clusters")
     return cent, scent
 
 
 def select_clusters(q, cent, scent, dtype, *, Ts, cluster, fanout, k_super, k_clusters, layer0=0,
-                    share_period=1, share_start=2, sel_in=None):
+                    share_period=1, share_start=2, sel_in=None, similarity="linear"):
     q, cent, scent = _c(q), _c(cent, np.float32), _c(scent, np.float32)
     L, B, Hq, d = q.shape
     Hkv = cent.shape[2]
     sel = np.zeros((L, B, Hkv, k_clusters), np.int32) if sel_in is None else _c(sel_in, np.int32).copy()
     score = np.zeros((L, B, Hkv, k_clusters), np.float64)
     _ok(lib().mpcref_select_clusters(B, layer0, L, Hq, Hkv, d, DTYPE_CODE[dtype], Ts, cluster, fanout,
-                                     k_super, k_clusters, share_period, share_start, _p(q), _p(cent),
-                                     _p(scent), _p(sel), _p(score)), "mpcref_select_clusters")
+                                     k_super, k_clusters, share_period, share_start, SIMILARITY[similarity],
+                                     _p(q), _p(cent), _p(scent), _p(sel), _p(score)), "mpcref_select_clusters")
     return sel, score
 
 

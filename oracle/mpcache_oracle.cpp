@@ -9,7 +9,10 @@
 //   mpcref_static_topk     pinned (full-sort ranking vs numpy lexsort, ties, identity budget)
 //   mpcref_cluster_bounds  pinned (numpy max/min, member bounds = token bounds)
 //   mpcref_centroid        pinned (alpha = 1 / 0 give the bounds, fp32 rounding by numpy float32)
-//   mpcref_cluster_scores  pinned (Eq. 2 ordering: linear score <= MP bound >= max dot product)
+//   mpcref_cluster_scores  pinned (Eq. 2 ordering: linear score <= MP bound >= max dot product;
+//                          single-token clusters give the dot product in every mode; with a
+//                          non-negative query the bound equals the alpha = 1 linear score)
+//   mpcref_cluster_mean    pinned (numpy mean in fp64)
 //   mpcref_topk            pinned (numpy lexsort)
 //   mpcref_attend          pinned (torch scaled_dot_product_attention, fp64)
 //   the rule functions     pinned by the integers stated for the five workloads
@@ -208,6 +211,23 @@ int mpcref_cluster_bounds(int32_t n_tok, int32_t d, int32_t dtype, const void* k
   return OK;
 }
 
+// Average of a cluster's keys, the naive representative the paper compares against (Sec. 3.3
+// opening; App. "comparison with average-based similarity"): the fp64 sum over the cluster's
+// tokens in token order divided by their count. Reading: the score is the dot product with this
+// average (like the other representatives), and it is stored rounded to fp32.
+int mpcref_cluster_mean(int32_t n_tok, int32_t d, int32_t dtype, const void* k, int32_t first,
+                        int32_t count, double* mean) {
+  if (n_tok <= 0 || d <= 0 || first < 0 || count <= 0 || first >= n_tok || !valid_dtype(dtype) ||
+      !k || !mean)
+    return EINVAL;
+  const int32_t last = std::min(n_tok, first + count);
+  for (int32_t i = 0; i < d; ++i) mean[i] = 0.0;
+  for (int32_t j = first; j < last; ++j)
+    for (int32_t i = 0; i < d; ++i) mean[i] += load(k, (size_t)j * d + i, dtype);
+  for (int32_t i = 0; i < d; ++i) mean[i] /= (double)(last - first);
+  return OK;
+}
+
 // Reordered linear similarity (Sec. 3.3, Eq. "sim"): the cluster is represented by
 // alpha * r^max + (1 - alpha) * r^min, precomputed once. Reading: it is stored in fp32, each
 // product rounded to fp32 and then their sum rounded to fp32, with alpha given in fp32 and
@@ -221,18 +241,28 @@ float mpcref_centroid(double rmax, double rmin, float alpha) {
   return (float)((double)pa + (double)pb);
 }
 
-// Similarity of the decode query with each cluster representative (Sec. 3.3, Eq. "sim"):
-// sum_i q_i * c_i. Reading for grouped heads: the G query heads of a kv head share one selection
-// scored by the sum of their similarities.
-int mpcref_cluster_scores(int32_t G, int32_t d, int32_t dtype, const void* q, int32_t n,
-                          const float* cent, double* score) {
-  if (G <= 0 || d <= 0 || n < 0 || !valid_dtype(dtype) || !q || (n && (!cent || !score)))
+// Similarity of the decode query with each cluster representative. Linear (Sec. 3.3, Eq. "sim")
+// and average: sum_i q_i * c_i with the stored representative c. Max-product bound (Sec. 3.3,
+// Eq. 2): sum_i max(q_i r^max_i, q_i r^min_i) over the stored bounds (rows r^max, r^min). Reading
+// for grouped heads: the G query heads of a kv head share one selection scored by the sum of their
+// similarities. `rep` holds n representatives of (similarity == 1 ? 2 : 1) rows of d floats.
+int mpcref_cluster_scores(int32_t G, int32_t d, int32_t dtype, int32_t similarity, const void* q,
+                          int32_t n, const float* rep, double* score) {
+  if (G <= 0 || d <= 0 || n < 0 || !valid_dtype(dtype) || similarity < 0 || similarity > 2 || !q ||
+      (n && (!rep || !score)))
     return EINVAL;
+  const int32_t R = similarity == 1 ? 2 : 1;
   for (int32_t c = 0; c < n; ++c) {
+    const float* r = rep + (size_t)c * R * d;
     double acc = 0.0;
     for (int32_t g = 0; g < G; ++g)
-      for (int32_t i = 0; i < d; ++i)
-        acc += load(q, (size_t)g * d + i, dtype) * (double)cent[(size_t)c * d + i];
+      for (int32_t i = 0; i < d; ++i) {
+        const double qi = load(q, (size_t)g * d + i, dtype);
+        if (similarity == 1)
+          acc += std::max(qi * (double)r[i], qi * (double)r[d + i]);
+        else
+          acc += qi * (double)r[i];
+      }
     score[c] = acc;
   }
   return OK;
@@ -339,12 +369,14 @@ int mpcref_static_evict(int32_t B, int32_t layer0, int32_t n_layers, int32_t Hq,
 // Only owner layers are written.
 int mpcref_build_clusters(int32_t B, int32_t layer0, int32_t n_layers, int32_t Hkv, int32_t d,
                           int32_t dtype, int32_t Ts, int32_t cluster, int32_t fanout, float alpha,
-                          int32_t share_period, int32_t share_start, const void* k_cache,
-                          float* cent, float* scent) {
+                          int32_t share_period, int32_t share_start, int32_t similarity,
+                          const void* k_cache, float* cent, float* scent) {
   if (B <= 0 || layer0 < 0 || n_layers <= 0 || Hkv <= 0 || d <= 0 || Ts <= 0 || cluster <= 0 ||
-      fanout <= 0 || !valid_dtype(dtype) || !k_cache || !cent || !scent)
+      fanout <= 0 || !valid_dtype(dtype) || similarity < 0 || similarity > 2 || !k_cache || !cent ||
+      !scent)
     return EINVAL;
   const int32_t C = ceil_div(Ts, cluster), S = ceil_div(C, fanout);
+  const int32_t R = similarity == 1 ? 2 : 1;
   const size_t es = elt_size(dtype);
   const int64_t units = (int64_t)n_layers * B * Hkv;
 #pragma omp parallel for schedule(dynamic)
@@ -353,17 +385,26 @@ int mpcref_build_clusters(int32_t B, int32_t layer0, int32_t n_layers, int32_t H
     if (mpcref_owner_layer(layer0 + l, share_period, share_start) != layer0 + l) continue;
     const char* kh = (const char*)k_cache + (size_t)u * Ts * d * es;
     std::vector<double> rmax(d), rmin(d);
-    for (int32_t c = 0; c < C; ++c) {
-      mpcref_cluster_bounds(Ts, d, dtype, kh, c * cluster, cluster, rmax.data(), rmin.data());
-      for (int32_t i = 0; i < d; ++i)
-        cent[((size_t)u * C + c) * d + i] = mpcref_centroid(rmax[i], rmin[i], alpha);
-    }
-    for (int32_t s = 0; s < S; ++s) {
-      mpcref_cluster_bounds(Ts, d, dtype, kh, s * fanout * cluster, fanout * cluster, rmax.data(),
-                            rmin.data());
-      for (int32_t i = 0; i < d; ++i)
-        scent[((size_t)u * S + s) * d + i] = mpcref_centroid(rmax[i], rmin[i], alpha);
-    }
+    // one representative of the tokens [first, first + count) into `out` (R rows of d)
+    auto represent = [&](int32_t first, int32_t count, float* out) {
+      if (similarity == 2) {
+        mpcref_cluster_mean(Ts, d, dtype, kh, first, count, rmax.data());
+        for (int32_t i = 0; i < d; ++i) out[i] = (float)rmax[i];
+        return;
+      }
+      mpcref_cluster_bounds(Ts, d, dtype, kh, first, count, rmax.data(), rmin.data());
+      for (int32_t i = 0; i < d; ++i) {
+        if (similarity == 1) {
+          out[i] = (float)rmax[i];  // key elements: exact in fp32
+          out[d + i] = (float)rmin[i];
+        } else {
+          out[i] = mpcref_centroid(rmax[i], rmin[i], alpha);
+        }
+      }
+    };
+    for (int32_t c = 0; c < C; ++c) represent(c * cluster, cluster, cent + ((size_t)u * C + c) * R * d);
+    for (int32_t s2 = 0; s2 < S; ++s2)
+      represent(s2 * fanout * cluster, fanout * cluster, scent + ((size_t)u * S + s2) * R * d);
   }
   return OK;
 }
@@ -375,11 +416,13 @@ int mpcref_build_clusters(int32_t B, int32_t layer0, int32_t n_layers, int32_t H
 int mpcref_select_clusters(int32_t B, int32_t layer0, int32_t n_layers, int32_t Hq, int32_t Hkv,
                            int32_t d, int32_t dtype, int32_t Ts, int32_t cluster, int32_t fanout,
                            int32_t k_super, int32_t k_clusters, int32_t share_period,
-                           int32_t share_start, const void* q, const float* cent,
+                           int32_t share_start, int32_t similarity, const void* q, const float* cent,
                            const float* scent, int32_t* sel, double* sel_score) {
   if (B <= 0 || layer0 < 0 || n_layers <= 0 || Hq <= 0 || Hkv <= 0 || d <= 0 || Ts <= 0 ||
-      cluster <= 0 || fanout <= 0 || !valid_dtype(dtype) || !q || !cent || !scent || !sel)
+      cluster <= 0 || fanout <= 0 || !valid_dtype(dtype) || similarity < 0 || similarity > 2 || !q ||
+      !cent || !scent || !sel)
     return EINVAL;
+  const int32_t R = similarity == 1 ? 2 : 1;
   const int32_t C = ceil_div(Ts, cluster), S = ceil_div(C, fanout);
   if (Hq % Hkv || k_super <= 0 || k_super > S || k_clusters <= 0) return ESHAPE;
   const int32_t tail = C - (S - 1) * fanout;
@@ -394,7 +437,7 @@ int mpcref_select_clusters(int32_t B, int32_t layer0, int32_t n_layers, int32_t 
     const int32_t b = (int32_t)((u / Hkv) % B), h = (int32_t)(u % Hkv);
     const char* qg = (const char*)q + (((size_t)l * B + b) * Hq + (size_t)h * G) * d * es;
     std::vector<double> s1(S);
-    mpcref_cluster_scores(G, d, dtype, qg, S, scent + (size_t)u * S * d, s1.data());
+    mpcref_cluster_scores(G, d, dtype, similarity, qg, S, scent + (size_t)u * S * R * d, s1.data());
     std::vector<int32_t> top1(k_super);
     mpcref_topk(S, s1.data(), k_super, top1.data());
     std::sort(top1.begin(), top1.end());
@@ -404,7 +447,7 @@ int mpcref_select_clusters(int32_t B, int32_t layer0, int32_t n_layers, int32_t 
     const int32_t n = (int32_t)cand.size();
     std::vector<double> s2(n);
     for (int32_t j = 0; j < n; ++j)
-      mpcref_cluster_scores(G, d, dtype, qg, 1, cent + ((size_t)u * C + cand[j]) * d, &s2[j]);
+      mpcref_cluster_scores(G, d, dtype, similarity, qg, 1, cent + ((size_t)u * C + cand[j]) * R * d, &s2[j]);
     std::vector<int32_t> top2(k_clusters);
     mpcref_topk(n, s2.data(), k_clusters, top2.data());
     std::sort(top2.begin(), top2.end());  // positions in the ascending candidate list

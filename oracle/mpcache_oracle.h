@@ -12,7 +12,8 @@
  *     to double on load.
  *   - layouts are row-major and contiguous:
  *       q_win [n_layers][B][Hq][W][d], k/v [n_layers][B][Hkv][T][d], q [n_layers][B][Hq][d],
- *       kept  [n_layers][B][Hkv][keep], cent [n_layers][B][Hkv][C][d], scent [...][S][d],
+ *       kept  [n_layers][B][Hkv][keep], cent [n_layers][B][Hkv][C][R][d], scent [...][S][R][d]
+ *       (R = 2 rows r^max, r^min for the max-product bound, else 1),
  *       sel   [n_layers][B][Hkv][k_clusters], out [n_layers][B][Hq][d].
  *   - q-head h reads kv-head h / (Hq / Hkv).
  *   - layer indices passed to the sharing rule are absolute: layer0 + local index.
@@ -44,9 +45,14 @@ int mpcref_static_topk(int32_t T, const double* score, int32_t keep, int32_t loc
                        int32_t* kept /*[keep], ascending*/);
 int mpcref_cluster_bounds(int32_t n_tok, int32_t d, int32_t dtype, const void* k /*[n_tok][d]*/,
                           int32_t first, int32_t count, double* rmax, double* rmin);
+int mpcref_cluster_mean(int32_t n_tok, int32_t d, int32_t dtype, const void* k /*[n_tok][d]*/,
+                        int32_t first, int32_t count, double* mean);
 float mpcref_centroid(double rmax, double rmin, float alpha);
-int mpcref_cluster_scores(int32_t G, int32_t d, int32_t dtype, const void* q /*[G][d]*/, int32_t n,
-                          const float* cent /*[n][d]*/, double* score);
+/* similarity: 0 linear alpha r^max + (1 - alpha) r^min, 1 max-product bound (rows r^max, r^min),
+ * 2 average; representatives have (similarity == 1 ? 2 : 1) rows of d floats. */
+int mpcref_cluster_scores(int32_t G, int32_t d, int32_t dtype, int32_t similarity,
+                          const void* q /*[G][d]*/, int32_t n, const float* rep /*[n][R][d]*/,
+                          double* score);
 int mpcref_mp_bound(int32_t d, const double* q, const double* rmax, const double* rmin,
                     double* bound);
 int mpcref_topk(int32_t n, const double* score, int32_t k, int32_t* idx /*[k], rank order*/);
@@ -62,13 +68,13 @@ int mpcref_static_evict(int32_t B, int32_t layer0, int32_t n_layers, int32_t Hq,
                         int32_t* kept, void* k_out, void* v_out, double* token_score);
 int mpcref_build_clusters(int32_t B, int32_t layer0, int32_t n_layers, int32_t Hkv, int32_t d,
                           int32_t dtype, int32_t Ts, int32_t cluster, int32_t fanout, float alpha,
-                          int32_t share_period, int32_t share_start, const void* k_cache,
-                          float* cent, float* scent);
+                          int32_t share_period, int32_t share_start, int32_t similarity,
+                          const void* k_cache, float* cent /*[..][C][R][d]*/, float* scent);
 int mpcref_select_clusters(int32_t B, int32_t layer0, int32_t n_layers, int32_t Hq, int32_t Hkv,
                            int32_t d, int32_t dtype, int32_t Ts, int32_t cluster, int32_t fanout,
                            int32_t k_super, int32_t k_clusters, int32_t share_period,
-                           int32_t share_start, const void* q, const float* cent,
-                           const float* scent, int32_t* sel, double* sel_score);
+                           int32_t share_start, int32_t similarity, const void* q,
+                           const float* cent, const float* scent, int32_t* sel, double* sel_score);
 int mpcref_sparse_decode_attn(int32_t B, int32_t n_layers, int32_t Hq, int32_t Hkv, int32_t d,
                               int32_t dtype, int32_t Ts, int32_t cluster, const void* q,
                               const void* k_cache, const void* v_cache, const int32_t* sel,

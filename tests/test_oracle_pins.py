@@ -251,6 +251,86 @@ def test_unit_cluster_score_is_dot_product():
     np.testing.assert_array_equal(got, exp)
 
 
+def test_cluster_mean_matches_exact_sum():
+    # the average representative: fp64 sum of the exact key values / count (math.fsum is exact)
+    import math
+    k = _rand_bits((37, 8), "bf16", 21)
+    kf = from_bits(k, "bf16")
+    for first, count in [(0, 16), (16, 16), (32, 16)]:
+        got = oracle.cluster_mean(k, "bf16", first, count)
+        rows = kf[first:first + count]
+        exp = np.array([math.fsum(rows[:, i]) / len(rows) for i in range(8)])
+        np.testing.assert_array_equal(got, exp)
+
+
+@pytest.mark.parametrize("similarity", ["linear", "maxprod", "mean"])
+def test_representatives_of_each_similarity(similarity):
+    # linear: alpha r^max + (1-alpha) r^min rounded as in Eq. "sim"; max-product: the two bound rows
+    # (Eq. 2); average: the fp32-rounded mean -- for clusters and for super-clusters (all tokens)
+    L, B, H, Ts, d, s, f = 1, 1, 2, 80, 8, 8, 3     # C = 10, S = 4 with a tail of 1
+    k = _rand_bits((L, B, H, Ts, d), "fp16", 22)
+    kf = from_bits(k, "fp16")
+    cent, scent = oracle.build_clusters(k, "fp16", cluster=s, fanout=f, alpha=0.6, similarity=similarity)
+    for h in range(H):
+        for rep, blocks in ((cent[0, 0, h], [(c * s, s) for c in range(10)]),
+                            (scent[0, 0, h], [(u * f * s, f * s) for u in range(4)])):
+            for j, (first, count) in enumerate(blocks):
+                rows = kf[0, 0, h, first:first + count]
+                if similarity == "maxprod":
+                    np.testing.assert_array_equal(rep[j, 0], rows.max(0).astype(np.float32))
+                    np.testing.assert_array_equal(rep[j, 1], rows.min(0).astype(np.float32))
+                elif similarity == "mean":
+                    np.testing.assert_array_equal(rep[j], (rows.sum(0) / len(rows)).astype(np.float32))
+                else:
+                    exp = [oracle.centroid(a, b, 0.6) for a, b in zip(rows.max(0), rows.min(0))]
+                    np.testing.assert_array_equal(rep[j], np.float32(exp))
+
+
+def test_maxprod_score_bounds_true_max_and_every_linear_score():
+    # Eq. 2: sum_i max(q_i r^max_i, q_i r^min_i) >= max_k q.k, and >= the linear score for every
+    # alpha in [0, 1]; summed over the group's heads
+    r = rng(23)
+    for trial in range(40):
+        G, d, s = 2, 16, 8
+        k = to_bits(r.standard_normal((s, d)) * 3, "bf16")
+        kf = from_bits(k, "bf16")
+        q = to_bits(r.standard_normal((G, d)), "bf16")
+        qf = from_bits(q, "bf16")
+        rep = np.stack([kf.max(0), kf.min(0)]).astype(np.float32)
+        mp = oracle.cluster_scores(q, rep[None], "bf16", "maxprod")[0]
+        brute = sum((kf @ qf[g]).max() for g in range(G))
+        assert mp >= brute - 1e-12
+        for a in (0.0, 0.3, 0.6, 1.0):
+            lin = sum(np.sum(np.maximum(qf[g] * rep[0], qf[g] * rep[1])) for g in range(G))
+            assert abs(mp - lin) <= 1e-12 * max(1.0, abs(lin))  # the bound itself, by numpy
+            cen = qf.sum(0) @ (a * rep[0].astype(np.float64) + (1 - a) * rep[1].astype(np.float64))
+            assert cen <= mp + 1e-9
+
+
+def test_single_token_clusters_score_the_dot_product_in_every_mode():
+    # s = 1: r^max = r^min = mean = k, so every representative scores q.k exactly (alpha = 1 for
+    # the linear form, whose fp32 products are exact then)
+    r = rng(24)
+    k = to_bits(r.standard_normal((1, 1, 1, 20, 8)), "bf16")
+    q = to_bits(r.standard_normal((2, 8)), "bf16")
+    exp = from_bits(k, "bf16")[0, 0, 0] @ from_bits(q, "bf16").sum(0)
+    for sim in ("linear", "maxprod", "mean"):
+        cent, _ = oracle.build_clusters(k, "bf16", cluster=1, fanout=4, alpha=1.0, similarity=sim)
+        got = oracle.cluster_scores(q, cent[0, 0, 0], "bf16", sim)
+        np.testing.assert_array_equal(got, exp)
+
+
+def test_maxprod_equals_alpha_one_linear_for_nonnegative_queries():
+    # with q >= 0 every max picks q_i r^max_i: the bound is the alpha = 1 linear score, term by term
+    r = rng(25)
+    k = to_bits(r.standard_normal((1, 1, 1, 64, 16)), "bf16")
+    q = to_bits(np.abs(r.standard_normal((3, 16))), "bf16")
+    lin, _ = oracle.build_clusters(k, "bf16", cluster=8, fanout=2, alpha=1.0)
+    mp, _ = oracle.build_clusters(k, "bf16", cluster=8, fanout=2, similarity="maxprod")
+    np.testing.assert_array_equal(oracle.cluster_scores(q, lin[0, 0, 0], "bf16"),
+                                  oracle.cluster_scores(q, mp[0, 0, 0], "bf16", "maxprod"))
+
+
 # ------------------------------------------------------------------------ selection (A5-A7)
 def test_topk_matches_lexsort():
     r = rng(17)
@@ -258,19 +338,47 @@ def test_topk_matches_lexsort():
     np.testing.assert_array_equal(oracle.topk(s, 12), _lexsort_topk(s, 12))
 
 
-def _select_case(seed, L=6, B=1, Hq=4, Hkv=2, Ts=200, d=16, s=8, f=4, dtype="bf16"):
+def _select_case(seed, L=6, B=1, Hq=4, Hkv=2, Ts=200, d=16, s=8, f=4, dtype="bf16", similarity="linear"):
     r = rng(seed)
     k = to_bits(r.standard_normal((L, B, Hkv, Ts, d)), dtype)
     q = to_bits(r.standard_normal((L, B, Hq, d)), dtype)
-    cent, scent = oracle.build_clusters(k, dtype, cluster=s, fanout=f)
+    cent, scent = oracle.build_clusters(k, dtype, cluster=s, fanout=f, similarity=similarity)
     return k, q, cent, scent
 
 
-def test_full_budget_selects_every_cluster():
-    k, q, cent, scent = _select_case(18, Ts=200, s=8, f=4)  # C = 25, S = 7 (tail 1)
+@pytest.mark.parametrize("similarity", ["linear", "maxprod", "mean"])
+def test_full_budget_selects_every_cluster(similarity):
+    k, q, cent, scent = _select_case(18, Ts=200, s=8, f=4, similarity=similarity)  # C = 25, S = 7 (tail 1)
     sel, _ = oracle.select_clusters(q, cent, scent, "bf16", Ts=200, cluster=8, fanout=4, k_super=7,
-                                    k_clusters=25)
+                                    k_clusters=25, similarity=similarity)
     assert np.all(sel == np.arange(25))
+
+
+@pytest.mark.parametrize("similarity", ["maxprod", "mean"])
+def test_hierarchical_selection_of_other_similarities_matches_independent_ranking(similarity):
+    # the two levels rank by the mode's score recomputed here with numpy from the key values
+    Ts, s, f, ks, kc, G, C = 200, 8, 4, 3, 5, 2, 25
+    k, q, cent, scent = _select_case(26, Ts=Ts, s=s, f=f, similarity=similarity)
+    sel, score = oracle.select_clusters(q, cent, scent, "bf16", Ts=Ts, cluster=s, fanout=f, k_super=ks,
+                                        k_clusters=kc, similarity=similarity)
+    qf, kf = from_bits(q, "bf16"), from_bits(k, "bf16")
+
+    def sc(qg, rows):  # rows [n_tok][d] of one representative
+        if similarity == "mean":
+            return qg.sum(0) @ (rows.sum(0) / len(rows)).astype(np.float32).astype(np.float64)
+        return sum(np.sum(np.maximum(qh * rows.max(0), qh * rows.min(0))) for qh in qg)
+
+    for l in range(q.shape[0]):
+        for h in range(2):
+            qg = qf[l, 0, h * G:(h + 1) * G]
+            kh = kf[l, 0, h]
+            s1 = np.array([sc(qg, kh[u * f * s:(u + 1) * f * s]) for u in range(7)])
+            sup = np.sort(_lexsort_topk(s1, ks))
+            cand = np.array([c for x in sup for c in range(x * f, min(C, (x + 1) * f))])
+            s2 = np.array([sc(qg, kh[c * s:(c + 1) * s]) for c in cand])
+            exp = np.sort(cand[_lexsort_topk(s2, kc)])
+            np.testing.assert_array_equal(sel[l, 0, h], exp)
+            np.testing.assert_allclose(score[l, 0, h], s2[np.searchsorted(cand, exp)], rtol=1e-12)
 
 
 def test_hierarchical_selection_matches_independent_ranking():
