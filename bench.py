@@ -36,6 +36,9 @@ def parse():
     p.add_argument("--decode-steps", type=int, default=None, help="decode steps per pass (default: workload's)")
     p.add_argument("--decode-mode", choices=("split", "fused"), default="split",
                    help="timed decode step: selection and attention as two kernels (default) or one launch")
+    p.add_argument("--similarity", choices=("linear", "maxprod", "mean"), default="linear",
+                   help="cluster similarity: the paper's linear form (default), the max-product bound (Eq. 2) "
+                        "or the cluster average")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--copy-calibration", action="store_true",
                    help="accepted for recorded profiling commands; the 1 GiB reference copy always runs")
@@ -68,12 +71,13 @@ def measured_traffic(kernel, workload, digest):
     return rec.get("bytes_per_launch")
 
 
-def decode_bytes(w, owners, sel, C, S):
-    """Algorithmic bytes of one decode step: reads of representatives, queries, gathered K/V rows
-    and selections; writes of selections and outputs. Every byte is counted once."""
+def decode_bytes(w, owners, sel, C, S, rep_rows=1):
+    """Algorithmic bytes of one decode step: reads of representatives (rep_rows rows of d floats
+    each), queries, gathered K/V rows and selections; writes of selections and outputs. Every
+    byte is counted once."""
     G, d, e = w.group, w.head_dim, w.elt
     n_own = len(owners)
-    sel_read = n_own * w.batch * w.n_kv_heads * ((S + w.k_super * w.fanout) * d * 4 + G * d * e)
+    sel_read = n_own * w.batch * w.n_kv_heads * ((S + w.k_super * w.fanout) * rep_rows * d * 4 + G * d * e)
     sel_write = w.n_layers * w.batch * w.n_kv_heads * w.k_clusters * 8
     # exact gathered token count (a partial last cluster holds fewer rows)
     last = w.keep - (C - 1) * w.cluster
@@ -90,7 +94,7 @@ def prefill_flops(w, n_owner):
     return n_owner * w.batch * w.n_q_heads * rows * 2 * w.head_dim
 
 
-def cpu_baseline(w, n_steps_sample, min_seconds=10.0, max_seconds=30.0):
+def cpu_baseline(w, n_steps_sample, similarity="linear", min_seconds=10.0, max_seconds=30.0):
     """The oracle's decode step (selection + sparse attention) on a sample of the workload: one
     sharing block of layers (2..2+P-1), every sequence and head, `n_steps_sample` fresh queries,
     repeated until at least `min_seconds` of CPU work (stopping at the first pass past
@@ -108,7 +112,8 @@ def cpu_baseline(w, n_steps_sample, min_seconds=10.0, max_seconds=30.0):
     import numpy as np
     k, v = np.stack(ks), np.stack(vs)
     cent, scent = oracle.build_clusters(k, w.dtype, cluster=w.cluster, fanout=w.fanout, layer0=layer0,
-                                        share_period=w.share_period, share_start=w.share_start)
+                                        share_period=w.share_period, share_start=w.share_start,
+                                        similarity=similarity)
     sp = synth.spec(w, n_layers=layer0 + n_l)
     qs = [synth.dq_host(sp, e, w.dtype)[layer0:] for e in range(n_steps_sample)]
     sm = 1.0 / math.sqrt(w.head_dim)
@@ -118,7 +123,8 @@ def cpu_baseline(w, n_steps_sample, min_seconds=10.0, max_seconds=30.0):
         for q in qs:
             sel, _ = oracle.select_clusters(q, cent, scent, w.dtype, Ts=w.keep, cluster=w.cluster, fanout=w.fanout,
                                             k_super=w.k_super, k_clusters=w.k_clusters, layer0=layer0,
-                                            share_period=w.share_period, share_start=w.share_start)
+                                            share_period=w.share_period, share_start=w.share_start,
+                                            similarity=similarity)
             oracle.sparse_decode_attn(q, k, v, sel, w.dtype, cluster=w.cluster, sm_scale=sm)
             steps += 1
             if time.perf_counter() - t0 > max_seconds:
@@ -176,7 +182,7 @@ def main():
                          head_dim=w.head_dim, dtype=synth.torch_dtype(w.dtype), T=w.T, window=w.window,
                          keep=w.keep, local_keep=w.local_keep, cluster=w.cluster, fanout=w.fanout,
                          k_super=w.k_super, k_clusters=w.k_clusters, share_period=w.share_period,
-                         share_start=w.share_start)
+                         share_start=w.share_start, similarity=args.similarity)
     torch.cuda.synchronize()
 
     fused = args.decode_mode == "fused"
@@ -243,7 +249,7 @@ def main():
     alt = {"mode": "split" if fused else "fused", "us": round(step_time(other), 3)}
 
     owners = [l for l in range(w.n_layers) if M.owner_layer(l, w.share_period, w.share_start) == l]
-    sel_b, att_b = decode_bytes(w, owners, path.sel.cpu().numpy(), path.C, path.S)
+    sel_b, att_b = decode_bytes(w, owners, path.sel.cpu().numpy(), path.C, path.S, M.rep_rows(args.similarity))
     step_b = sel_b + att_b
     att_gbs = att_b / (att_us * 1e-6) / 1e9
     dec_gbs = step_b / (dec_us * 1e-6) / 1e9
@@ -280,7 +286,7 @@ def main():
                    "q_heads": w.n_q_heads, "kv_heads": w.n_kv_heads, "head_dim": w.head_dim, "prompt_tokens": w.T,
                    "window_rows": w.window, "kept_tokens": w.keep, "cluster": w.cluster, "fanout": w.fanout,
                    "k_super": w.k_super, "k_clusters": w.k_clusters, "share_period": w.share_period,
-                   "decode_steps_per_pass": E},
+                   "similarity": args.similarity, "decode_steps_per_pass": E},
         "decode_step": {"mode": args.decode_mode, "us": round(dec_us, 3), "algorithmic_bytes": step_b,
                         "achieved_GBps": round(dec_gbs, 1), "frac_of_hbm_peak": round(dec_gbs / HBM_PEAK_GBS, 4)},
         "kernels": {"select_us": round(sel_us, 3), "attention_us": round(att_us, 3),
@@ -300,7 +306,7 @@ def main():
                     "note": "static eviction (two score passes, top-k, gather) + cluster build, all layers"},
     }
     if not args.no_cpu_baseline:
-        rec["cpu_baseline"] = cpu_baseline(w, min(E, 64))
+        rec["cpu_baseline"] = cpu_baseline(w, min(E, 64), args.similarity)
     print(json.dumps(rec), flush=True)
 
 

@@ -58,6 +58,12 @@ typedef struct {
   int32_t dtype;      /* mpc_dtype of q / k / v / out                     */
 } mpc_dims;
 
+/* Cluster similarity (Sec. 3.3). LINEAR: the reordered linear form (Eq. "sim"), one
+ * representative row alpha * r^max + (1 - alpha) * r^min. MAXPROD: the max-product upper bound
+ * (Eq. 2), two rows r^max, r^min. MEAN: the average of the cluster's keys (the baseline of the
+ * paper's average-based comparison), one row. */
+typedef enum { MPC_SIM_LINEAR = 0, MPC_SIM_MAXPROD = 1, MPC_SIM_MEAN = 2 } mpc_similarity;
+
 typedef struct {
   int32_t cluster_size; /* s: tokens per fine cluster                                        */
   int32_t fanout;       /* f: fine clusters per super-cluster                                */
@@ -66,6 +72,7 @@ typedef struct {
   float alpha;          /* weight of r^max in the representative (the paper uses 0.6)        */
   int32_t share_period; /* layers per shared selection (1 = no sharing)                     */
   int32_t share_start;  /* first layer that may share (2 in the paper)                       */
+  int32_t similarity;   /* mpc_similarity (MPC_SIM_LINEAR in the paper's method)              */
 } mpc_select_cfg;
 
 typedef struct {
@@ -109,15 +116,19 @@ mpc_status mpc_static_evict(const mpc_dims* dims, int32_t T, const mpc_evict_cfg
 
 /* Cluster representatives (Sec. 3.3: r^max / r^min under Eq. 1, reordered form Eq. "sim";
  * hierarchy of Sec. 3.3 / App. F). Fine cluster c covers kept tokens [c*s, min((c+1)*s, Ts));
- * super-cluster u covers fine clusters [u*f, min((u+1)*f, C)). Each representative is
- * fp32( fp32(alpha * r^max) + fp32((1-alpha)_fp32 * r^min) ) per channel. Owner layers only.
- *   k_cache [L][B][Hkv][Ts][d];  cent [L][B][Hkv][C][d] float out;  scent [L][B][Hkv][S][d] float out */
+ * super-cluster u covers fine clusters [u*f, min((u+1)*f, C)), i.e. their tokens. Per channel:
+ *   LINEAR   one row fp32( fp32(alpha * r^max) + fp32((1-alpha)_fp32 * r^min) );
+ *   MAXPROD  two rows, r^max then r^min (exact key values);
+ *   MEAN     one row, fp32( fp64 sum of the tokens' values / token count ).
+ * Owner layers only. R = 2 for MAXPROD, else 1.
+ *   k_cache [L][B][Hkv][Ts][d];  cent [L][B][Hkv][C][R][d] float out;  scent [L][B][Hkv][S][R][d] */
 mpc_status mpc_build_clusters(const mpc_dims* dims, int32_t Ts, const mpc_select_cfg* cfg,
                               const void* k_cache, float* cent, float* scent, void* stream);
 
 /* Query-aware dynamic selection of one decode step (Sec. 3.3; Alg. 3 step 2).
- * Score of a representative c for kv head h: sum over the group's q-heads g and channels i of
- * q_{g,i} * c_i, accumulated in fp64. Level 1 keeps the k_super best super-clusters, level 2 the
+ * Score of a representative for kv head h, summed over the group's q-heads g and channels i and
+ * accumulated in fp64: q_{g,i} * c_i (LINEAR, MEAN) or max(q_{g,i} r^max_i, q_{g,i} r^min_i)
+ * (MAXPROD, Eq. 2). Level 1 keeps the k_super best super-clusters, level 2 the
  * k_clusters best fine clusters among their members (ties: lower index first); the selection is
  * written in ascending cluster order. Non-owner layers receive their owner's selection; a layer
  * whose owner precedes layer0 is left untouched (the caller copies it).
@@ -153,8 +164,9 @@ mpc_status mpc_sparse_decode_attn(const mpc_dims* dims, int32_t Ts, int32_t clus
  *   sel_score optional; out [L][B][Hq][d]; lse optional.
  *   ws: mpc_workspace_bytes(MPC_OP_DECODE_STEP, dims, Ts, cfg) bytes, zero-filled before its first
  *   use; every completed call leaves it ready for the next (calls sharing it must not overlap).
- * Blocks whose attention is split over several workgroups per unit run the two kernels one after
- * the other instead (same results). */
+ * Blocks whose attention is split over several workgroups per unit, or whose selection and
+ * attention together need more LDS than one workgroup has, run the two kernels one after the other
+ * instead (same results). */
 mpc_status mpc_decode_step(const mpc_dims* dims, int32_t Ts, const mpc_select_cfg* cfg,
                            const void* q, const float* cent, const float* scent,
                            const void* k_cache, const void* v_cache, float sm_scale, int32_t* sel,

@@ -7,6 +7,6 @@ buffers preallocated.
 """
 from ._lib import (  # noqa: F401
     MPC_OP_DECODE_ATTN, MPC_OP_DECODE_STEP, MPC_OP_SELECT, MPC_OP_STATIC_EVICT, MpcDims, MpcError,
-    MpcEvictCfg, MpcSelectCfg, dims_of, lib, mpc_build_clusters, mpc_decode_step, mpc_select_clusters,
-    mpc_sparse_decode_attn, mpc_static_evict, owner_layer, select_cfg, workspace, workspace_bytes)
+    MpcEvictCfg, MpcSelectCfg, SIMILARITY, dims_of, lib, mpc_build_clusters, mpc_decode_step, mpc_select_clusters,
+    mpc_sparse_decode_attn, mpc_static_evict, owner_layer, rep_rows, select_cfg, workspace, workspace_bytes)
 from .pipeline import MPCachePath  # noqa: F401

@@ -26,7 +26,7 @@ class MpcSelectCfg(ctypes.Structure):
     _fields_ = [("cluster_size", ctypes.c_int32), ("fanout", ctypes.c_int32),
                 ("k_super", ctypes.c_int32), ("k_clusters", ctypes.c_int32),
                 ("alpha", ctypes.c_float), ("share_period", ctypes.c_int32),
-                ("share_start", ctypes.c_int32)]
+                ("share_start", ctypes.c_int32), ("similarity", ctypes.c_int32)]
 
 
 class MpcEvictCfg(ctypes.Structure):
@@ -135,15 +135,34 @@ def mpc_static_evict(q_win, k, v, kept_idx, k_out, v_out, *, keep, local_keep, s
         _ptr(v_out), _ptr(token_score), _ptr(row_lse), _ptr(ws), ws.numel(), _stream(stream)))
 
 
-def select_cfg(cluster, fanout, k_super, k_clusters, alpha=0.6, share_period=1, share_start=2):
+SIMILARITY = {"linear": 0, "maxprod": 1, "mean": 2}
+
+
+def rep_rows(similarity):
+    """Rows of d floats per cluster representative (r^max and r^min for the max-product bound)."""
+    return 2 if SIMILARITY[similarity] == 1 else 1
+
+
+def select_cfg(cluster, fanout, k_super, k_clusters, alpha=0.6, share_period=1, share_start=2,
+               similarity="linear"):
     return MpcSelectCfg(cluster_size=cluster, fanout=fanout, k_super=k_super, k_clusters=k_clusters,
-                        alpha=alpha, share_period=share_period, share_start=share_start)
+                        alpha=alpha, share_period=share_period, share_start=share_start,
+                        similarity=SIMILARITY[similarity])
 
 
 def mpc_build_clusters(k_cache, cent, scent, cfg, *, layer0=0, stream=None):
-    """k_cache [L][B][Hkv][Ts][d] -> cent [L][B][Hkv][C][d], scent [L][B][Hkv][S][d] (float32)."""
+    """k_cache [L][B][Hkv][Ts][d] -> cent [L][B][Hkv][C][R][d], scent [L][B][Hkv][S][R][d] (float32;
+    R = 2 rows r^max, r^min for the max-product bound, else 1 and the R axis may be omitted)."""
     _contig(k_cache, cent, scent)
     dims = dims_of(k_cache, k_cache, layer0)
+    L, B, Hkv, Ts, d = k_cache.shape
+    C = -(-Ts // cfg.cluster_size)
+    S = -(-C // cfg.fanout)
+    R = 2 if cfg.similarity == SIMILARITY["maxprod"] else 1
+    if cent.numel() != L * B * Hkv * C * R * d or scent.numel() != L * B * Hkv * S * R * d:
+        raise ValueError(f"cent / scent must hold [L][B][Hkv][C or S][{R}][d] floats")
+    if cent.dtype != torch.float32 or scent.dtype != torch.float32:
+        raise TypeError("cent / scent must be float32")
     _check("mpc_build_clusters", lib().mpc_build_clusters(
         ctypes.byref(dims), k_cache.shape[3], ctypes.byref(cfg), _ptr(k_cache), _ptr(cent), _ptr(scent),
         _stream(stream)))
@@ -153,6 +172,7 @@ def mpc_select_clusters(q, cent, scent, sel, cfg, *, Ts, sel_score=None, layer0=
     """q [L][B][Hq][d] -> sel [L][B][Hkv][k_clusters] (int32, ascending)."""
     _contig(q, cent, scent, sel, sel_score)
     dims = dims_of(q, cent, layer0)
+    dims.head_dim = q.shape[-1]
     dims.dtype = DTYPE_CODE[q.dtype]
     _check("mpc_select_clusters", lib().mpc_select_clusters(
         ctypes.byref(dims), Ts, ctypes.byref(cfg), _ptr(q), _ptr(cent), _ptr(scent), _ptr(sel), _ptr(sel_score),

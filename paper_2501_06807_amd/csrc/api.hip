@@ -217,6 +217,8 @@ mpc_status mpc_build_clusters(const mpc_dims* dims, int32_t Ts, const mpc_select
   if (Ts <= 0 || cfg->cluster_size <= 0 || cfg->fanout <= 0)
     return fail(MPC_EINVAL, "Ts, cluster_size and fanout must be positive");
   if (!(cfg->alpha >= 0.f && cfg->alpha <= 1.f)) return fail(MPC_EINVAL, "alpha must be in [0, 1]");
+  if (cfg->similarity < MPC_SIM_LINEAR || cfg->similarity > MPC_SIM_MEAN)
+    return fail(MPC_EINVAL, "unknown similarity %d", cfg->similarity);
   if (!k_cache || !cent || !scent) return fail(MPC_EINVAL, "a required tensor pointer is NULL");
   if (!aligned16(k_cache) || !aligned16(cent) || !aligned16(scent))
     return fail(MPC_EINVAL, "tensor bases must be 16-byte aligned");
@@ -237,6 +239,7 @@ mpc_status mpc_build_clusters(const mpc_dims* dims, int32_t Ts, const mpc_select
   a.start = cfg->share_start;
   a.alpha = cfg->alpha;
   a.beta = (float)(1.0 - (double)cfg->alpha);
+  a.similarity = cfg->similarity;
   if (a.n_layers > mpc::kMaxLayers) return fail(MPC_EUNSUPPORTED, "at most %d layers per call", mpc::kMaxLayers);
   if ((int64_t)a.n_layers * a.B * a.Hkv * a.S >= ((int64_t)1 << 31))
     return fail(MPC_EUNSUPPORTED, "grid too large");
@@ -261,6 +264,8 @@ mpc_status prepare_select(const mpc_dims* dims, int32_t Ts, const mpc_select_cfg
   if (Ts <= 0 || cfg->cluster_size <= 0 || cfg->fanout <= 0 || cfg->k_super <= 0 || cfg->k_clusters <= 0)
     return fail(MPC_EINVAL, "Ts, cluster_size, fanout and budgets must be positive");
   if (!q || !cent || !scent || !sel) return fail(MPC_EINVAL, "a required tensor pointer is NULL");
+  if (cfg->similarity < MPC_SIM_LINEAR || cfg->similarity > MPC_SIM_MEAN)
+    return fail(MPC_EINVAL, "unknown similarity %d", cfg->similarity);
   const int C = ceil_div(Ts, cfg->cluster_size), S = ceil_div(C, cfg->fanout);
   if (cfg->k_super > S) return fail(MPC_ESHAPE, "k_super %d > super-clusters %d", cfg->k_super, S);
   const int tail = C - (S - 1) * cfg->fanout;
@@ -269,6 +274,9 @@ mpc_status prepare_select(const mpc_dims* dims, int32_t Ts, const mpc_select_cfg
     return fail(MPC_ESHAPE, "k_clusters %d exceeds the smallest candidate set %d", cfg->k_clusters, min_cand);
   if (S > mpc::kSelMaxSuper || (int64_t)cfg->k_super * cfg->fanout > mpc::kSelMaxCand)
     return fail(MPC_EUNSUPPORTED, "selection sizes beyond the kernel limits");
+  const int qrows = cfg->similarity == MPC_SIM_MAXPROD ? dims->n_q_heads / dims->n_kv_heads : 1;
+  if (mpc::select_smem_bytes(dims->head_dim, S, cfg->k_super * cfg->fanout, qrows) > mpc::kMaxLds)
+    return fail(MPC_EUNSUPPORTED, "selection sizes need more LDS than a workgroup has");
   if (dims->n_layers > mpc::kMaxLayers) return fail(MPC_EUNSUPPORTED, "at most %d layers per call", mpc::kMaxLayers);
   mpc::SelectArgs a{};
   a.q = q;
@@ -289,6 +297,7 @@ mpc_status prepare_select(const mpc_dims* dims, int32_t Ts, const mpc_select_cfg
   a.k_clusters = cfg->k_clusters;
   a.period = cfg->share_period;
   a.start = cfg->share_start;
+  a.similarity = cfg->similarity;
   a.own = mpc::owner_table(a.layer0, a.n_layers, a.period, a.start);
   *out = a;
   return MPC_OK;
@@ -401,7 +410,8 @@ mpc_status mpc_decode_step(const mpc_dims* dims, int32_t Ts, const mpc_select_cf
   const int G = dims->n_q_heads / dims->n_kv_heads;
   hipStream_t st = (hipStream_t)stream;
   clear_stale_error();
-  if (plan.splits > 1) {  // small block: the two kernels in sequence
+  const mpc::FusedPlan fp = mpc::fused_plan(sa, dims->head_dim);
+  if (plan.splits > 1 || !mpc::fused_fits(fp, dims->head_dim, G)) {  // the two kernels in sequence
     da.part = (float*)((char*)ws + lay.part);
     da.cnt = (int*)((char*)ws + lay.part + decode_ws(dims).cnt);
     if (sa.own.n > 0 &&
@@ -418,7 +428,6 @@ mpc_status mpc_decode_step(const mpc_dims* dims, int32_t Ts, const mpc_select_cf
   f.sync = (mpc::FusedSync*)ws;
   f.state = (int*)((char*)ws + lay.state);
   f.cons = (int*)((char*)ws + lay.cons);
-  const mpc::FusedPlan fp = mpc::fused_plan(sa, dims->head_dim);
   if ((s = launched(mpc::launch_decode_step(f, fp, dims->dtype, dims->head_dim, G, st), "decode step")) != MPC_OK)
     return s;
   return ok();

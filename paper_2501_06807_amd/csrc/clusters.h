@@ -6,9 +6,10 @@ namespace mpc {
 
 struct BuildArgs {
   const void* k;   // [L][B][Hkv][Ts][d]
-  float* cent;     // [L][B][Hkv][C][d]
-  float* scent;    // [L][B][Hkv][S][d]
+  float* cent;     // [L][B][Hkv][C][R][d]  (R = 2 for the max-product bound, else 1)
+  float* scent;    // [L][B][Hkv][S][R][d]
   int B, layer0, n_layers, Hkv, Ts, s, f, C, S, period, start;
+  int similarity;     // mpc_similarity
   float alpha, beta;  // beta = fp32(1 - alpha)
   OwnerTable own;
 };

@@ -1,23 +1,28 @@
-// Cluster representatives: per-channel max / min of each fine cluster and super-cluster of the
-// kept cache, folded into alpha * r^max + (1 - alpha) * r^min, gfx950.
+// Cluster representatives of each fine cluster and super-cluster of the kept cache, gfx950:
+// per-channel max / min folded into alpha * r^max + (1 - alpha) * r^min (linear form), or the
+// two bound rows (max-product bound), or the average (fp64 sums, one rounding to fp32).
 //
 // One workgroup per (owner layer, sequence, kv head, super-cluster). Each wave streams the rows of
 // one fine cluster at a time with coalesced 16-byte loads (LPR lanes per row), reduces max / min
 // over its row groups with cross-lane shuffles, writes the fine representative and folds the
 // bounds into its super-cluster bounds; the waves' super bounds meet in LDS. Max / min are exact,
-// and the representative is two fp32 products and one fp32 sum with no contraction.
+// the linear representative is two fp32 products and one fp32 sum with no contraction, and the
+// average's fp64 sums of 16-bit keys are exact, so their order does not matter.
 #include "clusters.h"
 
 namespace mpc {
 namespace {
 
-template <class DT, int D, int NW>
+template <class DT, int D, int NW, int SIM>
 __global__ __launch_bounds__(NW* kWave) void k_build(BuildArgs a) {
 #pragma clang fp contract(off)
   constexpr int EPL = DT::kVec;
   constexpr int LPR = D / EPL;
   constexpr int RPW = kWave / LPR;
+  constexpr int R = SIM == MPC_SIM_MAXPROD ? 2 : 1;  // representative rows
+  constexpr bool MEAN = SIM == MPC_SIM_MEAN;
   __shared__ float s_max[NW][D], s_min[NW][D];
+  __shared__ double s_sum[MEAN ? NW : 1][MEAN ? D : 1];
 
   const int sup = blockIdx.x % a.S;
   const int ou = blockIdx.x / a.S;  // (owner index * B + b) * Hkv + h
@@ -28,18 +33,22 @@ __global__ __launch_bounds__(NW* kWave) void k_build(BuildArgs a) {
   const char* kh = (const char*)a.k + (size_t)unit * a.Ts * D * DT::kElt;
 
   float smax[EPL], smin[EPL];
+  double ssum[EPL];
 #pragma unroll
   for (int e = 0; e < EPL; ++e) {
     smax[e] = -INFINITY;
     smin[e] = INFINITY;
+    ssum[e] = 0.0;
   }
   const int c_end = min(a.C, (sup + 1) * a.f);
   for (int c = sup * a.f + w; c < c_end; c += NW) {
     float cmax[EPL], cmin[EPL];
+    double csum[EPL];
 #pragma unroll
     for (int e = 0; e < EPL; ++e) {
       cmax[e] = -INFINITY;
       cmin[e] = INFINITY;
+      csum[e] = 0.0;
     }
     const int r_end = min(a.Ts, (c + 1) * a.s);
     for (int r = c * a.s + rg; r < r_end; r += RPW) {
@@ -47,58 +56,106 @@ __global__ __launch_bounds__(NW* kWave) void k_build(BuildArgs a) {
       unpack<DT>(ldg16(kh + ((size_t)r * D + li * EPL) * DT::kElt), x);
 #pragma unroll
       for (int e = 0; e < EPL; ++e) {
-        cmax[e] = fmaxf(cmax[e], x[e]);
-        cmin[e] = fminf(cmin[e], x[e]);
+        if constexpr (MEAN) {
+          csum[e] += (double)x[e];
+        } else {
+          cmax[e] = fmaxf(cmax[e], x[e]);
+          cmin[e] = fminf(cmin[e], x[e]);
+        }
       }
     }
 #pragma unroll
     for (int o = LPR; o < kWave; o <<= 1) {
 #pragma unroll
       for (int e = 0; e < EPL; ++e) {
-        cmax[e] = fmaxf(cmax[e], __shfl_xor(cmax[e], o));
-        cmin[e] = fminf(cmin[e], __shfl_xor(cmin[e], o));
+        if constexpr (MEAN) {
+          csum[e] += __shfl_xor(csum[e], o);
+        } else {
+          cmax[e] = fmaxf(cmax[e], __shfl_xor(cmax[e], o));
+          cmin[e] = fminf(cmin[e], __shfl_xor(cmin[e], o));
+        }
       }
     }
     if (rg == 0) {
-      float* out = a.cent + ((size_t)unit * a.C + c) * D + li * EPL;
+      float* out = a.cent + ((size_t)unit * a.C + c) * R * D + li * EPL;
 #pragma unroll
-      for (int e = 0; e < EPL; ++e) out[e] = a.alpha * cmax[e] + a.beta * cmin[e];
+      for (int e = 0; e < EPL; ++e) {
+        if constexpr (SIM == MPC_SIM_LINEAR) {
+          out[e] = a.alpha * cmax[e] + a.beta * cmin[e];
+        } else if constexpr (SIM == MPC_SIM_MAXPROD) {
+          out[e] = cmax[e];
+          out[D + e] = cmin[e];
+        } else {
+          out[e] = (float)(csum[e] / (double)(r_end - c * a.s));
+        }
+      }
     }
 #pragma unroll
     for (int e = 0; e < EPL; ++e) {
-      smax[e] = fmaxf(smax[e], cmax[e]);
-      smin[e] = fminf(smin[e], cmin[e]);
+      if constexpr (MEAN) {
+        ssum[e] += csum[e];
+      } else {
+        smax[e] = fmaxf(smax[e], cmax[e]);
+        smin[e] = fminf(smin[e], cmin[e]);
+      }
     }
   }
   if (rg == 0) {
 #pragma unroll
     for (int e = 0; e < EPL; ++e) {
-      s_max[w][li * EPL + e] = smax[e];
-      s_min[w][li * EPL + e] = smin[e];
+      if constexpr (MEAN) {
+        s_sum[w][li * EPL + e] = ssum[e];
+      } else {
+        s_max[w][li * EPL + e] = smax[e];
+        s_min[w][li * EPL + e] = smin[e];
+      }
     }
   }
   __syncthreads();
+  const int n_tok = min(a.Ts, c_end * a.s) - sup * a.f * a.s;  // tokens of the super-cluster
+  float* sout = a.scent + ((size_t)unit * a.S + sup) * R * D;
   for (int i = tid; i < D; i += NW * kWave) {
-    float mx = -INFINITY, mn = INFINITY;
+    if constexpr (MEAN) {
+      double sum = 0.0;
 #pragma unroll
-    for (int j = 0; j < NW; ++j) {
-      mx = fmaxf(mx, s_max[j][i]);
-      mn = fminf(mn, s_min[j][i]);
+      for (int j = 0; j < NW; ++j) sum += s_sum[j][i];
+      sout[i] = (float)(sum / (double)n_tok);
+    } else {
+      float mx = -INFINITY, mn = INFINITY;
+#pragma unroll
+      for (int j = 0; j < NW; ++j) {
+        mx = fmaxf(mx, s_max[j][i]);
+        mn = fminf(mn, s_min[j][i]);
+      }
+      if constexpr (SIM == MPC_SIM_LINEAR) {
+        sout[i] = a.alpha * mx + a.beta * mn;
+      } else {
+        sout[i] = mx;
+        sout[D + i] = mn;
+      }
     }
-    a.scent[((size_t)unit * a.S + sup) * D + i] = a.alpha * mx + a.beta * mn;
   }
+}
+
+template <class DT, int D>
+void launch_sim(const BuildArgs& a, int blocks, hipStream_t st) {
+  constexpr int NW = 4;
+  if (a.similarity == MPC_SIM_MAXPROD)
+    hipLaunchKernelGGL((k_build<DT, D, NW, MPC_SIM_MAXPROD>), dim3(blocks), dim3(NW * kWave), 0, st, a);
+  else if (a.similarity == MPC_SIM_MEAN)
+    hipLaunchKernelGGL((k_build<DT, D, NW, MPC_SIM_MEAN>), dim3(blocks), dim3(NW * kWave), 0, st, a);
+  else
+    hipLaunchKernelGGL((k_build<DT, D, NW, MPC_SIM_LINEAR>), dim3(blocks), dim3(NW * kWave), 0, st, a);
 }
 
 template <class DT>
 hipError_t launch_dt(const BuildArgs& a, int D, int blocks, hipStream_t st) {
-  constexpr int NW = 4;
-  if (D == 64) {
-    hipLaunchKernelGGL((k_build<DT, 64, NW>), dim3(blocks), dim3(NW * kWave), 0, st, a);
-  } else if (D == 128) {
-    hipLaunchKernelGGL((k_build<DT, 128, NW>), dim3(blocks), dim3(NW * kWave), 0, st, a);
-  } else {
+  if (D == 64)
+    launch_sim<DT, 64>(a, blocks, st);
+  else if (D == 128)
+    launch_sim<DT, 128>(a, blocks, st);
+  else
     return hipErrorInvalidValue;
-  }
   return hipGetLastError();
 }
 

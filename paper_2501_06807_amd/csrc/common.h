@@ -11,7 +11,8 @@
 namespace mpc {
 
 constexpr int kWave = 64;
-constexpr int kNumCU = 256;  // compute units of an MI355X
+constexpr int kNumCU = 256;         // compute units of an MI355X
+constexpr size_t kMaxLds = 65536;   // LDS bytes one workgroup may allocate
 
 // Element-type tags. A 16-byte vector holds kVec elements.
 struct F32 {

@@ -26,6 +26,8 @@ struct FusedPlan {
 };
 
 FusedPlan fused_plan(const SelectArgs& s, int D);
+// Whether the selection's LDS and the attention's fit one workgroup's LDS together.
+bool fused_fits(const FusedPlan& p, int D, int G);
 hipError_t launch_decode_step(const FusedArgs& f, const FusedPlan& p, int dtype, int D, int G,
                               hipStream_t st);
 

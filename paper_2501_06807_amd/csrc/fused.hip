@@ -22,7 +22,7 @@ namespace {
 constexpr int kFusedWaves = 8;
 constexpr int kSpinLimit = 1 << 20;  // polls (each ~0.1-1 us) before a unit gives up
 
-template <class DT, int D, int G>
+template <class DT, int D, int G, bool MP>
 __global__ __launch_bounds__(kFusedWaves* kWave) void k_decode_step(FusedArgs f) {
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ int s_mode;  // 1 select then attend, 2 attend, 0 gave up
@@ -60,7 +60,7 @@ __global__ __launch_bounds__(kFusedWaves* kWave) void k_decode_step(FusedArgs f)
   const int mode = s_mode;
   if (mode == 1) {
     // one row pass in flight per wave keeps the selection's registers near the attention's
-    dev::select_block<DT, D, kFusedWaves, true, 1>(sa, head, smem);
+    dev::select_block<DT, D, kFusedWaves, true, 1, MP>(sa, head, smem);
     __builtin_amdgcn_s_waitcnt(0);  // this thread's selection stores have completed
     __syncthreads();
     if (tid == 0) __hip_atomic_store(&f.state[head], 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -83,8 +83,11 @@ __global__ __launch_bounds__(kFusedWaves* kWave) void k_decode_step(FusedArgs f)
 
 template <class DT, int D, int G>
 hipError_t launch_g(const FusedArgs& f, size_t smem, hipStream_t st) {
-  hipLaunchKernelGGL((k_decode_step<DT, D, G>), dim3(f.s.n_layers * f.s.B * f.s.Hkv), dim3(kFusedWaves * kWave),
-                     smem, st, f);
+  const dim3 grid(f.s.n_layers * f.s.B * f.s.Hkv), block(kFusedWaves * kWave);
+  if (f.s.similarity == MPC_SIM_MAXPROD)
+    hipLaunchKernelGGL((k_decode_step<DT, D, G, true>), grid, block, smem, st, f);
+  else
+    hipLaunchKernelGGL((k_decode_step<DT, D, G, false>), grid, block, smem, st, f);
   return hipGetLastError();
 }
 
@@ -111,8 +114,14 @@ hipError_t launch_dt(const FusedArgs& f, int D, int G, size_t smem, hipStream_t 
 FusedPlan fused_plan(const SelectArgs& s, int D) {
   FusedPlan p{};
   p.units = s.n_layers * s.B * s.Hkv;
-  p.smem = dev::select_smem_bytes_dev(D, s.S, s.NC);
+  p.smem = dev::select_smem_bytes_dev(D, s.S, s.NC, s.similarity == MPC_SIM_MAXPROD ? s.Hq / s.Hkv : 1);
   return p;
+}
+
+bool fused_fits(const FusedPlan& p, int D, int G) {
+  // the attention's static LDS: selection ids, per-wave (m, l) and partial outputs, a few words
+  const size_t att = 4 * dev::kMaxSel + (size_t)kFusedWaves * G * (2 + D) * 4 + 64;
+  return p.smem + att <= kMaxLds;
 }
 
 hipError_t launch_decode_step(const FusedArgs& f, const FusedPlan& p, int dtype, int D, int G,

@@ -16,10 +16,11 @@ struct SelectArgs {
   int B, layer0, n_layers, Hq, Hkv;
   int C, S, f, NC, k_super, k_clusters;  // NC = k_super * f
   int period, start;
+  int similarity;  // mpc_similarity: representatives of 2 rows (r^max, r^min) for the bound
   OwnerTable own;  // owner layers of the block (one workgroup per owner head)
 };
 
-size_t select_smem_bytes(int D, int S, int NC);
+size_t select_smem_bytes(int D, int S, int NC, int qrows);  // qrows: 1, or G for the bound
 hipError_t launch_select(const SelectArgs& a, int dtype, int D, hipStream_t st);
 
 }  // namespace mpc

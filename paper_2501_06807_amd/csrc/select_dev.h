@@ -71,6 +71,69 @@ __device__ __forceinline__ void tile_dot(const RowTile<D, PASS>& t, int n, int r
   }
 }
 
+// Max-product bound (Eq. 2) of a loaded tile of two-row representatives (r^max in floats [0, D),
+// r^min in [D, 2D) of each row): sum over the G heads and the channels of
+// max(q_{g,i} r^max_i, q_{g,i} r^min_i) in fp64 (the products are exact), qh = [G][D] (LDS).
+template <int D, int PASS>
+__device__ __forceinline__ void tile_dot_mp(const RowTile<2 * D, PASS>& t, int n, int r0, const double* qh, int G,
+                                            double* scores, uint32_t* img, unsigned long long* ck) {
+  constexpr int ROWS = kWave / 4;
+  const int lane = threadIdx.x % kWave, rq = lane >> 2, qk = lane & 3;
+#pragma unroll
+  for (int p = 0; p < PASS; ++p) {
+    double acc = 0.0;
+    for (int g = 0; g < G; ++g) {
+      const double* qg = qh + g * D;
+#pragma unroll
+      for (int c = 0; c < D / 16; ++c) {
+        const double2 q01 = *(const double2*)(qg + c * 16 + qk * 4);
+        const double2 q23 = *(const double2*)(qg + c * 16 + qk * 4 + 2);
+        const float4 hi = t.x[p][c], lo = t.x[p][c + D / 16];
+        acc += fmax(q01.x * (double)hi.x, q01.x * (double)lo.x) + fmax(q01.y * (double)hi.y, q01.y * (double)lo.y) +
+               fmax(q23.x * (double)hi.z, q23.x * (double)lo.z) + fmax(q23.y * (double)hi.w, q23.y * (double)lo.w);
+      }
+    }
+    acc = group_sum<4>(acc);
+    const int r = r0 + p * ROWS + rq;
+    if (qk == 0 && r < n) {
+      const double sc = t.valid[p] ? acc : -INFINITY;
+      scores[r] = sc;
+      img[r] = key_hi(sc);
+      ck[r] = rank_key(img[r], r);
+    }
+  }
+}
+
+// Scoring of one mode: dot-product modes (linear, average) take the group's summed query, the
+// max-product bound the G separate queries and two-row representatives (one row pass in flight).
+template <int D, int PASS, bool MP>
+struct Scoring {
+  static constexpr int RW = MP ? 2 * D : D;  // floats per representative
+  static constexpr int P = MP ? 1 : PASS;    // row passes per wave
+  using Tile = RowTile<RW, P>;
+  __device__ static void dot(const Tile& t, int n, int r0, const double* q, int G, double* scores, uint32_t* img,
+                             unsigned long long* ck) {
+    if constexpr (MP)
+      tile_dot_mp<D, P>(t, n, r0, q, G, scores, img, ck);
+    else
+      tile_dot<D, P>(t, n, r0, q, scores, img, ck);
+  }
+};
+
+// Query rows kept in LDS: the group sum (dot modes) or each of the G heads (bound), fp64.
+template <class DT, int D, bool MP>
+__device__ __forceinline__ void load_query(const void* q, size_t q0, int G, double* dst, int t0, int nt) {
+  if constexpr (MP) {
+    for (int i = t0; i < G * D; i += nt) dst[i] = (double)load_elt<DT>(q, q0 + (size_t)i);
+  } else {
+    for (int i = t0; i < D; i += nt) {
+      double acc = 0.0;
+      for (int g = 0; g < G; ++g) acc += (double)load_elt<DT>(q, q0 + (size_t)g * D + i);
+      dst[i] = acc;
+    }
+  }
+}
+
 // High 32 bits of an order-preserving integer image of a score (-0 is folded into +0 first).
 __device__ __forceinline__ uint32_t key_hi(double x) {
   const unsigned long long b = (unsigned long long)__double_as_longlong(x + 0.0);
@@ -192,12 +255,12 @@ __device__ __forceinline__ int ascending_pos(const int* top, int k, int j) {
 struct BlockLds {
   size_t qsum, s1, s2, ck, img1, img2, list_k, list_i, top, cand, total;
 };
-__host__ __device__ inline BlockLds block_lds(int D, int S, int NC) {
+__host__ __device__ inline BlockLds block_lds(int D, int S, int NC, int qrows) {
   auto al = [](size_t x) { return (x + 15) & ~(size_t)15; };
   const int m = S > NC ? S : NC;
   BlockLds o;
   o.qsum = 0;
-  o.s1 = al(o.qsum + (size_t)D * 8);
+  o.s1 = al(o.qsum + (size_t)qrows * D * 8);
   o.s2 = al(o.s1 + (size_t)S * 8);
   o.ck = al(o.s2 + (size_t)NC * 8);
   o.img1 = al(o.ck + (size_t)m * 8);
@@ -212,12 +275,15 @@ __host__ __device__ inline BlockLds block_lds(int D, int S, int NC) {
 
 // Selection of owner head `ou` by one workgroup of NW waves (`smem`: block_lds().total bytes).
 // COH: write the selection with device-coherent stores (read by another workgroup of the launch).
-// PASS: row passes per wave in flight (registers against memory parallelism).
-template <class DT, int D, int NW, bool COH, int PASS = 2>
+// PASS: row passes per wave in flight (registers against memory parallelism). MP: max-product
+// bound scores (two-row representatives), else dot-product scores.
+template <class DT, int D, int NW, bool COH, int PASS = 2, bool MP = false>
 __device__ void select_block(const SelectArgs& a, int ou, unsigned char* smem) {
+  using SC = Scoring<D, PASS, MP>;
   constexpr int NT = NW * kWave;
-  constexpr int TILE = NW * (kWave / 4) * PASS;  // rows per workgroup pass
-  const BlockLds lay = block_lds(D, a.S, a.NC);
+  constexpr int TILE = NW * (kWave / 4) * SC::P;  // rows per workgroup pass
+  const int G = a.Hq / a.Hkv;
+  const BlockLds lay = block_lds(D, a.S, a.NC, MP ? G : 1);
   double* qsum = (double*)(smem + lay.qsum);
   double* s1 = (double*)(smem + lay.s1);
   double* s2 = (double*)(smem + lay.s2);
@@ -234,21 +300,16 @@ __device__ void select_block(const SelectArgs& a, int ou, unsigned char* smem) {
   const int l = a.own.l[ou / BH], b = (ou / a.Hkv) % a.B, h = ou % a.Hkv;
   const size_t unit = (size_t)l * BH + ou % BH;
   const int abs_l = a.layer0 + l;
-  const int G = a.Hq / a.Hkv;
   const int tid = threadIdx.x, w = tid / kWave;
-  const float* scent = a.scent + unit * a.S * D;
-  const float* cent = a.cent + unit * a.C * D;
+  const float* scent = a.scent + unit * a.S * SC::RW;
+  const float* cent = a.cent + unit * a.C * SC::RW;
 
-  // the first level-1 tile is in flight while the query group is summed
-  RowTile<D, PASS> tile;
+  // the first level-1 tile is in flight while the query rows are loaded
+  typename SC::Tile tile;
   const int r1 = w * (TILE / NW);
-  if (r1 < a.S) tile_load<D, PASS>(scent, nullptr, a.S, r1, tile);
+  if (r1 < a.S) tile_load<SC::RW, SC::P>(scent, nullptr, a.S, r1, tile);
   const size_t q0 = (((size_t)l * a.B + b) * a.Hq + (size_t)h * G) * D;
-  for (int i = tid; i < D; i += NT) {
-    double acc = 0.0;
-    for (int g = 0; g < G; ++g) acc += (double)load_elt<DT>(a.q, q0 + (size_t)g * D + i);
-    qsum[i] = acc;
-  }
+  load_query<DT, D, MP>(a.q, q0, G, qsum, tid, NT);
   if (tid < 2) {
     bnd1[tid] = -1;
     bnd2[tid] = -1;
@@ -256,10 +317,10 @@ __device__ void select_block(const SelectArgs& a, int ou, unsigned char* smem) {
   __syncthreads();
 
   // level 1: super-cluster scores, top-k_super, their member clusters in ascending order
-  if (r1 < a.S) tile_dot<D, PASS>(tile, a.S, r1, qsum, s1, img1, ck);
+  if (r1 < a.S) SC::dot(tile, a.S, r1, qsum, G, s1, img1, ck);
   for (int r0 = r1 + TILE; r0 < a.S; r0 += TILE) {
-    tile_load<D, PASS>(scent, nullptr, a.S, r0, tile);
-    tile_dot<D, PASS>(tile, a.S, r0, qsum, s1, img1, ck);
+    tile_load<SC::RW, SC::P>(scent, nullptr, a.S, r0, tile);
+    SC::dot(tile, a.S, r0, qsum, G, s1, img1, ck);
   }
   __syncthreads();
   block_topk<NT>(ck, a.S, a.k_super, list_k, list_i, top, bnd1);
@@ -275,8 +336,8 @@ __device__ void select_block(const SelectArgs& a, int ou, unsigned char* smem) {
 
   // level 2: candidate scores, top-k_clusters, written in ascending cluster order
   for (int r0 = w * (TILE / NW); r0 < a.NC; r0 += TILE) {
-    tile_load<D, PASS>(cent, cand, a.NC, r0, tile);
-    tile_dot<D, PASS>(tile, a.NC, r0, qsum, s2, img2, ck);
+    tile_load<SC::RW, SC::P>(cent, cand, a.NC, r0, tile);
+    SC::dot(tile, a.NC, r0, qsum, G, s2, img2, ck);
   }
   __syncthreads();
   block_topk<NT>(ck, a.NC, a.k_clusters, list_k, list_i, top, bnd2);
@@ -343,12 +404,12 @@ __device__ void wave_topk(const double* sc, const uint32_t* img, const unsigned 
 struct WaveLds {
   size_t qsum, s1, s2, ck, img, top, cand, total;
 };
-__host__ __device__ inline WaveLds wave_lds(int D, int S, int NC) {
+__host__ __device__ inline WaveLds wave_lds(int D, int S, int NC, int qrows) {
   auto al = [](size_t x) { return (x + 15) & ~(size_t)15; };
   const int m = S > NC ? S : NC;
   WaveLds o;
   o.qsum = 0;
-  o.s1 = al((size_t)D * 8);
+  o.s1 = al((size_t)qrows * D * 8);
   o.s2 = al(o.s1 + (size_t)S * 8);
   o.ck = al(o.s2 + (size_t)NC * 8);
   o.img = al(o.ck + (size_t)m * 8);
@@ -357,18 +418,21 @@ __host__ __device__ inline WaveLds wave_lds(int D, int S, int NC) {
   o.total = al(o.cand + (size_t)NC * 4);
   return o;
 }
-__host__ __device__ inline size_t wave_region_bytes(int D, int S, int NC) { return wave_lds(D, S, NC).total; }
+__host__ __device__ inline size_t wave_region_bytes(int D, int S, int NC, int qrows) {
+  return wave_lds(D, S, NC, qrows).total;
+}
 
 // Selection of owner heads ou0 + w, one per wave w (`smem`: waves x wave_region_bytes()).
-template <class DT, int D, bool COH>
+template <class DT, int D, bool COH, bool MP = false>
 __device__ void select_waves(const SelectArgs& a, int ou0, unsigned char* smem) {
-  constexpr int PASS = 2;
-  constexpr int TILE = (kWave / 4) * PASS;  // rows per wave pass
+  using SC = Scoring<D, 2, MP>;
+  constexpr int TILE = (kWave / 4) * SC::P;  // rows per wave pass
   const int lane = threadIdx.x % kWave, w = threadIdx.x / kWave;
   const int BH = a.B * a.Hkv;
   const int ou = ou0 + w;  // (owner index * B + b) * Hkv + h
   if (ou >= a.own.n * BH) return;
-  const WaveLds lay = wave_lds(D, a.S, a.NC);
+  const int G = a.Hq / a.Hkv;
+  const WaveLds lay = wave_lds(D, a.S, a.NC, MP ? G : 1);
   unsigned char* base = smem + (size_t)w * lay.total;
   double* qsum = (double*)(base + lay.qsum);
   double* s1 = (double*)(base + lay.s1);
@@ -381,26 +445,21 @@ __device__ void select_waves(const SelectArgs& a, int ou0, unsigned char* smem) 
   const int l = a.own.l[ou / BH], b = (ou / a.Hkv) % a.B, h = ou % a.Hkv;
   const size_t unit = (size_t)l * BH + ou % BH;
   const int abs_l = a.layer0 + l;
-  const int G = a.Hq / a.Hkv;
-  const float* scent = a.scent + unit * a.S * D;
-  const float* cent = a.cent + unit * a.C * D;
+  const float* scent = a.scent + unit * a.S * SC::RW;
+  const float* cent = a.cent + unit * a.C * SC::RW;
 
-  // the first level-1 tile is in flight while the query group is summed
-  RowTile<D, PASS> tile;
-  tile_load<D, PASS>(scent, nullptr, a.S, 0, tile);
+  // the first level-1 tile is in flight while the query rows are loaded
+  typename SC::Tile tile;
+  tile_load<SC::RW, SC::P>(scent, nullptr, a.S, 0, tile);
   const size_t q0 = (((size_t)l * a.B + b) * a.Hq + (size_t)h * G) * D;
-  for (int i = lane; i < D; i += kWave) {
-    double acc = 0.0;
-    for (int g = 0; g < G; ++g) acc += (double)load_elt<DT>(a.q, q0 + (size_t)g * D + i);
-    qsum[i] = acc;
-  }
+  load_query<DT, D, MP>(a.q, q0, G, qsum, lane, kWave);
   wave_sync();
 
   // level 1
-  tile_dot<D, PASS>(tile, a.S, 0, qsum, s1, img, ck);
+  SC::dot(tile, a.S, 0, qsum, G, s1, img, ck);
   for (int r0 = TILE; r0 < a.S; r0 += TILE) {
-    tile_load<D, PASS>(scent, nullptr, a.S, r0, tile);
-    tile_dot<D, PASS>(tile, a.S, r0, qsum, s1, img, ck);
+    tile_load<SC::RW, SC::P>(scent, nullptr, a.S, r0, tile);
+    SC::dot(tile, a.S, r0, qsum, G, s1, img, ck);
   }
   wave_sync();
   wave_topk(s1, img, ck, a.S, a.k_super, top);
@@ -415,8 +474,8 @@ __device__ void select_waves(const SelectArgs& a, int ou0, unsigned char* smem) 
 
   // level 2
   for (int r0 = 0; r0 < a.NC; r0 += TILE) {
-    tile_load<D, PASS>(cent, cand, a.NC, r0, tile);
-    tile_dot<D, PASS>(tile, a.NC, r0, qsum, s2, img, ck);
+    tile_load<SC::RW, SC::P>(cent, cand, a.NC, r0, tile);
+    SC::dot(tile, a.NC, r0, qsum, G, s2, img, ck);
   }
   wave_sync();
   wave_topk(s2, img, ck, a.NC, a.k_clusters, top);
@@ -432,7 +491,7 @@ __device__ void select_waves(const SelectArgs& a, int ou0, unsigned char* smem) 
   }
 }
 
-inline size_t select_smem_bytes_dev(int D, int S, int NC) { return block_lds(D, S, NC).total; }
+inline size_t select_smem_bytes_dev(int D, int S, int NC, int qrows) { return block_lds(D, S, NC, qrows).total; }
 
 }  // namespace dev
 }  // namespace mpc

@@ -16,7 +16,7 @@ class MPCachePath:
 
     def __init__(self, *, n_layers, batch, n_q_heads, n_kv_heads, head_dim, dtype, T, window, keep,
                  local_keep, cluster, fanout, k_super, k_clusters, share_period, share_start=2,
-                 alpha=0.6, causal=True, layer0=0, device="cuda", keep_scores=False):
+                 alpha=0.6, causal=True, layer0=0, device="cuda", keep_scores=False, similarity="linear"):
         self.L, self.B, self.Hq, self.Hkv, self.d = n_layers, batch, n_q_heads, n_kv_heads, head_dim
         self.dtype, self.T, self.W, self.keep = dtype, T, window, keep
         self.local_keep, self.causal, self.layer0 = local_keep, causal, layer0
@@ -25,14 +25,16 @@ class MPCachePath:
         self.sm_scale = 1.0 / math.sqrt(head_dim)
         self.C = -(-keep // cluster)
         self.S = -(-self.C // fanout)
-        self.cfg = L.select_cfg(cluster, fanout, k_super, k_clusters, alpha, share_period, share_start)
+        self.cfg = L.select_cfg(cluster, fanout, k_super, k_clusters, alpha, share_period, share_start, similarity)
+        R = L.rep_rows(similarity)
+        rep = (R, head_dim) if R > 1 else (head_dim,)
         dev = torch.device(device)
         kv_shape = (n_layers, batch, n_kv_heads)
         self.kept = torch.zeros(*kv_shape, keep, dtype=torch.int32, device=dev)
         self.k_s = torch.empty(*kv_shape, keep, head_dim, dtype=dtype, device=dev)
         self.v_s = torch.empty_like(self.k_s)
-        self.cent = torch.zeros(*kv_shape, self.C, head_dim, dtype=torch.float32, device=dev)
-        self.scent = torch.zeros(*kv_shape, self.S, head_dim, dtype=torch.float32, device=dev)
+        self.cent = torch.zeros(*kv_shape, self.C, *rep, dtype=torch.float32, device=dev)
+        self.scent = torch.zeros(*kv_shape, self.S, *rep, dtype=torch.float32, device=dev)
         self.sel = torch.zeros(*kv_shape, k_clusters, dtype=torch.int32, device=dev)
         self.sel_score = torch.zeros(*kv_shape, k_clusters, dtype=torch.float32, device=dev)
         self.out = torch.empty(n_layers, batch, n_q_heads, head_dim, dtype=dtype, device=dev)

@@ -13,6 +13,7 @@ HEADER = "include/mpcache.h"
 def declared_functions():
     import os
     src = open(os.path.join(os.path.dirname(__file__), "..", HEADER)).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)  # declarations only, not comment text
     return sorted(set(re.findall(r"\b(mpc_[a-z_]+)\s*\(", src)))
 
 
@@ -75,6 +76,17 @@ def test_select_budget_validation():
     s, _ = _status("mpc_select_clusters", ctypes.byref(d), 300, ctypes.byref(ok_cfg), None, FAKE, FAKE,
                    FAKE, None, None, 0, None)
     assert s == L.MPC_EINVAL  # q is NULL
+
+
+def test_unknown_similarity_is_rejected_before_any_launch():
+    d = _dims()
+    cfg = L.select_cfg(32, 4, 2, 6)
+    cfg.similarity = 3
+    s, msg = _status("mpc_build_clusters", ctypes.byref(d), 300, ctypes.byref(cfg), FAKE, FAKE, FAKE, None)
+    assert s == L.MPC_EINVAL and "similarity" in msg
+    s, msg = _status("mpc_select_clusters", ctypes.byref(d), 300, ctypes.byref(cfg), FAKE, FAKE, FAKE, FAKE, None,
+                     None, 0, None)
+    assert s == L.MPC_EINVAL and "similarity" in msg
 
 
 def test_decode_validation_and_workspace():

@@ -51,25 +51,29 @@ def _queries(w, layer0, step=0):
     return synth.dq_host(sp, step, w.dtype)[layer0:]
 
 
+SIMS = ["linear", "maxprod", "mean"]
+
+
+@pytest.mark.parametrize("sim", SIMS)
 @pytest.mark.parametrize("name", list(CASES))
-def test_build_clusters_bit_exact(name):
+def test_build_clusters_bit_exact(name, sim):
     w, layer0 = _workload(name)
-    say(f"[build] {name} L={w.n_layers} Hkv={w.n_kv_heads} Ts={w.keep} s={w.cluster} f={w.fanout}")
+    say(f"[build] {name} {sim} L={w.n_layers} Hkv={w.n_kv_heads} Ts={w.keep} s={w.cluster} f={w.fanout}")
     k, _ = _cache(w, layer0)
     cent_ref, scent_ref = oracle.build_clusters(k, w.dtype, cluster=w.cluster, fanout=w.fanout, alpha=0.6,
-                                                layer0=layer0, share_period=w.share_period)
+                                                layer0=layer0, share_period=w.share_period, similarity=sim)
     import paper_2501_06807_amd as M
     kd = bits_to_torch(k, w.dtype)
     cent = torch.zeros(cent_ref.shape, dtype=torch.float32, device="cuda")
     scent = torch.zeros(scent_ref.shape, dtype=torch.float32, device="cuda")
-    cfg = M.select_cfg(w.cluster, w.fanout, w.k_super, w.k_clusters, 0.6, w.share_period)
+    cfg = M.select_cfg(w.cluster, w.fanout, w.k_super, w.k_clusters, 0.6, w.share_period, similarity=sim)
     M.mpc_build_clusters(kd, cent, scent, cfg, layer0=layer0)
     torch.cuda.synchronize()
     np.testing.assert_array_equal(cent.cpu().numpy(), cent_ref)
     np.testing.assert_array_equal(scent.cpu().numpy(), scent_ref)
 
 
-def _check_selection(w, layer0, q, cent, scent, sel_gpu, sel_ref, score_gpu):
+def _check_selection(w, layer0, q, cent, scent, sel_gpu, sel_ref, score_gpu, sim="linear"):
     C, S, f, G = cent.shape[3], scent.shape[3], w.fanout, w.group
     n_swaps = 0
     for l in range(w.n_layers):
@@ -81,14 +85,14 @@ def _check_selection(w, layer0, q, cent, scent, sel_gpu, sel_ref, score_gpu):
         for b in range(w.batch):
             for h in range(w.n_kv_heads):
                 qg = q[l, b, h * G:(h + 1) * G]
-                s_all = oracle.cluster_scores(qg, cent[l, b, h], w.dtype)
+                s_all = oracle.cluster_scores(qg, cent[l, b, h], w.dtype, sim)
                 got, exp = sel_gpu[l, b, h], sel_ref[l, b, h]
                 assert np.all(np.diff(got) > 0)
                 if np.array_equal(got, exp):
                     np.testing.assert_allclose(score_gpu[l, b, h], s_all[got].astype(np.float32), rtol=1e-6)
                     continue
                 # a swap is allowed only at a tie, at level 1 or level 2
-                s1 = oracle.cluster_scores(qg, scent[l, b, h], w.dtype)
+                s1 = oracle.cluster_scores(qg, scent[l, b, h], w.dtype, sim)
                 b1 = boundary_score(s1, w.k_super)
                 cand = [c for c in range(C) if abs(s1[c // f] - b1) <= 1e-6 * abs(b1) or c // f in
                         set(np.argsort(-s1, kind="stable")[:w.k_super].tolist())]
@@ -101,22 +105,23 @@ def _check_selection(w, layer0, q, cent, scent, sel_gpu, sel_ref, score_gpu):
     return n_swaps
 
 
-@pytest.mark.parametrize("name", list(CASES))
-def test_select_matches_oracle(name):
+@pytest.mark.parametrize("name,sim", [(n, "linear") for n in CASES] +
+                         [(n, sim) for n in ("C1", "C3", "C4", "C5") for sim in ("maxprod", "mean")])
+def test_select_matches_oracle(name, sim):
     w, layer0 = _workload(name)
-    say(f"[select] {name} L={w.n_layers}@{layer0} Hq={w.n_q_heads} Hkv={w.n_kv_heads} k_super={w.k_super} "
+    say(f"[select] {name} {sim} L={w.n_layers}@{layer0} Hq={w.n_q_heads} Hkv={w.n_kv_heads} k_super={w.k_super} "
         f"k_clusters={w.k_clusters} P={w.share_period}")
     k, _ = _cache(w, layer0)
     cent, scent = oracle.build_clusters(k, w.dtype, cluster=w.cluster, fanout=w.fanout, alpha=0.6,
-                                        layer0=layer0, share_period=w.share_period)
+                                        layer0=layer0, share_period=w.share_period, similarity=sim)
     import paper_2501_06807_amd as M
-    cfg = M.select_cfg(w.cluster, w.fanout, w.k_super, w.k_clusters, 0.6, w.share_period)
+    cfg = M.select_cfg(w.cluster, w.fanout, w.k_super, w.k_clusters, 0.6, w.share_period, similarity=sim)
     cent_d, scent_d = torch.from_numpy(cent).cuda(), torch.from_numpy(scent).cuda()
     for step in range(3):
         q = _queries(w, layer0, step)
         sel_ref, _ = oracle.select_clusters(q, cent, scent, w.dtype, Ts=w.keep, cluster=w.cluster,
                                             fanout=w.fanout, k_super=w.k_super, k_clusters=w.k_clusters,
-                                            layer0=layer0, share_period=w.share_period)
+                                            layer0=layer0, share_period=w.share_period, similarity=sim)
         sel = torch.full(sel_ref.shape, -7, dtype=torch.int32, device="cuda")
         sc = torch.zeros(sel_ref.shape, dtype=torch.float32, device="cuda")
         M.mpc_select_clusters(bits_to_torch(q, w.dtype), cent_d, scent_d, sel, cfg, Ts=w.keep, sel_score=sc,
@@ -128,28 +133,30 @@ def test_select_matches_oracle(name):
             if oracle.owner_layer(layer0 + l, w.share_period, w.share_start) < layer0:
                 assert np.all(sel_g[l] == -7)
                 sel_ref[l] = -7
-        swaps = _check_selection(w, layer0, q, cent, scent, sel_g, sel_ref, sc.cpu().numpy())
+        swaps = _check_selection(w, layer0, q, cent, scent, sel_g, sel_ref, sc.cpu().numpy(), sim)
         say(f"  step {step}: tie swaps {swaps}")
 
 
-def test_select_many_heads_matches_oracle():
+@pytest.mark.parametrize("sim", SIMS)
+def test_select_many_heads_matches_oracle(sim):
     """At least 512 owner heads: the one-wave-per-head selection kernel; every head is checked."""
     w = synth.get("C4").with_(n_layers=8, keep=2048, k_super=4, k_clusters=8)
-    say(f"[select many heads] C4 shape L=8 B=4 Hkv=32 Ts=2048 k_super=4 k_clusters=8")
+    say(f"[select many heads] {sim} C4 shape L=8 B=4 Hkv=32 Ts=2048 k_super=4 k_clusters=8")
     k, _ = _cache(w, 0)
     cent, scent = oracle.build_clusters(k, w.dtype, cluster=w.cluster, fanout=w.fanout, alpha=0.6,
-                                        share_period=w.share_period)
+                                        share_period=w.share_period, similarity=sim)
     import paper_2501_06807_amd as M
-    cfg = M.select_cfg(w.cluster, w.fanout, w.k_super, w.k_clusters, 0.6, w.share_period)
+    cfg = M.select_cfg(w.cluster, w.fanout, w.k_super, w.k_clusters, 0.6, w.share_period, similarity=sim)
     q = _queries(w, 0, 7)
     sel_ref, _ = oracle.select_clusters(q, cent, scent, w.dtype, Ts=w.keep, cluster=w.cluster, fanout=w.fanout,
-                                        k_super=w.k_super, k_clusters=w.k_clusters, share_period=w.share_period)
+                                        k_super=w.k_super, k_clusters=w.k_clusters, share_period=w.share_period,
+                                        similarity=sim)
     sel = torch.zeros(sel_ref.shape, dtype=torch.int32, device="cuda")
     sc = torch.zeros(sel_ref.shape, dtype=torch.float32, device="cuda")
     M.mpc_select_clusters(bits_to_torch(q, w.dtype), torch.from_numpy(cent).cuda(), torch.from_numpy(scent).cuda(),
                           sel, cfg, Ts=w.keep, sel_score=sc)
     torch.cuda.synchronize()
-    swaps = _check_selection(w, 0, q, cent, scent, sel.cpu().numpy(), sel_ref, sc.cpu().numpy())
+    swaps = _check_selection(w, 0, q, cent, scent, sel.cpu().numpy(), sel_ref, sc.cpu().numpy(), sim)
     say(f"  tie swaps {swaps}")
 
 

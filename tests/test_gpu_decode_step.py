@@ -32,11 +32,15 @@ CASES = {
     # small blocks: the two kernels in sequence
     "C1": ("C1", dict(), 0),
     "C2": ("C2", dict(), 0),
+    # the other similarity measures in one launch (four heads per group for the bound)
+    "C5-L32-maxprod": ("C5", dict(keep=8192, k_super=8), 0, "maxprod"),
+    "C3-L8-mean": ("C3", dict(n_layers=8), 0, "mean"),
 }
 
 
 def _setup(case):
-    name, kw, layer0 = CASES[case]
+    name, kw, layer0 = CASES[case][:3]
+    sim = CASES[case][3] if len(CASES[case]) > 3 else "linear"
     w = synth.get(name).with_(**kw)
     ks, vs = [], []
     for l in range(w.n_layers):
@@ -45,8 +49,8 @@ def _setup(case):
         vs.append(v)
     k, v = np.stack(ks), np.stack(vs)
     cent, scent = oracle.build_clusters(k, w.dtype, cluster=w.cluster, fanout=w.fanout, alpha=0.6, layer0=layer0,
-                                        share_period=w.share_period)
-    return w, layer0, k, v, cent, scent
+                                        share_period=w.share_period, similarity=sim)
+    return w, layer0, k, v, cent, scent, sim
 
 
 def _queries(w, layer0, step):
@@ -63,13 +67,13 @@ def _sync_state(ws, n_heads):
 
 @pytest.mark.parametrize("case", list(CASES))
 def test_decode_step_equals_two_calls_and_oracle(case):
-    w, layer0, k, v, cent, scent = _setup(case)
+    w, layer0, k, v, cent, scent, sim = _setup(case)
     import paper_2501_06807_amd as M
     units = w.n_layers * w.batch * w.n_kv_heads
     say(f"[step] {case}: L={w.n_layers}@{layer0} B={w.batch} Hq={w.n_q_heads} Hkv={w.n_kv_heads} Ts={w.keep} "
         f"s={w.cluster} f={w.fanout} k_super={w.k_super} k_clusters={w.k_clusters} units={units}")
     dt = synth.torch_dtype(w.dtype)
-    cfg = M.select_cfg(w.cluster, w.fanout, w.k_super, w.k_clusters, 0.6, w.share_period)
+    cfg = M.select_cfg(w.cluster, w.fanout, w.k_super, w.k_clusters, 0.6, w.share_period, similarity=sim)
     kd, vd = bits_to_torch(k, w.dtype), bits_to_torch(v, w.dtype)
     cent_d, scent_d = torch.from_numpy(cent).cuda(), torch.from_numpy(scent).cuda()
     shape_sel = (w.n_layers, w.batch, w.n_kv_heads, w.k_clusters)
@@ -90,7 +94,7 @@ def test_decode_step_equals_two_calls_and_oracle(case):
         qd = bits_to_torch(q, w.dtype)
         sel_ref, _ = oracle.select_clusters(q, cent, scent, w.dtype, Ts=w.keep, cluster=w.cluster, fanout=w.fanout,
                                             k_super=w.k_super, k_clusters=w.k_clusters, layer0=layer0,
-                                            share_period=w.share_period, sel_in=sel_in)
+                                            share_period=w.share_period, sel_in=sel_in, similarity=sim)
         outs = []
         for fused in (False, True):
             sel = torch.from_numpy(np.ascontiguousarray(sel_ref)).cuda()
@@ -120,7 +124,7 @@ def test_decode_step_equals_two_calls_and_oracle(case):
         assert err == 0 and not words.any(), f"error {err}, non-zero head words {words.nonzero().flatten()[:8]}"
         # oracle: selection (tie rule) and attention over the selection the GPU made
         sel_g = s1.numpy()
-        swaps = _check_selection(w, layer0, q, cent, scent, sel_g, sel_ref.copy(), c1.numpy())
+        swaps = _check_selection(w, layer0, q, cent, scent, sel_g, sel_ref.copy(), c1.numpy(), sim)
         ref, lse_ref = oracle.sparse_decode_attn(q, k, v, np.ascontiguousarray(sel_g), w.dtype, cluster=w.cluster,
                                                  sm_scale=sm)
         worst = assert_out_close(to_f64(o1), ref, w.dtype, case)
