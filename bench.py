@@ -248,6 +248,23 @@ def main():
     step_time(other)
     alt = {"mode": "split" if fused else "fused", "us": round(step_time(other), 3)}
 
+    # selection quality on the last step's queries: the share of each head's full softmax mass
+    # (over every kept token) that falls on the selected clusters, exp(lse_selected - lse_all)
+    path.decode(qs[E - 1])
+    lse_sel = path.lse.clone()
+    all_sel = torch.arange(path.C, dtype=torch.int32, device=dev).expand(*path.sel.shape[:3], path.C).contiguous()
+    out_all = torch.empty_like(path.out)
+    lse_all = torch.empty_like(path.lse)
+    ws_all = M.workspace(M.workspace_bytes(M.MPC_OP_DECODE_ATTN, M.dims_of(path.out, path.k_s), w.keep), dev)
+    M.mpc_sparse_decode_attn(qs[E - 1], path.k_s, path.v_s, all_sel, out_all, cluster_size=w.cluster,
+                             sm_scale=path.sm_scale, lse=lse_all, ws=ws_all)
+    recall = torch.exp(lse_sel.double() - lse_all.double())
+    quality = {"attention_mass_recall_mean": round(recall.mean().item(), 4),
+               "attention_mass_recall_min": round(recall.min().item(), 4),
+               "note": "share of each head's softmax mass over all kept tokens that the selected clusters hold "
+                       "(last decode step, every layer, sequence and query head)"}
+    del all_sel, out_all, lse_all, ws_all
+
     owners = [l for l in range(w.n_layers) if M.owner_layer(l, w.share_period, w.share_start) == l]
     sel_b, att_b = decode_bytes(w, owners, path.sel.cpu().numpy(), path.C, path.S, M.rep_rows(args.similarity))
     step_b = sel_b + att_b
@@ -295,6 +312,7 @@ def main():
                     "note": "each kernel launched once per decode step, back to back, between two HIP "
                             "events; per-launch average (attention reads each step's own selection)"},
         "decode_step_other_mode": alt,
+        "selection_quality": quality,
         "roofline": roofline,
         "copy_ceiling": {"GBps": round(copy_gbs, 1), "frac_of_peak": round(copy_gbs / HBM_PEAK_GBS, 4),
                          "note": "1 GiB device-to-device copy, read + write bytes"},

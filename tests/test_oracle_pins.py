@@ -331,6 +331,25 @@ def test_maxprod_equals_alpha_one_linear_for_nonnegative_queries():
                                   oracle.cluster_scores(q, mp[0, 0, 0], "bf16", "maxprod"))
 
 
+def test_average_dilutes_a_single_important_token():
+    # the paper's argument against the average (Sec. 3.3 opening; appendix comparison): a cluster
+    # holding one key aligned with q among opposed keys ranks below a uniformly mild cluster under
+    # the average, but above it under the max-product bound and the alpha = 0.6 linear form, which
+    # follow the true maximum dot product
+    d, s = 8, 16
+    q = np.zeros((1, d)); q[0, 0] = 1.0
+    a = np.full((s, d), 0.0); a[:, 0] = -1.0; a[0, 0] = 8.0       # one key with q.k = 8, the rest -1
+    b = np.full((s, d), 0.0); b[:, 0] = 1.0                         # every key q.k = 1
+    k = to_bits(np.concatenate([a, b])[None, None, None], "fp32")
+    qb = to_bits(q, "fp32")
+    true_max = [8.0, 1.0]
+    for sim, winner in (("maxprod", 0), ("linear", 0), ("mean", 1)):
+        cent, _ = oracle.build_clusters(k, "fp32", cluster=s, fanout=2, alpha=0.6, similarity=sim)
+        sc = oracle.cluster_scores(qb, cent[0, 0, 0], "fp32", sim)
+        assert int(np.argmax(sc)) == winner, (sim, sc)
+    assert int(np.argmax(true_max)) == 0
+
+
 # ------------------------------------------------------------------------ selection (A5-A7)
 def test_topk_matches_lexsort():
     r = rng(17)
