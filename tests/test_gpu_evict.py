@@ -22,7 +22,7 @@ def _prefill(w, layer0=0):
     return np.stack(qs), np.stack(ks), np.stack(vs)
 
 
-def _run_gpu(w, qw, k, v, layer0=0, kept_in=None):
+def _run_gpu(w, qw, k, v, layer0=0, kept_in=None, causal=True, sm=None):
     import paper_2501_06807_amd as M
     L, B, Hkv = k.shape[:3]
     dt = w.dtype
@@ -33,7 +33,8 @@ def _run_gpu(w, qw, k, v, layer0=0, kept_in=None):
     score = torch.zeros((L, B, Hkv, w.T), dtype=torch.float32, device="cuda")
     row_lse = torch.zeros((L, B, w.n_q_heads, w.window), dtype=torch.float32, device="cuda")
     M.mpc_static_evict(bits_to_torch(qw, dt), bits_to_torch(k, dt), bits_to_torch(v, dt), kept, k_out, v_out,
-                       keep=w.keep, local_keep=w.local_keep, sm_scale=1.0 / math.sqrt(w.head_dim),
+                       keep=w.keep, local_keep=w.local_keep,
+                       sm_scale=1.0 / math.sqrt(w.head_dim) if sm is None else sm, causal=causal,
                        layer0=layer0, share_period=w.share_period, share_start=w.share_start,
                        token_score=score, row_lse=row_lse)
     torch.cuda.synchronize()
@@ -138,3 +139,30 @@ def test_identity_budget_keeps_everything():
     assert np.all(kept == np.arange(512))
     np.testing.assert_array_equal(ko, k)
     np.testing.assert_array_equal(vo, v)
+
+
+@pytest.mark.parametrize("name", ["C1", "C2"])
+def test_literal_algorithm_readings(name):
+    """Alg. 3 read literally: no causal mask, no 1/sqrt(d) in the window scores, and the pairing
+    l % 2 of layers (sharing from layer 0). The kept sets follow the oracle under the tie rule;
+    token scores are compared against the largest one (sharper softmaxes underflow the smallest)."""
+    w = synth.get(name).with_(share_start=0, **({"n_layers": 4} if name == "C2" else {}))
+    say(f"[evict literal] {name} causal=0 sm_scale=1 share_start=0 P={w.share_period}")
+    qw, k, v = _prefill(w)
+    kept_g, ko_g, vo_g, sc_g, _ = _run_gpu(w, qw, k, v, causal=False, sm=1.0)
+    kept_r, _, _, sc_r = oracle.static_evict(qw, k, v, w.dtype, keep=w.keep, local_keep=w.local_keep, sm_scale=1.0,
+                                             causal=False, share_period=w.share_period, share_start=0,
+                                             with_scores=True)
+    loc = min(w.local_keep, w.keep)
+    for l in range(w.n_layers):
+        o = oracle.owner_layer(l, w.share_period, 0)
+        for b in range(w.batch):
+            for h in range(w.n_kv_heads):
+                if o == l:
+                    top = float(sc_r[l, b, h].max())
+                    np.testing.assert_allclose(sc_g[l, b, h], sc_r[l, b, h], rtol=2e-5, atol=1e-6 * top)
+                    bnd = boundary_score(sc_r[l, b, h, :w.T - loc], w.keep - loc)
+                    assert_sets_tie_equal(kept_g[l, b, h], kept_r[l, b, h], sc_r[l, b, h], bnd, f"l {l} h {h}")
+                else:
+                    np.testing.assert_array_equal(kept_g[l, b, h], kept_g[o, b, h])
+                np.testing.assert_array_equal(ko_g[l, b, h], k[l, b, h, kept_g[l, b, h]])
