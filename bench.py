@@ -248,6 +248,30 @@ def main():
     step_time(other)
     alt = {"mode": "split" if fused else "fused", "us": round(step_time(other), 3)}
 
+    # cache state: each decode step alone between two events, once right after the previous step
+    # (warm: L2 and the 256 MB memory-side cache hold what the earlier steps left) and once after a
+    # read of 1 GiB of unrelated data (cold: nothing of the path's data is cached)
+    flush = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+
+    def single_steps(cold):
+        t = []
+        for e in range(E):
+            if cold:
+                flush.sum()
+            a, b = mk(), mk()
+            a.record()
+            step_fn(qs[e])
+            b.record()
+            t.append((a, b))
+        torch.cuda.synchronize()
+        return mean([a.elapsed_time(b) for a, b in t]) * 1e3
+
+    single_steps(False)
+    cache = {"warm_us": round(single_steps(False), 3), "cold_us": round(single_steps(True), 3),
+             "note": "one decode step between two HIP events (so launch latency is inside both); cold = "
+                     "after reading 1 GiB of other data, which evicts L2 and the memory-side cache"}
+    del flush
+
     # selection quality on the last step's queries: the share of each head's full softmax mass
     # (over every kept token) that falls on the selected clusters, exp(lse_selected - lse_all)
     path.decode(qs[E - 1])
@@ -312,6 +336,7 @@ def main():
                     "note": "each kernel launched once per decode step, back to back, between two HIP "
                             "events; per-launch average (attention reads each step's own selection)"},
         "decode_step_other_mode": alt,
+        "decode_step_cache": cache,
         "selection_quality": quality,
         "roofline": roofline,
         "copy_ceiling": {"GBps": round(copy_gbs, 1), "frac_of_peak": round(copy_gbs / HBM_PEAK_GBS, 4),
