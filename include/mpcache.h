@@ -6,7 +6,8 @@
  *   - hierarchical cluster representatives alpha*r^max + (1-alpha)*r^min (Sec. 3.3, Eq. "sim");
  *   - query-aware two-level cluster selection with cross-layer index sharing (Sec. 3.3, 3.4;
  *     Alg. 3 step 2);
- *   - gather + softmax attention over the selected clusters (Alg. 1 steps 3-4).
+ *   - gather + softmax attention over the selected clusters (Alg. 1 steps 3-4);
+ *   - decode-time growth of the kept cache (App. A.3: each decoded token's k, v are appended).
  *
  * Conventions shared by every entry point
  *   - Tensor arguments are DEVICE pointers owned by the caller, contiguous row-major, with
@@ -15,6 +16,11 @@
  *     absolute layer dims->layer0), Hq / Hkv query / kv heads (q-head h reads kv-head h / G,
  *     G = Hq / Hkv), d head dim, T prompt tokens, W window rows, Ts kept tokens,
  *     s cluster size, C = ceil(Ts / s) clusters, f fan-out, S = ceil(C / f) super-clusters.
+ *   - Kept-cache tensors are allocated for Tcap rows per (layer, sequence, kv head), where
+ *     Tcap = dims->kv_capacity, or the rows of the call when it is 0 (Ts, plus n_tail where a call
+ *     takes a tail; keep for the eviction's outputs). K/V caches are [L][B][Hkv][Tcap][d];
+ *     representatives have Ccap = ceil(Tcap / s) cluster slots and Scap = ceil(Ccap / f)
+ *     super-cluster slots. A cache that grows during decoding (mpc_append_kv) keeps one Tcap.
  *   - Cross-layer sharing: owner(l) = l if period <= 1 or l < start, else
  *     start + period * floor((l - start) / period), on absolute layer indices (Sec. 3.4: the
  *     first two layers never share, so start = 2 follows the paper's text; start = 0 gives the
@@ -56,6 +62,8 @@ typedef struct {
   int32_t n_kv_heads; /* Hkv                                              */
   int32_t head_dim;   /* d                                                */
   int32_t dtype;      /* mpc_dtype of q / k / v / out                     */
+  int32_t kv_capacity; /* Tcap: rows allocated per (layer, sequence, kv head) in the kept
+                        * cache; 0 = exactly the rows of the call                            */
 } mpc_dims;
 
 /* Cluster similarity (Sec. 3.3). LINEAR: the reordered linear form (Eq. "sim"), one
@@ -103,7 +111,7 @@ size_t mpc_workspace_bytes(int32_t op, const mpc_dims* dims, int32_t T_or_Ts, co
  *   q_win       [L][B][Hq][W][d]   window queries (read for owner layers only)
  *   k, v        [L][B][Hkv][T][d]  prompt cache
  *   kept_idx    [L][B][Hkv][keep]  int32 out (in for layers owned before layer0)
- *   k_out,v_out [L][B][Hkv][keep][d] out
+ *   k_out,v_out [L][B][Hkv][Tcap][d] out, rows [0, keep) written (Tcap >= keep)
  *   token_score [L][B][Hkv][T] float, optional out (NULL = not returned); owner layers only
  *   row_lse     [L][B][Hq][W] float, optional out: natural log-sum-exp of each window row's
  *               scaled scores (the softmax normaliser); owner layers only
@@ -121,7 +129,8 @@ mpc_status mpc_static_evict(const mpc_dims* dims, int32_t T, const mpc_evict_cfg
  *   MAXPROD  two rows, r^max then r^min (exact key values);
  *   MEAN     one row, fp32( fp64 sum of the tokens' values / token count ).
  * Owner layers only. R = 2 for MAXPROD, else 1.
- *   k_cache [L][B][Hkv][Ts][d];  cent [L][B][Hkv][C][R][d] float out;  scent [L][B][Hkv][S][R][d] */
+ *   k_cache [L][B][Hkv][Tcap][d];  cent [L][B][Hkv][Ccap][R][d] float out (slots [0, C) written);
+ *   scent [L][B][Hkv][Scap][R][d] (slots [0, S)). */
 mpc_status mpc_build_clusters(const mpc_dims* dims, int32_t Ts, const mpc_select_cfg* cfg,
                               const void* k_cache, float* cent, float* scent, void* stream);
 
@@ -132,7 +141,8 @@ mpc_status mpc_build_clusters(const mpc_dims* dims, int32_t Ts, const mpc_select
  * k_clusters best fine clusters among their members (ties: lower index first); the selection is
  * written in ascending cluster order. Non-owner layers receive their owner's selection; a layer
  * whose owner precedes layer0 is left untouched (the caller copies it).
- *   q [L][B][Hq][d];  cent / scent as produced by mpc_build_clusters;
+ *   q [L][B][Hq][d];  cent / scent as produced by mpc_build_clusters (Ccap / Scap slots, the
+ *   first C / S used);
  *   sel [L][B][Hkv][k_clusters] int32 out;  sel_score same shape, float, optional (score rounded
  *   to fp32). ws may be NULL (no workspace needed). Limits: S <= 1024, k_super * f <= 1024. */
 mpc_status mpc_select_clusters(const mpc_dims* dims, int32_t Ts, const mpc_select_cfg* cfg,
@@ -142,16 +152,19 @@ mpc_status mpc_select_clusters(const mpc_dims* dims, int32_t Ts, const mpc_selec
 
 /* Sparse attention over the selected clusters (Alg. 1 steps 3-4; Alg. 3 step 2):
  * o_h = softmax(sm_scale * q_h K'^T) V' with K', V' the kept-cache rows of the clusters in
- * sel[l][b][h / G] (tokens past Ts in a partial last cluster are skipped).
- *   q [L][B][Hq][d];  k_cache, v_cache [L][B][Hkv][Ts][d];  sel [L][B][Hkv][k_clusters] int32
- *   (every entry in [0, C));  out [L][B][Hq][d] (dtype);  lse [L][B][Hq] float, optional
- *   (natural-log log-sum-exp of the scaled scores). fp32 accumulation; 16-bit types take exact
- *   pairwise products summed in fp32. Limits: k_clusters <= 1024, Ts * d * element size <= 2 GiB.
+ * sel[l][b][h / G] (tokens past Ts in a partial last cluster are skipped), followed by the n_tail
+ * unclustered rows [Ts, Ts + n_tail) that decoding appended (mpc_append_kv), which every head
+ * attends in full.
+ *   q [L][B][Hq][d];  k_cache, v_cache [L][B][Hkv][Tcap][d];  sel [L][B][Hkv][k_clusters] int32
+ *   (entries outside [0, C) contribute nothing);  n_tail >= 0, and Ts % s == 0 when n_tail > 0;
+ *   out [L][B][Hq][d] (dtype);  lse [L][B][Hq] float, optional (natural-log log-sum-exp of the
+ *   scaled scores). fp32 accumulation; 16-bit types take exact pairwise products summed in fp32.
+ *   Limits: k_clusters + ceil(n_tail / s) <= 1024, Tcap * d * element size <= 2 GiB.
  *   ws: mpc_workspace_bytes(MPC_OP_DECODE_ATTN, dims, Ts, NULL) bytes (split-K partials and
  *   per-unit arrival counters, used when there are fewer (layer, sequence, kv head) units than
  *   twice the compute units), zero-filled before its first use; every completed call leaves the
  *   counters at zero (calls sharing it must not overlap). May be NULL when that size is 0. */
-mpc_status mpc_sparse_decode_attn(const mpc_dims* dims, int32_t Ts, int32_t cluster_size,
+mpc_status mpc_sparse_decode_attn(const mpc_dims* dims, int32_t Ts, int32_t n_tail, int32_t cluster_size,
                                   const void* q, const void* k_cache, const void* v_cache,
                                   const int32_t* sel, int32_t k_clusters, float sm_scale,
                                   void* out, float* lse, void* ws, size_t ws_bytes, void* stream);
@@ -159,7 +172,8 @@ mpc_status mpc_sparse_decode_attn(const mpc_dims* dims, int32_t Ts, int32_t clus
 /* One decode step in one launch: mpc_select_clusters followed by mpc_sparse_decode_attn (same
  * definitions, same results bit for bit), with the attention of a layer starting as soon as its
  * owner's selection is published instead of after a kernel boundary.
- *   q [L][B][Hq][d]; cent, scent from mpc_build_clusters; k_cache, v_cache [L][B][Hkv][Ts][d];
+ *   q [L][B][Hq][d]; cent, scent from mpc_build_clusters; k_cache, v_cache [L][B][Hkv][Tcap][d];
+ *   n_tail: unclustered rows after Ts, attended in full (as in mpc_sparse_decode_attn);
  *   sel [L][B][Hkv][cfg->k_clusters] int32 out (in for layers owned before layer0);
  *   sel_score optional; out [L][B][Hq][d]; lse optional.
  *   ws: mpc_workspace_bytes(MPC_OP_DECODE_STEP, dims, Ts, cfg) bytes, zero-filled before its first
@@ -167,11 +181,30 @@ mpc_status mpc_sparse_decode_attn(const mpc_dims* dims, int32_t Ts, int32_t clus
  * Blocks whose attention is split over several workgroups per unit, or whose selection and
  * attention together need more LDS than one workgroup has, run the two kernels one after the other
  * instead (same results). */
-mpc_status mpc_decode_step(const mpc_dims* dims, int32_t Ts, const mpc_select_cfg* cfg,
+mpc_status mpc_decode_step(const mpc_dims* dims, int32_t Ts, int32_t n_tail, const mpc_select_cfg* cfg,
                            const void* q, const float* cent, const float* scent,
                            const void* k_cache, const void* v_cache, float sm_scale, int32_t* sel,
                            float* sel_score, void* out, float* lse, void* ws, size_t ws_bytes,
                            void* stream);
+
+/* Decode-time growth of the kept cache (App. A.3: the k, v of each decoded token are appended to
+ * the cache). The cache of a block is the pair (Ts, n_tail): clustered rows [0, Ts) with
+ * representatives, and n_tail newer rows [Ts, Ts + n_tail), 0 <= n_tail <= s, that every decode
+ * attention reads in full. One call per decoded token, for every layer of the block:
+ *   1. if the tail is full (n_tail == s) it is sealed: rows [Ts, Ts + s) become cluster Ts / s, and
+ *      on owner layers that cluster's representative and its super-cluster's are rebuilt from the
+ *      rows, exactly as mpc_build_clusters over Ts + s rows would give them; Ts += s, n_tail = 0;
+ *   2. the new k, v are written at row Ts + n_tail; n_tail += 1.
+ * So the state after the call is (Ts + s, 1) when n_tail == s, else (Ts, n_tail + 1), and the
+ * token just appended is always in the tail.
+ *   k_new, v_new [L][B][Hkv][d];  k_cache, v_cache [L][B][Hkv][Tcap][d] in/out;
+ *   cent, scent [L][B][Hkv][Ccap / Scap][R][d] float in/out (cfg->similarity gives R).
+ * Requires Ts % s == 0 and a row free after sealing (Ts + n_tail + 1 <= Tcap, Tcap =
+ * dims->kv_capacity, which must be set). The caller keeps (Ts, n_tail) and passes them to the
+ * selection (Ts) and attention (Ts, n_tail) calls. */
+mpc_status mpc_append_kv(const mpc_dims* dims, int32_t Ts, int32_t n_tail, const mpc_select_cfg* cfg,
+                         const void* k_new, const void* v_new, void* k_cache, void* v_cache,
+                         float* cent, float* scent, void* stream);
 
 /* Owner layer of absolute layer `l` under the sharing rule above. */
 int32_t mpc_owner_layer(int32_t l, int32_t period, int32_t start);

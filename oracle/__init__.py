@@ -41,7 +41,8 @@ def lib():
             "mpcref_static_evict": ([I] * 11 + [F, I, I, I] + [V] * 7, ctypes.c_int),
             "mpcref_build_clusters": ([I] * 9 + [F, I, I, I] + [V] * 3, ctypes.c_int),
             "mpcref_select_clusters": ([I] * 15 + [V] * 5, ctypes.c_int),
-            "mpcref_sparse_decode_attn": ([I] * 8 + [V] * 4 + [I, F, V, V], ctypes.c_int),
+            "mpcref_append_state": ([I, I, I, V, V], ctypes.c_int),
+            "mpcref_sparse_decode_attn": ([I] * 9 + [V] * 4 + [I, F, V, V], ctypes.c_int),
             "mpcref_dense_decode_attn": ([I] * 7 + [V] * 3 + [F, V, V], ctypes.c_int),
             "mpcref_threads": ([], ctypes.c_int),
         }
@@ -242,13 +243,22 @@ def select_clusters(q, cent, scent, dtype, *, Ts, cluster, fanout, k_super, k_cl
     return sel, score
 
 
-def sparse_decode_attn(q, k_cache, v_cache, sel, dtype, *, cluster, sm_scale):
+def append_state(Ts, n_tail, cluster):
+    """(Ts, n_tail) after one decode-time append (App. A.3; sealing rule is our reading)."""
+    a, b = ctypes.c_int32(), ctypes.c_int32()
+    _ok(lib().mpcref_append_state(Ts, n_tail, cluster, ctypes.byref(a), ctypes.byref(b)), "mpcref_append_state")
+    return a.value, b.value
+
+
+def sparse_decode_attn(q, k_cache, v_cache, sel, dtype, *, cluster, sm_scale, n_tail=0):
+    """k_cache / v_cache [L][B][Hkv][Ts + n_tail][d]: clustered rows, then n_tail tail rows that every
+    head attends."""
     q, k_cache, v_cache, sel = _c(q), _c(k_cache), _c(v_cache), _c(sel, np.int32)
     L, B, Hq, d = q.shape
-    Hkv, Ts = k_cache.shape[2], k_cache.shape[3]
+    Hkv, Ts = k_cache.shape[2], k_cache.shape[3] - n_tail
     out = np.empty((L, B, Hq, d), np.float64)
     lse = np.empty((L, B, Hq), np.float64)
-    _ok(lib().mpcref_sparse_decode_attn(B, L, Hq, Hkv, d, DTYPE_CODE[dtype], Ts, cluster, _p(q),
+    _ok(lib().mpcref_sparse_decode_attn(B, L, Hq, Hkv, d, DTYPE_CODE[dtype], Ts, n_tail, cluster, _p(q),
                                         _p(k_cache), _p(v_cache), _p(sel), sel.shape[-1], sm_scale,
                                         _p(out), _p(lse)), "mpcref_sparse_decode_attn")
     return out, lse

@@ -466,16 +466,34 @@ int mpcref_select_clusters(int32_t B, int32_t layer0, int32_t n_layers, int32_t 
   return OK;
 }
 
-// Sparse attention of every query head over the tokens of its kv head's selected clusters.
+// Decode-time cache growth (App. A.3): every decoded token's k, v are concatenated to the cache.
+// The paper does not say how new tokens join clusters. Reading: they collect in an unclustered
+// tail that is always attended; when a token arrives and the tail already holds s tokens, those s
+// become the next cluster (Ts grows by s) before the new token starts the tail again.
+int mpcref_append_state(int32_t Ts, int32_t n_tail, int32_t cluster, int32_t* Ts_out, int32_t* n_tail_out) {
+  if (Ts < 0 || cluster <= 0 || n_tail < 0 || n_tail > cluster || !Ts_out || !n_tail_out) return EINVAL;
+  if (n_tail == cluster) {
+    Ts += cluster;
+    n_tail = 0;
+  }
+  *Ts_out = Ts;
+  *n_tail_out = n_tail + 1;
+  return OK;
+}
+
+// Sparse attention of every query head over the tokens of its kv head's selected clusters, then
+// the n_tail decode-time tokens that follow the clustered ones (k_cache holds Ts + n_tail rows per
+// head).
 int mpcref_sparse_decode_attn(int32_t B, int32_t n_layers, int32_t Hq, int32_t Hkv, int32_t d,
-                              int32_t dtype, int32_t Ts, int32_t cluster, const void* q,
+                              int32_t dtype, int32_t Ts, int32_t n_tail, int32_t cluster, const void* q,
                               const void* k_cache, const void* v_cache, const int32_t* sel,
                               int32_t k_clusters, float sm_scale, double* out, double* lse) {
-  if (B <= 0 || n_layers <= 0 || Hq <= 0 || Hkv <= 0 || d <= 0 || Ts <= 0 || cluster <= 0 ||
+  if (B <= 0 || n_layers <= 0 || Hq <= 0 || Hkv <= 0 || d <= 0 || Ts <= 0 || n_tail < 0 || cluster <= 0 ||
       k_clusters <= 0 || !valid_dtype(dtype) || !q || !k_cache || !v_cache || !sel || !out)
     return EINVAL;
   if (Hq % Hkv) return ESHAPE;
   const int32_t G = Hq / Hkv, C = ceil_div(Ts, cluster);
+  const int32_t rows_per_head = Ts + n_tail;
   const size_t es = elt_size(dtype);
   const int64_t units = (int64_t)n_layers * B * Hq;
   int rc = OK;
@@ -495,7 +513,9 @@ int mpcref_sparse_decode_attn(int32_t B, int32_t n_layers, int32_t Hq, int32_t H
       for (int32_t t = c * cluster; t < std::min(Ts, (c + 1) * cluster); ++t) rows.push_back(t);
     }
     if (rows.empty()) continue;
-    const size_t head = (size_t)kvu * Ts * d * es;
+    // the tokens appended while decoding (App. A.3), not yet in any cluster: always attended
+    for (int32_t t = Ts; t < Ts + n_tail; ++t) rows.push_back(t);
+    const size_t head = (size_t)kvu * rows_per_head * d * es;
     mpcref_attend(d, dtype, sm_scale, (const char*)q + (size_t)u * d * es, (int32_t)rows.size(),
                   rows.data(), (const char*)k_cache + head, (const char*)v_cache + head,
                   out + (size_t)u * d, lse ? lse + u : nullptr);

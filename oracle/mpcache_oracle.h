@@ -75,8 +75,14 @@ int mpcref_select_clusters(int32_t B, int32_t layer0, int32_t n_layers, int32_t 
                            int32_t k_super, int32_t k_clusters, int32_t share_period,
                            int32_t share_start, int32_t similarity, const void* q,
                            const float* cent, const float* scent, int32_t* sel, double* sel_score);
+/* Decode-time growth: (Ts, n_tail) after one appended token (a full tail of `cluster` rows is
+ * sealed into a cluster first). Our reading; the paper only states the concatenation. */
+int mpcref_append_state(int32_t Ts, int32_t n_tail, int32_t cluster, int32_t* Ts_out,
+                        int32_t* n_tail_out);
+/* k_cache / v_cache hold Ts + n_tail rows per (layer, sequence, kv head): the clustered rows, then
+ * the tail rows every head attends. */
 int mpcref_sparse_decode_attn(int32_t B, int32_t n_layers, int32_t Hq, int32_t Hkv, int32_t d,
-                              int32_t dtype, int32_t Ts, int32_t cluster, const void* q,
+                              int32_t dtype, int32_t Ts, int32_t n_tail, int32_t cluster, const void* q,
                               const void* k_cache, const void* v_cache, const int32_t* sel,
                               int32_t k_clusters, float sm_scale, double* out, double* lse);
 int mpcref_dense_decode_attn(int32_t B, int32_t n_layers, int32_t Hq, int32_t Hkv, int32_t d,

@@ -19,7 +19,7 @@ DTYPE_CODE = {torch.float32: 0, torch.float16: 1, torch.bfloat16: 2}
 
 class MpcDims(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in
-                ("batch", "layer0", "n_layers", "n_q_heads", "n_kv_heads", "head_dim", "dtype")]
+                ("batch", "layer0", "n_layers", "n_q_heads", "n_kv_heads", "head_dim", "dtype", "kv_capacity")]
 
 
 class MpcSelectCfg(ctypes.Structure):
@@ -44,8 +44,8 @@ class MpcError(RuntimeError):
 
 _LIB = None
 EXPORTS = ("mpc_workspace_bytes", "mpc_static_evict", "mpc_build_clusters", "mpc_select_clusters",
-           "mpc_sparse_decode_attn", "mpc_decode_step", "mpc_owner_layer", "mpc_status_string",
-           "mpc_last_error")
+           "mpc_sparse_decode_attn", "mpc_decode_step", "mpc_append_kv", "mpc_owner_layer",
+           "mpc_status_string", "mpc_last_error")
 
 
 def lib():
@@ -61,11 +61,12 @@ def lib():
         L.mpc_static_evict.argtypes = [P(MpcDims), I, P(MpcEvictCfg)] + [V] * 8 + [V, ctypes.c_size_t, V]
         L.mpc_build_clusters.argtypes = [P(MpcDims), I, P(MpcSelectCfg), V, V, V, V]
         L.mpc_select_clusters.argtypes = [P(MpcDims), I, P(MpcSelectCfg)] + [V] * 5 + [V, ctypes.c_size_t, V]
-        L.mpc_sparse_decode_attn.argtypes = [P(MpcDims), I, I, V, V, V, V, I, F, V, V, V, ctypes.c_size_t, V]
-        L.mpc_decode_step.argtypes = [P(MpcDims), I, P(MpcSelectCfg)] + [V] * 5 + [F] + [V] * 4 + [
+        L.mpc_sparse_decode_attn.argtypes = [P(MpcDims), I, I, I, V, V, V, V, I, F, V, V, V, ctypes.c_size_t, V]
+        L.mpc_decode_step.argtypes = [P(MpcDims), I, I, P(MpcSelectCfg)] + [V] * 5 + [F] + [V] * 4 + [
             V, ctypes.c_size_t, V]
+        L.mpc_append_kv.argtypes = [P(MpcDims), I, I, P(MpcSelectCfg)] + [V] * 7
         for fn in ("mpc_static_evict", "mpc_build_clusters", "mpc_select_clusters", "mpc_sparse_decode_attn",
-                   "mpc_decode_step"):
+                   "mpc_decode_step", "mpc_append_kv"):
             getattr(L, fn).restype = ctypes.c_int
         L.mpc_owner_layer.argtypes = [I, I, I]
         L.mpc_owner_layer.restype = I
@@ -92,11 +93,13 @@ def _check(fn, status):
 
 
 def dims_of(q_like, kv, layer0=0):
-    """mpc_dims from a query-like tensor [L][B][Hq][..][d] and a cache [L][B][Hkv][..][d]."""
+    """mpc_dims from a query-like tensor [L][B][Hq][..][d] and a cache [L][B][Hkv][Tcap][d]; the
+    cache's row axis is its capacity."""
     if kv.dtype not in DTYPE_CODE:
         raise TypeError(f"unsupported dtype {kv.dtype}")
+    cap = kv.shape[3] if kv.dim() == 5 else 0
     return MpcDims(batch=kv.shape[1], layer0=layer0, n_layers=kv.shape[0], n_q_heads=q_like.shape[2],
-                   n_kv_heads=kv.shape[2], head_dim=kv.shape[-1], dtype=DTYPE_CODE[kv.dtype])
+                   n_kv_heads=kv.shape[2], head_dim=kv.shape[-1], dtype=DTYPE_CODE[kv.dtype], kv_capacity=cap)
 
 
 def _contig(*ts):
@@ -125,6 +128,7 @@ def mpc_static_evict(q_win, k, v, kept_idx, k_out, v_out, *, keep, local_keep, s
     """q_win [L][B][Hq][W][d], k/v [L][B][Hkv][T][d] -> kept_idx [L][B][Hkv][keep], k_out/v_out."""
     _contig(q_win, k, v, kept_idx, k_out, v_out, token_score, row_lse, ws)
     dims = dims_of(q_win, k, layer0)
+    dims.kv_capacity = k_out.shape[3]
     T, W = k.shape[3], q_win.shape[3]
     cfg = MpcEvictCfg(window=W, keep=keep, local_keep=local_keep, sm_scale=sm_scale, causal=int(causal),
                       share_period=share_period, share_start=share_start)
@@ -150,61 +154,96 @@ def select_cfg(cluster, fanout, k_super, k_clusters, alpha=0.6, share_period=1, 
                         similarity=SIMILARITY[similarity])
 
 
-def mpc_build_clusters(k_cache, cent, scent, cfg, *, layer0=0, stream=None):
-    """k_cache [L][B][Hkv][Ts][d] -> cent [L][B][Hkv][C][R][d], scent [L][B][Hkv][S][R][d] (float32;
-    R = 2 rows r^max, r^min for the max-product bound, else 1 and the R axis may be omitted)."""
+def _slots(cap, cfg):
+    C = -(-cap // cfg.cluster_size)
+    return C, -(-C // cfg.fanout)
+
+
+def mpc_build_clusters(k_cache, cent, scent, cfg, *, Ts=None, layer0=0, stream=None):
+    """k_cache [L][B][Hkv][Tcap][d] (rows [0, Ts) used, Ts = Tcap by default) -> cent
+    [L][B][Hkv][Ccap][R][d], scent [L][B][Hkv][Scap][R][d] (float32; R = 2 rows r^max, r^min for the
+    max-product bound, else 1 and the R axis may be omitted)."""
     _contig(k_cache, cent, scent)
     dims = dims_of(k_cache, k_cache, layer0)
-    L, B, Hkv, Ts, d = k_cache.shape
-    C = -(-Ts // cfg.cluster_size)
-    S = -(-C // cfg.fanout)
+    L, B, Hkv, cap, d = k_cache.shape
+    Ts = cap if Ts is None else Ts
+    C, S = _slots(cap, cfg)
     R = 2 if cfg.similarity == SIMILARITY["maxprod"] else 1
     if cent.numel() != L * B * Hkv * C * R * d or scent.numel() != L * B * Hkv * S * R * d:
         raise ValueError(f"cent / scent must hold [L][B][Hkv][C or S][{R}][d] floats")
     if cent.dtype != torch.float32 or scent.dtype != torch.float32:
         raise TypeError("cent / scent must be float32")
     _check("mpc_build_clusters", lib().mpc_build_clusters(
-        ctypes.byref(dims), k_cache.shape[3], ctypes.byref(cfg), _ptr(k_cache), _ptr(cent), _ptr(scent),
-        _stream(stream)))
+        ctypes.byref(dims), Ts, ctypes.byref(cfg), _ptr(k_cache), _ptr(cent), _ptr(scent), _stream(stream)))
 
 
 def mpc_select_clusters(q, cent, scent, sel, cfg, *, Ts, sel_score=None, layer0=0, stream=None):
-    """q [L][B][Hq][d] -> sel [L][B][Hkv][k_clusters] (int32, ascending)."""
+    """q [L][B][Hq][d], cent / scent with Ccap / Scap slots (the first ceil(Ts / s) used) ->
+    sel [L][B][Hkv][k_clusters] (int32, ascending)."""
     _contig(q, cent, scent, sel, sel_score)
     dims = dims_of(q, cent, layer0)
     dims.head_dim = q.shape[-1]
     dims.dtype = DTYPE_CODE[q.dtype]
+    dims.kv_capacity = cent.shape[3] * cfg.cluster_size
+    if scent.shape[3] != _slots(dims.kv_capacity, cfg)[1]:
+        raise ValueError("scent must have ceil(Ccap / fanout) super-cluster slots")
     _check("mpc_select_clusters", lib().mpc_select_clusters(
         ctypes.byref(dims), Ts, ctypes.byref(cfg), _ptr(q), _ptr(cent), _ptr(scent), _ptr(sel), _ptr(sel_score),
         None, 0, _stream(stream)))
 
 
-def mpc_sparse_decode_attn(q, k_cache, v_cache, sel, out, *, cluster_size, sm_scale, lse=None, ws=None,
-                           layer0=0, stream=None):
-    """q [L][B][Hq][d], k/v [L][B][Hkv][Ts][d], sel [L][B][Hkv][k] -> out [L][B][Hq][d]."""
+def mpc_sparse_decode_attn(q, k_cache, v_cache, sel, out, *, cluster_size, sm_scale, Ts=None, n_tail=0, lse=None,
+                           ws=None, layer0=0, stream=None):
+    """q [L][B][Hq][d], k/v [L][B][Hkv][Tcap][d], sel [L][B][Hkv][k] -> out [L][B][Hq][d]. Clustered rows
+    [0, Ts) (Ts = Tcap - n_tail by default) and tail rows [Ts, Ts + n_tail)."""
     _contig(q, k_cache, v_cache, sel, out, lse, ws)
     dims = dims_of(q, k_cache, layer0)
-    Ts = k_cache.shape[3]
+    Ts = k_cache.shape[3] - n_tail if Ts is None else Ts
     if ws is None:
         ws = workspace(workspace_bytes(MPC_OP_DECODE_ATTN, dims, Ts), q.device)
     _check("mpc_sparse_decode_attn", lib().mpc_sparse_decode_attn(
-        ctypes.byref(dims), Ts, cluster_size, _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(sel), sel.shape[-1],
+        ctypes.byref(dims), Ts, n_tail, cluster_size, _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(sel), sel.shape[-1],
         sm_scale, _ptr(out), _ptr(lse), _ptr(ws), ws.numel(), _stream(stream)))
 
 
-def mpc_decode_step(q, cent, scent, k_cache, v_cache, sel, out, cfg, *, sm_scale, sel_score=None, lse=None,
-                    ws=None, layer0=0, stream=None):
+def mpc_decode_step(q, cent, scent, k_cache, v_cache, sel, out, cfg, *, sm_scale, Ts=None, n_tail=0, sel_score=None,
+                    lse=None, ws=None, layer0=0, stream=None):
     """Selection of every owner head then sparse attention of every head, in one call.
 
-    q [L][B][Hq][d], cent/scent as built, k/v [L][B][Hkv][Ts][d] -> sel [L][B][Hkv][k], out [L][B][Hq][d].
+    q [L][B][Hq][d], cent/scent as built, k/v [L][B][Hkv][Tcap][d] (clustered rows [0, Ts), Ts = Tcap - n_tail
+    by default, then the tail) -> sel [L][B][Hkv][k], out [L][B][Hq][d].
     ws must come from workspace() (zero-filled) and be reused by later calls of the same shape.
     """
     _contig(q, cent, scent, k_cache, v_cache, sel, out, sel_score, lse, ws)
     dims = dims_of(q, k_cache, layer0)
-    Ts = k_cache.shape[3]
+    Ts = k_cache.shape[3] - n_tail if Ts is None else Ts
     if ws is None:
         ws = workspace(workspace_bytes(MPC_OP_DECODE_STEP, dims, Ts, cfg), q.device)
     _check("mpc_decode_step", lib().mpc_decode_step(
-        ctypes.byref(dims), Ts, ctypes.byref(cfg), _ptr(q), _ptr(cent), _ptr(scent), _ptr(k_cache), _ptr(v_cache),
+        ctypes.byref(dims), Ts, n_tail, ctypes.byref(cfg), _ptr(q), _ptr(cent), _ptr(scent), _ptr(k_cache), _ptr(v_cache),
         sm_scale, _ptr(sel), _ptr(sel_score), _ptr(out), _ptr(lse), _ptr(ws), ws.numel(), _stream(stream)))
     return ws
+
+
+def append_state(Ts, n_tail, cluster_size):
+    """(Ts, n_tail) after one mpc_append_kv call: a full tail is sealed first, then the new row
+    joins the tail."""
+    return (Ts + cluster_size, 1) if n_tail == cluster_size else (Ts, n_tail + 1)
+
+
+def mpc_append_kv(k_new, v_new, k_cache, v_cache, cent, scent, cfg, *, Ts, n_tail, layer0=0, stream=None):
+    """Appends one decoded token: k_new / v_new [L][B][Hkv][d] into k/v [L][B][Hkv][Tcap][d] (sealing a full
+    tail into a cluster, whose representatives in cent / scent are rebuilt). Returns the new (Ts, n_tail)."""
+    _contig(k_new, v_new, k_cache, v_cache, cent, scent)
+    dims = dims_of(k_cache, k_cache, layer0)
+    if k_new.shape != k_cache.shape[:3] + k_cache.shape[4:] or v_new.shape != k_new.shape:
+        raise ValueError("k_new / v_new must be [L][B][Hkv][d] like the cache")
+    if k_new.dtype != k_cache.dtype or v_new.dtype != k_cache.dtype or v_cache.dtype != k_cache.dtype:
+        raise TypeError("k_new / v_new / v_cache must have the cache's dtype")
+    C, S = _slots(k_cache.shape[3], cfg)
+    if cent.shape[3] != C or scent.shape[3] != S:
+        raise ValueError(f"cent / scent must have {C} / {S} slots for a capacity of {k_cache.shape[3]} rows")
+    _check("mpc_append_kv", lib().mpc_append_kv(
+        ctypes.byref(dims), Ts, n_tail, ctypes.byref(cfg), _ptr(k_new), _ptr(v_new), _ptr(k_cache), _ptr(v_cache),
+        _ptr(cent), _ptr(scent), _stream(stream)))
+    return append_state(Ts, n_tail, cfg.cluster_size)

@@ -3,6 +3,7 @@
 #include <cstdarg>
 #include <cstdio>
 
+#include "append.h"
 #include "clusters.h"
 #include "common.h"
 #include "decode_attn.h"
@@ -47,6 +48,19 @@ mpc_status check_dims(const mpc_dims* d) {
     return fail(MPC_EUNSUPPORTED, "head_dim %d not in {64, 128}", d->head_dim);
   if ((int64_t)d->n_layers * d->batch * d->n_q_heads > (1 << 24))
     return fail(MPC_EUNSUPPORTED, "too many (layer, sequence, head) units");
+  if (d->kv_capacity < 0) return fail(MPC_EINVAL, "kv_capacity must be >= 0");
+  return MPC_OK;
+}
+
+// Allocated kept-cache rows per (layer, sequence, kv head): dims->kv_capacity, or the rows the call
+// uses when it is 0. Fails when the capacity is smaller than those rows.
+mpc_status cache_rows(const mpc_dims* d, int64_t used, int* rows) {
+  const int64_t cap = d->kv_capacity ? d->kv_capacity : used;
+  if (cap < used)
+    return fail(MPC_ESHAPE, "kv_capacity %d below the %lld rows in use", d->kv_capacity, (long long)used);
+  if (cap * d->head_dim * elt_size(d->dtype) > ((int64_t)1 << 31))
+    return fail(MPC_EUNSUPPORTED, "a (layer, sequence, kv head) K/V block above 2 GiB");
+  *rows = (int)cap;
   return MPC_OK;
 }
 
@@ -167,6 +181,8 @@ mpc_status mpc_static_evict(const mpc_dims* dims, int32_t T, const mpc_evict_cfg
       (int64_t)dims->n_layers * dims->batch * dims->n_kv_heads * ((T + mpc::kColBlockKeys - 1) / mpc::kColBlockKeys) >=
           ((int64_t)1 << 31))
     return fail(MPC_EUNSUPPORTED, "grid too large");
+  int out_rows = 0;
+  if ((s = cache_rows(dims, cfg->keep, &out_rows)) != MPC_OK) return s;
   const EvictWs lay = evict_ws(dims, T, cfg->window);
   if (!ws || ws_bytes < lay.total)
     return fail(MPC_EWORKSPACE, "static eviction needs %zu workspace bytes", lay.total);
@@ -189,6 +205,7 @@ mpc_status mpc_static_evict(const mpc_dims* dims, int32_t T, const mpc_evict_cfg
   a.T = T;
   a.W = cfg->window;
   a.keep = cfg->keep;
+  a.out_rows = out_rows;
   a.local_keep = cfg->local_keep;
   a.causal = cfg->causal;
   a.period = cfg->share_period;
@@ -222,6 +239,8 @@ mpc_status mpc_build_clusters(const mpc_dims* dims, int32_t Ts, const mpc_select
   if (!k_cache || !cent || !scent) return fail(MPC_EINVAL, "a required tensor pointer is NULL");
   if (!aligned16(k_cache) || !aligned16(cent) || !aligned16(scent))
     return fail(MPC_EINVAL, "tensor bases must be 16-byte aligned");
+  int rows = 0;
+  if ((s = cache_rows(dims, Ts, &rows)) != MPC_OK) return s;
   mpc::BuildArgs a{};
   a.k = k_cache;
   a.cent = cent;
@@ -235,6 +254,11 @@ mpc_status mpc_build_clusters(const mpc_dims* dims, int32_t Ts, const mpc_select
   a.f = cfg->fanout;
   a.C = ceil_div(Ts, a.s);
   a.S = ceil_div(a.C, a.f);
+  a.rows = rows;
+  a.cs = ceil_div(rows, a.s);
+  a.ss = ceil_div(a.cs, a.f);
+  a.sup0 = 0;
+  a.n_sup = a.S;
   a.period = cfg->share_period;
   a.start = cfg->share_start;
   a.alpha = cfg->alpha;
@@ -278,6 +302,8 @@ mpc_status prepare_select(const mpc_dims* dims, int32_t Ts, const mpc_select_cfg
   if (mpc::select_smem_bytes(dims->head_dim, S, cfg->k_super * cfg->fanout, qrows) > mpc::kMaxLds)
     return fail(MPC_EUNSUPPORTED, "selection sizes need more LDS than a workgroup has");
   if (dims->n_layers > mpc::kMaxLayers) return fail(MPC_EUNSUPPORTED, "at most %d layers per call", mpc::kMaxLayers);
+  int rows = 0;
+  if ((s = cache_rows(dims, Ts, &rows)) != MPC_OK) return s;
   mpc::SelectArgs a{};
   a.q = q;
   a.cent = cent;
@@ -291,6 +317,8 @@ mpc_status prepare_select(const mpc_dims* dims, int32_t Ts, const mpc_select_cfg
   a.Hkv = dims->n_kv_heads;
   a.C = C;
   a.S = S;
+  a.cs = ceil_div(rows, cfg->cluster_size);
+  a.ss = ceil_div(a.cs, cfg->fanout);
   a.f = cfg->fanout;
   a.NC = cfg->k_super * cfg->fanout;
   a.k_super = cfg->k_super;
@@ -303,7 +331,7 @@ mpc_status prepare_select(const mpc_dims* dims, int32_t Ts, const mpc_select_cfg
   return MPC_OK;
 }
 
-mpc_status prepare_decode(const mpc_dims* dims, int32_t Ts, int32_t cluster_size, const void* q,
+mpc_status prepare_decode(const mpc_dims* dims, int32_t Ts, int32_t n_tail, int32_t cluster_size, const void* q,
                           const void* k_cache, const void* v_cache, const int32_t* sel, int32_t k_clusters,
                           float sm_scale, void* out, float* lse, mpc::DecodeArgs* da, mpc::DecodePlan* plan) {
   mpc_status s = check_dims(dims);
@@ -318,12 +346,16 @@ mpc_status prepare_decode(const mpc_dims* dims, int32_t Ts, int32_t cluster_size
   if (G != 1 && G != 2 && G != 4 && G != 8) return fail(MPC_EUNSUPPORTED, "group size %d not in {1,2,4,8}", G);
   const int C = ceil_div(Ts, cluster_size);
   if (k_clusters > C) return fail(MPC_ESHAPE, "k_clusters %d > clusters %d", k_clusters, C);
-  if (k_clusters > 1024) return fail(MPC_EUNSUPPORTED, "k_clusters above 1024");
-  if ((int64_t)k_clusters * cluster_size >= ((int64_t)1 << 30)) return fail(MPC_EUNSUPPORTED, "too many tokens");
-  if ((int64_t)Ts * dims->head_dim * elt_size(dims->dtype) > ((int64_t)1 << 31))
-    return fail(MPC_EUNSUPPORTED, "a (layer, sequence, kv head) K/V block above 2 GiB");
+  if (n_tail < 0) return fail(MPC_EINVAL, "n_tail must be >= 0");
+  if (n_tail > 0 && Ts % cluster_size)
+    return fail(MPC_ESHAPE, "a tail needs Ts (%d) to be a multiple of the cluster size %d", Ts, cluster_size);
+  int rows = 0;
+  if ((s = cache_rows(dims, (int64_t)Ts + n_tail, &rows)) != MPC_OK) return s;
+  const int n_list = k_clusters + ceil_div(n_tail, cluster_size);
+  if (n_list > 1024) return fail(MPC_EUNSUPPORTED, "k_clusters plus tail clusters above 1024");
+  if ((int64_t)n_list * cluster_size >= ((int64_t)1 << 30)) return fail(MPC_EUNSUPPORTED, "too many tokens");
   const int units = dims->n_layers * dims->batch * dims->n_kv_heads;
-  *plan = mpc::decode_plan(units, k_clusters * cluster_size, dims->head_dim, elt_size(dims->dtype));
+  *plan = mpc::decode_plan(units, n_list * cluster_size, dims->head_dim, elt_size(dims->dtype));
   mpc::DecodeArgs a{};
   a.q = q;
   a.k = k_cache;
@@ -334,6 +366,8 @@ mpc_status prepare_decode(const mpc_dims* dims, int32_t Ts, int32_t cluster_size
   a.part = nullptr;
   a.cnt = nullptr;
   a.Ts = Ts;
+  a.rows = rows;
+  a.n_tail = n_tail;
   a.s = cluster_size;
   a.C = C;
   a.k_sel = k_clusters;
@@ -365,13 +399,13 @@ mpc_status mpc_select_clusters(const mpc_dims* dims, int32_t Ts, const mpc_selec
   return ok();
 }
 
-mpc_status mpc_sparse_decode_attn(const mpc_dims* dims, int32_t Ts, int32_t cluster_size,
+mpc_status mpc_sparse_decode_attn(const mpc_dims* dims, int32_t Ts, int32_t n_tail, int32_t cluster_size,
                                   const void* q, const void* k_cache, const void* v_cache,
                                   const int32_t* sel, int32_t k_clusters, float sm_scale,
                                   void* out, float* lse, void* ws, size_t ws_bytes, void* stream) {
   mpc::DecodeArgs a{};
   mpc::DecodePlan plan{};
-  mpc_status s = prepare_decode(dims, Ts, cluster_size, q, k_cache, v_cache, sel, k_clusters, sm_scale, out,
+  mpc_status s = prepare_decode(dims, Ts, n_tail, cluster_size, q, k_cache, v_cache, sel, k_clusters, sm_scale, out,
                                 lse, &a, &plan);
   if (s != MPC_OK) return s;
   const size_t need = decode_ws_bytes(dims);
@@ -390,7 +424,7 @@ mpc_status mpc_sparse_decode_attn(const mpc_dims* dims, int32_t Ts, int32_t clus
   return ok();
 }
 
-mpc_status mpc_decode_step(const mpc_dims* dims, int32_t Ts, const mpc_select_cfg* cfg,
+mpc_status mpc_decode_step(const mpc_dims* dims, int32_t Ts, int32_t n_tail, const mpc_select_cfg* cfg,
                            const void* q, const float* cent, const float* scent,
                            const void* k_cache, const void* v_cache, float sm_scale, int32_t* sel,
                            float* sel_score, void* out, float* lse, void* ws, size_t ws_bytes,
@@ -400,7 +434,7 @@ mpc_status mpc_decode_step(const mpc_dims* dims, int32_t Ts, const mpc_select_cf
   if (s != MPC_OK) return s;
   mpc::DecodeArgs da{};
   mpc::DecodePlan plan{};
-  s = prepare_decode(dims, Ts, cfg->cluster_size, q, k_cache, v_cache, sel, cfg->k_clusters, sm_scale, out, lse,
+  s = prepare_decode(dims, Ts, n_tail, cfg->cluster_size, q, k_cache, v_cache, sel, cfg->k_clusters, sm_scale, out, lse,
                      &da, &plan);
   if (s != MPC_OK) return s;
   const StepWs lay = step_ws(dims, cfg);
@@ -430,6 +464,77 @@ mpc_status mpc_decode_step(const mpc_dims* dims, int32_t Ts, const mpc_select_cf
   f.cons = (int*)((char*)ws + lay.cons);
   if ((s = launched(mpc::launch_decode_step(f, fp, dims->dtype, dims->head_dim, G, st), "decode step")) != MPC_OK)
     return s;
+  return ok();
+}
+
+mpc_status mpc_append_kv(const mpc_dims* dims, int32_t Ts, int32_t n_tail, const mpc_select_cfg* cfg,
+                         const void* k_new, const void* v_new, void* k_cache, void* v_cache,
+                         float* cent, float* scent, void* stream) {
+  mpc_status s = check_dims(dims);
+  if (s != MPC_OK) return s;
+  if (!cfg) return fail(MPC_EINVAL, "cfg is NULL");
+  if (cfg->cluster_size <= 0 || cfg->fanout <= 0) return fail(MPC_EINVAL, "cluster_size and fanout must be positive");
+  if (!(cfg->alpha >= 0.f && cfg->alpha <= 1.f)) return fail(MPC_EINVAL, "alpha must be in [0, 1]");
+  if (cfg->similarity < MPC_SIM_LINEAR || cfg->similarity > MPC_SIM_MEAN)
+    return fail(MPC_EINVAL, "unknown similarity %d", cfg->similarity);
+  if (!k_new || !v_new || !k_cache || !v_cache || !cent || !scent)
+    return fail(MPC_EINVAL, "a required tensor pointer is NULL");
+  if (!aligned16(k_new) || !aligned16(v_new) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(cent) ||
+      !aligned16(scent))
+    return fail(MPC_EINVAL, "tensor bases must be 16-byte aligned");
+  const int s_ = cfg->cluster_size;
+  if (Ts < 0 || Ts % s_) return fail(MPC_ESHAPE, "Ts %d must be a non-negative multiple of the cluster size %d", Ts, s_);
+  if (n_tail < 0 || n_tail > s_) return fail(MPC_ESHAPE, "n_tail %d not in [0, %d]", n_tail, s_);
+  if (dims->kv_capacity <= 0) return fail(MPC_EINVAL, "kv_capacity must be set for a growing cache");
+  if (dims->n_layers > mpc::kMaxLayers) return fail(MPC_EUNSUPPORTED, "at most %d layers per call", mpc::kMaxLayers);
+  const bool seal = n_tail == s_;
+  const int Ts_new = seal ? Ts + s_ : Ts;
+  const int row = seal ? Ts_new : Ts + n_tail;  // row of the new token
+  int rows = 0;
+  if ((s = cache_rows(dims, (int64_t)row + 1, &rows)) != MPC_OK) return s;
+  const int64_t units = (int64_t)dims->n_layers * dims->batch * dims->n_kv_heads;
+  hipStream_t st = (hipStream_t)stream;
+  clear_stale_error();
+  if (seal) {
+    // rebuild the new cluster and its super-cluster on owner layers (the other clusters of that
+    // super-cluster are recomputed too, to the same values)
+    mpc::BuildArgs a{};
+    a.k = k_cache;
+    a.cent = cent;
+    a.scent = scent;
+    a.B = dims->batch;
+    a.layer0 = dims->layer0;
+    a.n_layers = dims->n_layers;
+    a.Hkv = dims->n_kv_heads;
+    a.Ts = Ts_new;
+    a.s = s_;
+    a.f = cfg->fanout;
+    a.C = Ts_new / s_;
+    a.S = ceil_div(a.C, a.f);
+    a.rows = rows;
+    a.cs = ceil_div(rows, s_);
+    a.ss = ceil_div(a.cs, a.f);
+    a.sup0 = (a.C - 1) / a.f;
+    a.n_sup = 1;
+    a.period = cfg->share_period;
+    a.start = cfg->share_start;
+    a.alpha = cfg->alpha;
+    a.beta = (float)(1.0 - (double)cfg->alpha);
+    a.similarity = cfg->similarity;
+    a.own = mpc::owner_table(a.layer0, a.n_layers, a.period, a.start);
+    if (a.own.n > 0 && (s = launched(mpc::launch_build(a, dims->dtype, dims->head_dim, st), "seal")) != MPC_OK)
+      return s;
+  }
+  mpc::AppendArgs ap{};
+  ap.k_new = k_new;
+  ap.v_new = v_new;
+  ap.k = k_cache;
+  ap.v = v_cache;
+  ap.units = units;
+  ap.rows = rows;
+  ap.row = row;
+  ap.row_bytes = dims->head_dim * elt_size(dims->dtype);
+  if ((s = launched(mpc::launch_append_rows(ap, st), "append")) != MPC_OK) return s;
   return ok();
 }
 

@@ -2,10 +2,12 @@
 // per-channel max / min folded into alpha * r^max + (1 - alpha) * r^min (linear form), or the
 // two bound rows (max-product bound), or the average (fp64 sums, one rounding to fp32).
 //
-// One workgroup per (owner layer, sequence, kv head, super-cluster). Each wave streams the rows of
-// one fine cluster at a time with coalesced 16-byte loads (LPR lanes per row), reduces max / min
-// over its row groups with cross-lane shuffles, writes the fine representative and folds the
-// bounds into its super-cluster bounds; the waves' super bounds meet in LDS. Max / min are exact,
+// One workgroup per (owner layer, sequence, kv head, super-cluster), over all super-clusters or,
+// when a decode-time tail is sealed into a new cluster, over the one super-cluster that holds it.
+// Each wave streams the rows of one fine cluster at a time with coalesced 16-byte loads (LPR
+// lanes per row), reduces max / min over its row groups with cross-lane shuffles, writes the fine
+// representative and folds the bounds into its super-cluster bounds; the waves' super bounds meet
+// in LDS. Max / min are exact,
 // the linear representative is two fp32 products and one fp32 sum with no contraction, and the
 // average's fp64 sums of 16-bit keys are exact, so their order does not matter.
 #include "clusters.h"
@@ -24,13 +26,13 @@ __global__ __launch_bounds__(NW* kWave) void k_build(BuildArgs a) {
   __shared__ float s_max[NW][D], s_min[NW][D];
   __shared__ double s_sum[MEAN ? NW : 1][MEAN ? D : 1];
 
-  const int sup = blockIdx.x % a.S;
-  const int ou = blockIdx.x / a.S;  // (owner index * B + b) * Hkv + h
+  const int sup = a.sup0 + blockIdx.x % a.n_sup;
+  const int ou = blockIdx.x / a.n_sup;  // (owner index * B + b) * Hkv + h
   const int l = a.own.l[ou / (a.B * a.Hkv)];
   const size_t unit = (size_t)l * a.B * a.Hkv + ou % (a.B * a.Hkv);
   const int tid = threadIdx.x, lane = tid % kWave, w = tid / kWave;
   const int rg = lane / LPR, li = lane % LPR;
-  const char* kh = (const char*)a.k + (size_t)unit * a.Ts * D * DT::kElt;
+  const char* kh = (const char*)a.k + (size_t)unit * a.rows * D * DT::kElt;
 
   float smax[EPL], smin[EPL];
   double ssum[EPL];
@@ -77,7 +79,7 @@ __global__ __launch_bounds__(NW* kWave) void k_build(BuildArgs a) {
       }
     }
     if (rg == 0) {
-      float* out = a.cent + ((size_t)unit * a.C + c) * R * D + li * EPL;
+      float* out = a.cent + ((size_t)unit * a.cs + c) * R * D + li * EPL;
 #pragma unroll
       for (int e = 0; e < EPL; ++e) {
         if constexpr (SIM == MPC_SIM_LINEAR) {
@@ -113,7 +115,7 @@ __global__ __launch_bounds__(NW* kWave) void k_build(BuildArgs a) {
   }
   __syncthreads();
   const int n_tok = min(a.Ts, c_end * a.s) - sup * a.f * a.s;  // tokens of the super-cluster
-  float* sout = a.scent + ((size_t)unit * a.S + sup) * R * D;
+  float* sout = a.scent + ((size_t)unit * a.ss + sup) * R * D;
   for (int i = tid; i < D; i += NW * kWave) {
     if constexpr (MEAN) {
       double sum = 0.0;
@@ -162,7 +164,7 @@ hipError_t launch_dt(const BuildArgs& a, int D, int blocks, hipStream_t st) {
 }  // namespace
 
 hipError_t launch_build(const BuildArgs& a, int dtype, int D, hipStream_t st) {
-  const int blocks = a.own.n * a.B * a.Hkv * a.S;
+  const int blocks = a.own.n * a.B * a.Hkv * a.n_sup;
   switch (dtype) {
     case MPC_FP32: return launch_dt<F32>(a, D, blocks, st);
     case MPC_FP16: return launch_dt<F16>(a, D, blocks, st);

@@ -8,6 +8,29 @@ namespace dev {
 
 constexpr int kMaxSel = 1024;
 
+// The unit's cluster list in LDS: its selected clusters, with ids outside [0, C) replaced by -1
+// (they contribute nothing), then the clusters C, C + 1, ... that hold the tail rows
+// [Ts, Ts + n_tail) (Ts is a multiple of s when there is a tail). Returns the list length.
+// COH_SEL: the selection was written by another workgroup of the same launch, so it is read with
+// device-coherent loads.
+template <int NW, bool COH_SEL>
+__device__ __forceinline__ int load_list(const DecodeArgs& a, int unit, int32_t* s_sel) {
+  const int n_list = a.k_sel + (a.n_tail + a.s - 1) / a.s;
+  for (int i = threadIdx.x; i < n_list; i += NW * kWave) {
+    int c = a.C + (i - a.k_sel);
+    if (i < a.k_sel) {
+      const int32_t* src = a.sel + (size_t)unit * a.k_sel + i;
+      if constexpr (COH_SEL)
+        c = __hip_atomic_load(src, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      else
+        c = *src;
+      if ((unsigned)c >= (unsigned)a.C) c = -1;
+    }
+    s_sel[i] = c;
+  }
+  return n_list;
+}
+
 // Cross-wave merge of one unit's (m, l, acc) from LDS, then the output (one split) or the split-K
 // partial and, for the last split to arrive, the merge of all partials.
 template <class DT, int D, int G, int NW>
@@ -92,13 +115,7 @@ __device__ __forceinline__ void attend_unit(const DecodeArgs& a, int unit, int s
   const int tid = threadIdx.x, lane = tid % kWave, w = tid / kWave;
   const int rg = lane / LPR, li = lane % LPR;
 
-  for (int i = tid; i < a.k_sel; i += NW * kWave) {
-    const int32_t* src = a.sel + (size_t)unit * a.k_sel + i;
-    if constexpr (COH_SEL)
-      s_sel[i] = __hip_atomic_load(src, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    else
-      s_sel[i] = *src;
-  }
+  const int n_list = load_list<NW, COH_SEL>(a, unit, s_sel);
 
   // unit = (l * B + b) * Hkv + h ; q-heads h*G .. h*G+G-1 of the same (l, b)
   const size_t q_row0 = (size_t)(unit / a.Hkv) * a.Hq + (size_t)(unit % a.Hkv) * G;
@@ -118,11 +135,11 @@ __device__ __forceinline__ void attend_unit(const DecodeArgs& a, int unit, int s
   }
   __syncthreads();
 
-  const int n_slot = a.k_sel * a.s;
+  const int n_slot = n_list * a.s, rows_end = a.Ts + a.n_tail;
   const int chunk = (n_slot + a.splits - 1) / a.splits;
   const int lo = split * chunk, hi = min(n_slot, lo + chunk);
-  const char* kbase = (const char*)a.k + (size_t)unit * a.Ts * D * DT::kElt;
-  const char* vbase = (const char*)a.v + (size_t)unit * a.Ts * D * DT::kElt;
+  const char* kbase = (const char*)a.k + (size_t)unit * a.rows * D * DT::kElt;
+  const char* vbase = (const char*)a.v + (size_t)unit * a.rows * D * DT::kElt;
 
   float m[G], l[G], acc[G][EPL];
 #pragma unroll
@@ -149,12 +166,12 @@ __device__ __forceinline__ void attend_unit(const DecodeArgs& a, int unit, int s
   auto fetch = [&](int base, uint4 (&kr)[U], uint4 (&vr)[U], bool (&ok)[U]) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      // ids come from the caller, so anything outside [0, C) or past the kept length contributes
-      // nothing (and loads row 0 harmlessly)
+      // a masked slot (past the list, a rejected id, past the cached rows) contributes nothing
+      // and loads row 0 harmlessly
       const int sl = base + (u * NW + w) * RPW + rg;
-      const int c = s_sel[min(cpos[u], a.k_sel - 1)];
+      const int c = s_sel[min(cpos[u], n_list - 1)];
       const int r = c * a.s + crow[u];
-      ok[u] = (sl < hi) & ((unsigned)c < (unsigned)a.C) & (r < a.Ts);
+      ok[u] = (sl < hi) & (c >= 0) & (r < rows_end);
       const unsigned off = (unsigned)(ok[u] ? r : 0) * (unsigned)(D * DT::kElt) + (unsigned)(li * 16);
       kr[u] = ldg16(kbase + off);
       vr[u] = ldg16(vbase + off);
@@ -309,13 +326,7 @@ __device__ __forceinline__ void attend_unit_g4(const DecodeArgs& a, int unit, in
   const int tk = lane % 16, kq = lane / 16;    // score layout: token of the 16, quarter of a 32-wide k step
   const int rg = lane / LPR, li = lane % LPR;  // row layout: row of the load, 16-byte column
 
-  for (int i = tid; i < a.k_sel; i += NW * kWave) {
-    const int32_t* src = a.sel + (size_t)unit * a.k_sel + i;
-    if constexpr (COH_SEL)
-      s_sel[i] = __hip_atomic_load(src, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    else
-      s_sel[i] = *src;
-  }
+  const int n_list = load_list<NW, COH_SEL>(a, unit, s_sel);
   const size_t q_row0 = (size_t)(unit / a.Hkv) * a.Hq + (size_t)(unit % a.Hkv) * G;
   uint4 qa[KK];  // A operand: row tk holds head tk % 4
 #pragma unroll
@@ -323,11 +334,11 @@ __device__ __forceinline__ void attend_unit_g4(const DecodeArgs& a, int unit, in
     qa[kk] = ldg16((const char*)a.q + ((q_row0 + tk % G) * D + kk * 32 + kq * 8) * DT::kElt);
   __syncthreads();
 
-  const int n_slot = a.k_sel * a.s;
+  const int n_slot = n_list * a.s, rows_end = a.Ts + a.n_tail;
   const int chunk = (n_slot + a.splits - 1) / a.splits;
   const int lo = split * chunk, hi = min(n_slot, lo + chunk);
-  const char* kbase = (const char*)a.k + (size_t)unit * a.Ts * D * DT::kElt;
-  const char* vbase = (const char*)a.v + (size_t)unit * a.Ts * D * DT::kElt;
+  const char* kbase = (const char*)a.k + (size_t)unit * a.rows * D * DT::kElt;
+  const char* vbase = (const char*)a.v + (size_t)unit * a.rows * D * DT::kElt;
 
   // slot cursors (cluster position, row), advanced by STEP slots per step without a division:
   // [0] the score-layout token of this lane, [1 + u] its row-layout rows
@@ -341,9 +352,9 @@ __device__ __forceinline__ void attend_unit_g4(const DecodeArgs& a, int unit, in
   const int step_pos = STEP / a.s, step_row = STEP % a.s;
   // row of cursor j at step `base`; invalid slots read row 0 and are masked
   auto row_of = [&](int j, int sl, bool& ok) {
-    const int c = s_sel[min(cpos[j], a.k_sel - 1)];
+    const int c = s_sel[min(cpos[j], n_list - 1)];
     const int r = c * a.s + crow[j];
-    ok = (sl < hi) & ((unsigned)c < (unsigned)a.C) & (r < a.Ts);
+    ok = (sl < hi) & (c >= 0) & (r < rows_end);
     crow[j] += step_row;
     cpos[j] += step_pos;
     if (crow[j] >= a.s) {

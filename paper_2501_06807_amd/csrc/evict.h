@@ -14,12 +14,13 @@ struct EvictArgs {
   const void* k;       // [L][B][Hkv][T][d]
   const void* v;
   int32_t* kept;       // [L][B][Hkv][keep]
-  void* k_out;         // [L][B][Hkv][keep][d]
+  void* k_out;         // [L][B][Hkv][out_rows][d], rows [0, keep) written
   void* v_out;
   float* score;        // [L][B][Hkv][T] accumulated attention (token_score or workspace)
   double* rowstat;     // [L][B][Hq][W]: -(c * max + log2(sum)) per window row
   float* row_lse;      // [L][B][Hq][W] natural log-sum-exp, optional
   int B, layer0, n_layers, Hq, Hkv, T, W, keep, local_keep, causal, period, start;
+  int out_rows;        // row capacity of k_out / v_out per (layer, sequence, kv head)
   OwnerTable own;      // owner layers of the block
   float c_hi, c_lo;    // sm_scale * log2(e) as an unevaluated fp32 sum
   double c64;          // the same in fp64

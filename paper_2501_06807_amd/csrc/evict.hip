@@ -445,7 +445,7 @@ __global__ __launch_bounds__(256) void k_gather(EvictArgs a) {
     if (src_l != l && c16 == 0) a.kept[unit * a.keep + i] = idx;
     idx = min(max(idx, 0), a.T - 1);  // indices supplied by the caller are clamped into the cache
     const size_t so = (unit * a.T + idx) * RB + c16 * 16;
-    const size_t dst = (unit * a.keep + i) * RB + c16 * 16;
+    const size_t dst = (unit * a.out_rows + i) * RB + c16 * 16;
     *(uint4*)((char*)a.k_out + dst) = ldg16((const char*)a.k + so);
     *(uint4*)((char*)a.v_out + dst) = ldg16((const char*)a.v + so);
   }

@@ -9,12 +9,13 @@ constexpr int kSelMaxCand = 1024;   // k_super * fanout limit (LDS)
 
 struct SelectArgs {
   const void* q;        // [L][B][Hq][d]
-  const float* cent;    // [L][B][Hkv][C][d]
-  const float* scent;   // [L][B][Hkv][S][d]
+  const float* cent;    // [L][B][Hkv][cs][R][d], the first C slots used
+  const float* scent;   // [L][B][Hkv][ss][R][d], the first S slots used
   int32_t* sel;         // [L][B][Hkv][k_clusters]
   float* sel_score;     // same or null
   int B, layer0, n_layers, Hq, Hkv;
   int C, S, f, NC, k_super, k_clusters;  // NC = k_super * f
+  int cs, ss;                            // allocated cluster / super-cluster slots per head
   int period, start;
   int similarity;  // mpc_similarity: representatives of 2 rows (r^max, r^min) for the bound
   OwnerTable own;  // owner layers of the block (one workgroup per owner head)

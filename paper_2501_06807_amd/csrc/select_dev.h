@@ -301,8 +301,8 @@ __device__ void select_block(const SelectArgs& a, int ou, unsigned char* smem) {
   const size_t unit = (size_t)l * BH + ou % BH;
   const int abs_l = a.layer0 + l;
   const int tid = threadIdx.x, w = tid / kWave;
-  const float* scent = a.scent + unit * a.S * SC::RW;
-  const float* cent = a.cent + unit * a.C * SC::RW;
+  const float* scent = a.scent + unit * a.ss * SC::RW;
+  const float* cent = a.cent + unit * a.cs * SC::RW;
 
   // the first level-1 tile is in flight while the query rows are loaded
   typename SC::Tile tile;
@@ -445,8 +445,8 @@ __device__ void select_waves(const SelectArgs& a, int ou0, unsigned char* smem) 
   const int l = a.own.l[ou / BH], b = (ou / a.Hkv) % a.B, h = ou % a.Hkv;
   const size_t unit = (size_t)l * BH + ou % BH;
   const int abs_l = a.layer0 + l;
-  const float* scent = a.scent + unit * a.S * SC::RW;
-  const float* cent = a.cent + unit * a.C * SC::RW;
+  const float* scent = a.scent + unit * a.ss * SC::RW;
+  const float* cent = a.cent + unit * a.cs * SC::RW;
 
   // the first level-1 tile is in flight while the query rows are loaded
   typename SC::Tile tile;

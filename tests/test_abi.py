@@ -91,18 +91,18 @@ def test_unknown_similarity_is_rejected_before_any_launch():
 
 def test_decode_validation_and_workspace():
     d = _dims(n_layers=1, n_q_heads=8, n_kv_heads=8)
-    s, _ = _status("mpc_sparse_decode_attn", ctypes.byref(d), 256, 16, FAKE, FAKE, FAKE, FAKE, 17, 0.1,
+    s, _ = _status("mpc_sparse_decode_attn", ctypes.byref(d), 256, 0, 16, FAKE, FAKE, FAKE, FAKE, 17, 0.1,
                    FAKE, None, None, 0, None)
     assert s == L.MPC_ESHAPE  # 17 clusters > C = 16
     d3 = _dims(n_layers=1, n_q_heads=24, n_kv_heads=8)
-    s, _ = _status("mpc_sparse_decode_attn", ctypes.byref(d3), 256, 16, FAKE, FAKE, FAKE, FAKE, 4, 0.1,
+    s, _ = _status("mpc_sparse_decode_attn", ctypes.byref(d3), 256, 0, 16, FAKE, FAKE, FAKE, FAKE, 4, 0.1,
                    FAKE, None, None, 0, None)
     assert s == L.MPC_EUNSUPPORTED  # group of 3
     # few units and enough tokens -> split-K -> a workspace is required (validation fails before
     # any launch, so the fake pointers are never used)
     need = L.workspace_bytes(L.MPC_OP_DECODE_ATTN, d, 256)
     assert need > 0
-    s, msg = _status("mpc_sparse_decode_attn", ctypes.byref(d), 256, 16, FAKE, FAKE, FAKE, FAKE, 16, 0.1,
+    s, msg = _status("mpc_sparse_decode_attn", ctypes.byref(d), 256, 0, 16, FAKE, FAKE, FAKE, FAKE, 16, 0.1,
                      FAKE, None, None, 0, None)
     assert s == L.MPC_EWORKSPACE and str(need) in msg
     # many units -> no split -> no workspace
@@ -118,7 +118,7 @@ def test_decode_step_validation_and_workspace():
     assert owners == 10
     assert need >= 16 + owners * 4 * 32 * 4  # counters + one flag per owner head
     call = lambda d, c, ws, nb: _status(
-        "mpc_decode_step", ctypes.byref(d), 9824, ctypes.byref(c), FAKE, FAKE, FAKE, FAKE, FAKE, 0.088, FAKE,
+        "mpc_decode_step", ctypes.byref(d), 9824, 0, ctypes.byref(c), FAKE, FAKE, FAKE, FAKE, FAKE, 0.088, FAKE,
         None, FAKE, None, ws, nb, None)
     s, msg = call(big, cfg, None, 0)
     assert s == L.MPC_EWORKSPACE and str(need) in msg
@@ -161,3 +161,46 @@ def test_status_strings():
     lib = L.lib()
     for s in range(6):
         assert lib.mpc_status_string(s)
+
+
+def test_append_validation():
+    cfg = L.select_cfg(16, 4, 2, 4)
+    call = lambda d, Ts, nt, c=cfg: _status("mpc_append_kv", ctypes.byref(d), Ts, nt, ctypes.byref(c), FAKE, FAKE,
+                                            FAKE, FAKE, FAKE, FAKE, None)
+    d = _dims(kv_capacity=300)
+    s, msg = call(d, 250, 3)
+    assert s == L.MPC_ESHAPE and "multiple" in msg      # Ts not a multiple of s
+    assert call(d, 256, 17)[0] == L.MPC_ESHAPE            # tail longer than a cluster
+    assert call(d, 256, -1)[0] == L.MPC_ESHAPE
+    assert call(_dims(), 256, 3)[0] == L.MPC_EINVAL       # no capacity given
+    # 288 + 12 = 300 rows in use: no row left for the new token
+    s, msg = call(d, 288, 12)
+    assert s == L.MPC_ESHAPE and "kv_capacity" in msg
+    # a full tail at 272 + 16 is sealed first, and the new row 288 still fits
+    bad = L.select_cfg(16, 4, 2, 4)
+    bad.similarity = 5
+    assert call(d, 272, 16, bad)[0] == L.MPC_EINVAL
+    s, _ = _status("mpc_append_kv", ctypes.byref(d), 272, 16, ctypes.byref(cfg), None, FAKE, FAKE, FAKE, FAKE, FAKE,
+                   None)
+    assert s == L.MPC_EINVAL                               # k_new is NULL
+
+
+def test_capacity_and_tail_validation():
+    d = _dims(n_layers=1, n_q_heads=8, n_kv_heads=8)
+    attn = lambda dd, Ts, nt, k=4: _status("mpc_sparse_decode_attn", ctypes.byref(dd), Ts, nt, 16, FAKE, FAKE,
+                                           FAKE, FAKE, k, 0.1, FAKE, None, None, 0, None)
+    assert attn(d, 250, 3)[0] == L.MPC_ESHAPE             # a tail after a partial cluster
+    assert attn(d, 256, -2)[0] == L.MPC_EINVAL
+    assert attn(_dims(n_layers=1, n_q_heads=8, n_kv_heads=8, kv_capacity=260), 256, 5)[0] == L.MPC_ESHAPE
+    assert attn(_dims(n_layers=1, n_q_heads=8, n_kv_heads=8, kv_capacity=-1), 256, 0)[0] == L.MPC_EINVAL
+    big = _dims(n_layers=1, n_q_heads=8, n_kv_heads=8, kv_capacity=20000)
+    assert attn(big, 16000, 16 * 30, k=1000)[0] == L.MPC_EUNSUPPORTED  # 1000 + 30 list entries
+    cfg = L.select_cfg(16, 4, 2, 4)
+    s, msg = _status("mpc_build_clusters", ctypes.byref(_dims(kv_capacity=200)), 256, ctypes.byref(cfg), FAKE,
+                     FAKE, FAKE, None)
+    assert s == L.MPC_ESHAPE and "kv_capacity" in msg
+    ecfg = L.MpcEvictCfg(window=100, keep=200, local_keep=32, sm_scale=0.088, causal=1, share_period=1,
+                         share_start=2)
+    s, msg = _status("mpc_static_evict", ctypes.byref(_dims(kv_capacity=150)), 1000, ctypes.byref(ecfg), FAKE, FAKE,
+                     FAKE, FAKE, FAKE, FAKE, None, None, FAKE, 1 << 30, None)
+    assert s == L.MPC_ESHAPE and "kv_capacity" in msg

@@ -485,6 +485,73 @@ def test_sparse_attention_gathers_selected_clusters_with_partial_tail():
         np.testing.assert_allclose(out[0, 0, h], ref, rtol=1e-12, atol=1e-13)
 
 
+# ------------------------------------------------------------------------ decode-time growth (App. A.3)
+def test_tail_rows_join_the_attended_tokens():
+    # clusters 0 and 2 of Ts = 32 (s = 8) plus a tail of 5 appended rows: softmax attention over
+    # exactly those 21 rows, checked against torch's attention on the gathered rows
+    L, B, Hq, Hkv, Ts, n_tail, d, s = 1, 2, 4, 2, 32, 5, 8, 8
+    r = rng(31)
+    k = to_bits(r.standard_normal((L, B, Hkv, Ts + n_tail, d)), "fp16")
+    v = to_bits(r.standard_normal((L, B, Hkv, Ts + n_tail, d)), "fp16")
+    q = to_bits(r.standard_normal((L, B, Hq, d)), "fp16")
+    sel = np.tile(np.array([0, 2], np.int32), (L, B, Hkv, 1))
+    out, lse = oracle.sparse_decode_attn(q, k, v, sel, "fp16", cluster=s, sm_scale=0.4, n_tail=n_tail)
+    rows = list(range(0, 8)) + list(range(16, 24)) + list(range(32, 37))
+    qf, kf, vf = (from_bits(x, "fp16") for x in (q, k, v))
+    sm32 = float(np.float32(0.4))
+    for b in range(B):
+        for h in range(Hq):
+            kk, vv = kf[0, b, h // 2, rows], vf[0, b, h // 2, rows]
+            np.testing.assert_allclose(out[0, b, h], _sdpa(qf[0, b, h], kk, vv, sm32), rtol=1e-12, atol=1e-13)
+            lref = torch.logsumexp(torch.from_numpy(sm32 * kk @ qf[0, b, h]), 0).item()
+            assert abs(lse[0, b, h] - lref) < 1e-12
+
+
+def test_full_budget_with_tail_is_dense_attention_over_the_grown_cache():
+    # every cluster selected + the tail = the decode attention of App. A.3 over the whole cache
+    L, B, Hq, Hkv, Ts, n_tail, d, s = 2, 1, 2, 2, 24, 7, 8, 8
+    r = rng(32)
+    k = to_bits(r.standard_normal((L, B, Hkv, Ts + n_tail, d)), "bf16")
+    v = to_bits(r.standard_normal((L, B, Hkv, Ts + n_tail, d)), "bf16")
+    q = to_bits(r.standard_normal((L, B, Hq, d)), "bf16")
+    sel = np.tile(np.arange(3, dtype=np.int32), (L, B, Hkv, 1))
+    sp, lse_s = oracle.sparse_decode_attn(q, k, v, sel, "bf16", cluster=s, sm_scale=0.3, n_tail=n_tail)
+    dn, lse_d = oracle.dense_decode_attn(q, k, v, "bf16", sm_scale=0.3)
+    np.testing.assert_allclose(sp, dn, rtol=1e-13, atol=1e-14)
+    np.testing.assert_allclose(lse_s, lse_d, rtol=1e-13)
+
+
+@pytest.mark.parametrize("s", [1, 4, 16])
+def test_append_state_walk(s):
+    # from (Ts0, 0), n appends leave Ts0 + n rows, the newest n_tail in [1, s] of them unclustered,
+    # and the clustered count a multiple of s above Ts0: clusters are sealed only when full
+    Ts0 = 3 * s
+    Ts, nt = Ts0, 0
+    for n in range(1, 5 * s + 3):
+        Ts, nt = oracle.append_state(Ts, nt, s)
+        assert Ts + nt == Ts0 + n
+        assert 1 <= nt <= s
+        assert Ts == Ts0 + s * ((n - 1) // s)
+    with pytest.raises(oracle.OracleError):
+        oracle.append_state(0, s + 1, s)
+
+
+def test_sealed_cluster_is_the_cluster_of_the_longer_cache():
+    # sealing is the cluster build over the first Ts + s rows: the earlier clusters and the
+    # super-clusters that do not hold the new cluster keep their representatives
+    L, B, Hkv, d, s, f = 1, 1, 1, 8, 4, 2
+    r = rng(33)
+    k = to_bits(r.standard_normal((L, B, Hkv, 28, d)), "bf16")
+    before = oracle.build_clusters(k[:, :, :, :20], "bf16", cluster=s, fanout=f)   # C = 5, S = 3
+    after = oracle.build_clusters(k[:, :, :, :24], "bf16", cluster=s, fanout=f)    # C = 6, S = 3
+    np.testing.assert_array_equal(after[0][..., :5, :], before[0])
+    np.testing.assert_array_equal(after[1][..., :2, :], before[1][..., :2, :])
+    # the grown super-cluster 2 now bounds clusters 4 and 5
+    kf = from_bits(k, "bf16")[0, 0, 0, 16:24]
+    np.testing.assert_array_equal(after[1][0, 0, 0, 2], [oracle.centroid(hi, lo, 0.6) for hi, lo in
+                                                         zip(kf.max(axis=0), kf.min(axis=0))])
+
+
 # ------------------------------------------------------------------------ whole static eviction
 def test_static_evict_identity_sharing_and_gather():
     L, B, Hq, Hkv, T, W, d = 4, 1, 4, 2, 48, 9, 8
