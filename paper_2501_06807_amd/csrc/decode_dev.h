@@ -115,8 +115,6 @@ __device__ __forceinline__ void attend_unit(const DecodeArgs& a, int unit, int s
   const int tid = threadIdx.x, lane = tid % kWave, w = tid / kWave;
   const int rg = lane / LPR, li = lane % LPR;
 
-  const int n_list = load_list<NW, COH_SEL>(a, unit, s_sel);
-
   // unit = (l * B + b) * Hkv + h ; q-heads h*G .. h*G+G-1 of the same (l, b)
   const size_t q_row0 = (size_t)(unit / a.Hkv) * a.Hq + (size_t)(unit % a.Hkv) * G;
   // 16-bit types: q stays packed and the dot products use the two-wide dot instructions (exact
@@ -133,6 +131,8 @@ __device__ __forceinline__ void attend_unit(const DecodeArgs& a, int unit, int s
       for (int e = 0; e < EPL; ++e) qf[g][e] = t[e] * a.qscale;
     }
   }
+  // the cluster list after the query loads, so that both are in flight together
+  const int n_list = load_list<NW, COH_SEL>(a, unit, s_sel);
   __syncthreads();
 
   const int n_slot = n_list * a.s, rows_end = a.Ts + a.n_tail;
@@ -326,12 +326,13 @@ __device__ __forceinline__ void attend_unit_g4(const DecodeArgs& a, int unit, in
   const int tk = lane % 16, kq = lane / 16;    // score layout: token of the 16, quarter of a 32-wide k step
   const int rg = lane / LPR, li = lane % LPR;  // row layout: row of the load, 16-byte column
 
-  const int n_list = load_list<NW, COH_SEL>(a, unit, s_sel);
   const size_t q_row0 = (size_t)(unit / a.Hkv) * a.Hq + (size_t)(unit % a.Hkv) * G;
   uint4 qa[KK];  // A operand: row tk holds head tk % 4
 #pragma unroll
   for (int kk = 0; kk < KK; ++kk)
     qa[kk] = ldg16((const char*)a.q + ((q_row0 + tk % G) * D + kk * 32 + kq * 8) * DT::kElt);
+  // the cluster list after the query loads, so that both are in flight together
+  const int n_list = load_list<NW, COH_SEL>(a, unit, s_sel);
   __syncthreads();
 
   const int n_slot = n_list * a.s, rows_end = a.Ts + a.n_tail;

@@ -59,8 +59,9 @@ __global__ __launch_bounds__(kFusedWaves* kWave) void k_decode_step(FusedArgs f)
   __syncthreads();
   const int mode = s_mode;
   if (mode == 1) {
-    // one row pass in flight per wave keeps the selection's registers near the attention's
-    dev::select_block<DT, D, kFusedWaves, true, 1, MP>(sa, head, smem);
+    // one row pass in flight per wave and the query in LDS keep the selection's registers near
+    // the attention's
+    dev::select_block<DT, D, kFusedWaves, true, 1, MP, false>(sa, head, smem);
     __builtin_amdgcn_s_waitcnt(0);  // this thread's selection stores have completed
     __syncthreads();
     if (tid == 0) __hip_atomic_store(&f.state[head], 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);

@@ -40,14 +40,64 @@ __device__ __forceinline__ void tile_load(const float* M, const int* idx, int n,
   }
 }
 
-// Reduces a loaded tile against qsum (LDS, fp64) and writes scores[r], img[r] = key_hi(score) and
-// the composite key ck[r] of its rows.
 __device__ __forceinline__ uint32_t key_hi(double x);
 __device__ __forceinline__ unsigned long long rank_key(uint32_t img, int i);
 
+// The lane's share of the summed query, held in registers for every row it reduces: floats
+// c*16 + 4k .. +3 (k = lane % 4) of each 16-float step, in fp64.
+template <int D>
+struct QReg {
+  double v[D / 16][4];
+};
+
+template <int D>
+__device__ __forceinline__ void qreg_load(const double* qsum, QReg<D>& q) {
+  const int qk = threadIdx.x & 3;
+#pragma unroll
+  for (int c = 0; c < D / 16; ++c) {
+    const double2 a = *(const double2*)(qsum + c * 16 + qk * 4);
+    const double2 b = *(const double2*)(qsum + c * 16 + qk * 4 + 2);
+    q.v[c][0] = a.x;
+    q.v[c][1] = a.y;
+    q.v[c][2] = b.x;
+    q.v[c][3] = b.y;
+  }
+}
+
+// Writes the score of row r (quad lane 0): scores[r], img[r] = key_hi(score), the composite key
+// ck[r].
+__device__ __forceinline__ void put_score(double acc, bool valid, int r, int n, double* scores, uint32_t* img,
+                                          unsigned long long* ck) {
+  if ((threadIdx.x & 3) == 0 && r < n) {
+    const double sc = valid ? acc : -INFINITY;
+    scores[r] = sc;
+    img[r] = key_hi(sc);
+    ck[r] = rank_key(img[r], r);
+  }
+}
+
+// Reduces a loaded tile against the summed query held in registers and writes the scores of its
+// rows.
 template <int D, int PASS>
-__device__ __forceinline__ void tile_dot(const RowTile<D, PASS>& t, int n, int r0, const double* qsum,
+__device__ __forceinline__ void tile_dot(const RowTile<D, PASS>& t, int n, int r0, const QReg<D>& q,
                                          double* scores, uint32_t* img, unsigned long long* ck) {
+  constexpr int ROWS = kWave / 4;
+  const int rq = (threadIdx.x % kWave) >> 2;
+#pragma unroll
+  for (int p = 0; p < PASS; ++p) {
+    double acc = 0.0;
+#pragma unroll
+    for (int c = 0; c < D / 16; ++c)
+      acc += q.v[c][0] * (double)t.x[p][c].x + q.v[c][1] * (double)t.x[p][c].y + q.v[c][2] * (double)t.x[p][c].z +
+             q.v[c][3] * (double)t.x[p][c].w;
+    put_score(group_sum<4>(acc), t.valid[p], r0 + p * ROWS + rq, n, scores, img, ck);
+  }
+}
+
+// The same with the summed query read from LDS at every row (fewer registers).
+template <int D, int PASS>
+__device__ __forceinline__ void tile_dot_lds(const RowTile<D, PASS>& t, int n, int r0, const double* qsum,
+                                             double* scores, uint32_t* img, unsigned long long* ck) {
   constexpr int ROWS = kWave / 4;
   const int lane = threadIdx.x % kWave, rq = lane >> 2, qk = lane & 3;
 #pragma unroll
@@ -60,14 +110,7 @@ __device__ __forceinline__ void tile_dot(const RowTile<D, PASS>& t, int n, int r
       acc += q01.x * (double)t.x[p][c].x + q01.y * (double)t.x[p][c].y + q23.x * (double)t.x[p][c].z +
              q23.y * (double)t.x[p][c].w;
     }
-    acc = group_sum<4>(acc);
-    const int r = r0 + p * ROWS + rq;
-    if (qk == 0 && r < n) {
-      const double sc = t.valid[p] ? acc : -INFINITY;
-      scores[r] = sc;
-      img[r] = key_hi(sc);
-      ck[r] = rank_key(img[r], r);
-    }
+    put_score(group_sum<4>(acc), t.valid[p], r0 + p * ROWS + rq, n, scores, img, ck);
   }
 }
 
@@ -104,19 +147,35 @@ __device__ __forceinline__ void tile_dot_mp(const RowTile<2 * D, PASS>& t, int n
   }
 }
 
-// Scoring of one mode: dot-product modes (linear, average) take the group's summed query, the
-// max-product bound the G separate queries and two-row representatives (one row pass in flight).
-template <int D, int PASS, bool MP>
+// Scoring of one mode: dot-product modes (linear, average) take the group's summed query (from
+// registers if QREG, else from LDS), the max-product bound the G separate queries (LDS) and
+// two-row representatives (one row pass in flight).
+template <int D, int PASS, bool MP, bool QREG = true>
 struct Scoring {
   static constexpr int RW = MP ? 2 * D : D;  // floats per representative
   static constexpr int P = MP ? 1 : PASS;    // row passes per wave
+  static constexpr bool kReg = QREG && !MP;
   using Tile = RowTile<RW, P>;
-  __device__ static void dot(const Tile& t, int n, int r0, const double* q, int G, double* scores, uint32_t* img,
+  struct Empty {};
+  struct Query {
+    std::conditional_t<kReg, QReg<D>, Empty> reg;
+    const double* lds;  // summed query [D], or the bound's [G][D]
+    int G;
+  };
+  // after the query rows are in LDS (and visible to the calling thread)
+  __device__ static void prepare(Query& q, const double* lds, int G) {
+    q.lds = lds;
+    q.G = G;
+    if constexpr (kReg) qreg_load<D>(lds, q.reg);
+  }
+  __device__ static void dot(const Tile& t, int n, int r0, const Query& q, double* scores, uint32_t* img,
                              unsigned long long* ck) {
     if constexpr (MP)
-      tile_dot_mp<D, P>(t, n, r0, q, G, scores, img, ck);
+      tile_dot_mp<D, P>(t, n, r0, q.lds, q.G, scores, img, ck);
+    else if constexpr (kReg)
+      tile_dot<D, P>(t, n, r0, q.reg, scores, img, ck);
     else
-      tile_dot<D, P>(t, n, r0, q, scores, img, ck);
+      tile_dot_lds<D, P>(t, n, r0, q.lds, scores, img, ck);
   }
 };
 
@@ -251,6 +310,28 @@ __device__ __forceinline__ int ascending_pos(const int* top, int k, int j) {
   return p;
 }
 
+// Writes the level-2 result: entry top[j] (j < k_clusters) goes to its ascending position, in
+// layer l and the following layers of the call that share its selection. Threads t0, t0 + nt, ...
+template <bool COH>
+__device__ __forceinline__ void emit_selection(const SelectArgs& a, const int* top, const int* cand,
+                                               const double* s2, int l, int b, int h, int t0, int nt) {
+  const int abs_l = a.layer0 + l;
+  int l_end = l + 1;  // layers [l, l_end) of the call use this selection
+  while (l_end < a.n_layers && owner_layer(a.layer0 + l_end, a.period, a.start) == abs_l) ++l_end;
+  const size_t stride = (size_t)a.B * a.Hkv * a.k_clusters;
+  const size_t o0 = (((size_t)l * a.B + b) * a.Hkv + h) * a.k_clusters;
+  for (int j = t0; j < a.k_clusters; j += nt) {
+    const int i = top[j], p = ascending_pos(top, a.k_clusters, j);
+    const int c = cand[i];
+    const float sc = (float)s2[i];
+    for (int l2 = l; l2 < l_end; ++l2) {
+      const size_t o = o0 + (size_t)(l2 - l) * stride + p;
+      store_sel<COH>(a.sel + o, c);
+      if (a.sel_score) a.sel_score[o] = sc;
+    }
+  }
+}
+
 // LDS carve-up of the one-workgroup-per-head selection (host and device).
 struct BlockLds {
   size_t qsum, s1, s2, ck, img1, img2, list_k, list_i, top, cand, total;
@@ -276,10 +357,11 @@ __host__ __device__ inline BlockLds block_lds(int D, int S, int NC, int qrows) {
 // Selection of owner head `ou` by one workgroup of NW waves (`smem`: block_lds().total bytes).
 // COH: write the selection with device-coherent stores (read by another workgroup of the launch).
 // PASS: row passes per wave in flight (registers against memory parallelism). MP: max-product
-// bound scores (two-row representatives), else dot-product scores.
-template <class DT, int D, int NW, bool COH, int PASS = 2, bool MP = false>
+// bound scores (two-row representatives), else dot-product scores. QREG: keep the summed query in
+// registers (faster) rather than reading it from LDS at every row (fewer registers).
+template <class DT, int D, int NW, bool COH, int PASS = 2, bool MP = false, bool QREG = true>
 __device__ void select_block(const SelectArgs& a, int ou, unsigned char* smem) {
-  using SC = Scoring<D, PASS, MP>;
+  using SC = Scoring<D, PASS, MP, QREG>;
   constexpr int NT = NW * kWave;
   constexpr int TILE = NW * (kWave / 4) * SC::P;  // rows per workgroup pass
   const int G = a.Hq / a.Hkv;
@@ -299,7 +381,6 @@ __device__ void select_block(const SelectArgs& a, int ou, unsigned char* smem) {
   const int BH = a.B * a.Hkv;
   const int l = a.own.l[ou / BH], b = (ou / a.Hkv) % a.B, h = ou % a.Hkv;
   const size_t unit = (size_t)l * BH + ou % BH;
-  const int abs_l = a.layer0 + l;
   const int tid = threadIdx.x, w = tid / kWave;
   const float* scent = a.scent + unit * a.ss * SC::RW;
   const float* cent = a.cent + unit * a.cs * SC::RW;
@@ -315,12 +396,14 @@ __device__ void select_block(const SelectArgs& a, int ou, unsigned char* smem) {
     bnd2[tid] = -1;
   }
   __syncthreads();
+  typename SC::Query qr;
+  SC::prepare(qr, qsum, G);
 
   // level 1: super-cluster scores, top-k_super, their member clusters in ascending order
-  if (r1 < a.S) SC::dot(tile, a.S, r1, qsum, G, s1, img1, ck);
+  if (r1 < a.S) SC::dot(tile, a.S, r1, qr, s1, img1, ck);
   for (int r0 = r1 + TILE; r0 < a.S; r0 += TILE) {
     tile_load<SC::RW, SC::P>(scent, nullptr, a.S, r0, tile);
-    SC::dot(tile, a.S, r0, qsum, G, s1, img1, ck);
+    SC::dot(tile, a.S, r0, qr, s1, img1, ck);
   }
   __syncthreads();
   block_topk<NT>(ck, a.S, a.k_super, list_k, list_i, top, bnd1);
@@ -337,22 +420,12 @@ __device__ void select_block(const SelectArgs& a, int ou, unsigned char* smem) {
   // level 2: candidate scores, top-k_clusters, written in ascending cluster order
   for (int r0 = w * (TILE / NW); r0 < a.NC; r0 += TILE) {
     tile_load<SC::RW, SC::P>(cent, cand, a.NC, r0, tile);
-    SC::dot(tile, a.NC, r0, qsum, G, s2, img2, ck);
+    SC::dot(tile, a.NC, r0, qr, s2, img2, ck);
   }
   __syncthreads();
   block_topk<NT>(ck, a.NC, a.k_clusters, list_k, list_i, top, bnd2);
   repair_top<NT>(s2, img2, a.NC, a.k_clusters, bnd2, top);
-  for (int j = tid; j < a.k_clusters; j += NT) {
-    const int i = top[j], p = ascending_pos(top, a.k_clusters, j);
-    const int c = cand[i];
-    const float sc = (float)s2[i];
-    // this layer and the following layers that share its selection
-    for (int l2 = l; l2 < a.n_layers && owner_layer(a.layer0 + l2, a.period, a.start) == abs_l; ++l2) {
-      const size_t o = (((size_t)l2 * a.B + b) * a.Hkv + h) * a.k_clusters + p;
-      store_sel<COH>(a.sel + o, c);
-      if (a.sel_score) a.sel_score[o] = sc;
-    }
-  }
+  emit_selection<COH>(a, top, cand, s2, l, b, h, tid, NT);
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -444,7 +517,6 @@ __device__ void select_waves(const SelectArgs& a, int ou0, unsigned char* smem) 
 
   const int l = a.own.l[ou / BH], b = (ou / a.Hkv) % a.B, h = ou % a.Hkv;
   const size_t unit = (size_t)l * BH + ou % BH;
-  const int abs_l = a.layer0 + l;
   const float* scent = a.scent + unit * a.ss * SC::RW;
   const float* cent = a.cent + unit * a.cs * SC::RW;
 
@@ -454,12 +526,14 @@ __device__ void select_waves(const SelectArgs& a, int ou0, unsigned char* smem) 
   const size_t q0 = (((size_t)l * a.B + b) * a.Hq + (size_t)h * G) * D;
   load_query<DT, D, MP>(a.q, q0, G, qsum, lane, kWave);
   wave_sync();
+  typename SC::Query qr;
+  SC::prepare(qr, qsum, G);
 
   // level 1
-  SC::dot(tile, a.S, 0, qsum, G, s1, img, ck);
+  SC::dot(tile, a.S, 0, qr, s1, img, ck);
   for (int r0 = TILE; r0 < a.S; r0 += TILE) {
     tile_load<SC::RW, SC::P>(scent, nullptr, a.S, r0, tile);
-    SC::dot(tile, a.S, r0, qsum, G, s1, img, ck);
+    SC::dot(tile, a.S, r0, qr, s1, img, ck);
   }
   wave_sync();
   wave_topk(s1, img, ck, a.S, a.k_super, top);
@@ -475,20 +549,11 @@ __device__ void select_waves(const SelectArgs& a, int ou0, unsigned char* smem) 
   // level 2
   for (int r0 = 0; r0 < a.NC; r0 += TILE) {
     tile_load<SC::RW, SC::P>(cent, cand, a.NC, r0, tile);
-    SC::dot(tile, a.NC, r0, qsum, G, s2, img, ck);
+    SC::dot(tile, a.NC, r0, qr, s2, img, ck);
   }
   wave_sync();
   wave_topk(s2, img, ck, a.NC, a.k_clusters, top);
-  for (int j = lane; j < a.k_clusters; j += kWave) {
-    const int i = top[j], p = ascending_pos(top, a.k_clusters, j);
-    const int c = cand[i];
-    const float sc = (float)s2[i];
-    for (int l2 = l; l2 < a.n_layers && owner_layer(a.layer0 + l2, a.period, a.start) == abs_l; ++l2) {
-      const size_t o = (((size_t)l2 * a.B + b) * a.Hkv + h) * a.k_clusters + p;
-      store_sel<COH>(a.sel + o, c);
-      if (a.sel_score) a.sel_score[o] = sc;
-    }
-  }
+  emit_selection<COH>(a, top, cand, s2, l, b, h, lane, kWave);
 }
 
 inline size_t select_smem_bytes_dev(int D, int S, int NC, int qrows) { return block_lds(D, S, NC, qrows).total; }
