@@ -4,9 +4,9 @@
 // fp32 representatives accumulated in fp64: the summed group query against one row (linear form,
 // average), or the G queries against the r^max / r^min rows (max-product bound). Every product of
 // a 16-bit or fp32 input with an fp32 representative is exact in fp64, so only the summation order
-// differs from a sequential sum. Ranking is by (score desc, index asc): one wave searches the
-// k-th largest order-preserving 64-bit image of the fp64 scores bit by bit with ballots, and
-// output positions are ballot prefix counts in ascending id order. Only owner heads get work.
+// differs from a sequential sum. Ranking is by (score desc, index asc) on unique composite integer
+// keys with an exact fp64 re-rank of a tied boundary group; output positions are counts over the
+// selected ids. Only owner heads get work.
 #include "select_dev.h"
 
 namespace mpc {
