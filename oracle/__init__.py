@@ -33,16 +33,17 @@ def lib():
             "mpcref_static_topk": ([I, V, I, I, V], ctypes.c_int),
             "mpcref_cluster_bounds": ([I, I, I, V, I, I, V, V], ctypes.c_int),
             "mpcref_centroid": ([D, D, F], F),
-            "mpcref_cluster_scores": ([I, I, I, I, V, I, V, V], ctypes.c_int),
+            "mpcref_cluster_scores": ([I, I, I, I, I, V, I, V, V], ctypes.c_int),
             "mpcref_cluster_mean": ([I, I, I, V, I, I, V], ctypes.c_int),
             "mpcref_mp_bound": ([I, V, V, V, V], ctypes.c_int),
             "mpcref_topk": ([I, V, I, V], ctypes.c_int),
             "mpcref_attend": ([I, I, F, V, I, V, V, V, V, V], ctypes.c_int),
             "mpcref_static_evict": ([I] * 11 + [F, I, I, I] + [V] * 7, ctypes.c_int),
             "mpcref_build_clusters": ([I] * 9 + [F, I, I, I] + [V] * 3, ctypes.c_int),
-            "mpcref_select_clusters": ([I] * 15 + [V] * 5, ctypes.c_int),
+            "mpcref_select_clusters": ([I] * 16 + [V] * 5, ctypes.c_int),
             "mpcref_append_state": ([I, I, I, V, V], ctypes.c_int),
-            "mpcref_sparse_decode_attn": ([I] * 9 + [V] * 4 + [I, F, V, V], ctypes.c_int),
+            "mpcref_sparse_decode_attn": ([I] * 9 + [V] * 4 + [I, I, F, V, V], ctypes.c_int),
+            "mpcref_commonality": ([I] * 4 + [V, V], ctypes.c_int),
             "mpcref_dense_decode_attn": ([I] * 7 + [V] * 3 + [F, V, V], ctypes.c_int),
             "mpcref_threads": ([], ctypes.c_int),
         }
@@ -143,6 +144,7 @@ def centroid(rmax, rmin, alpha):
 
 
 SIMILARITY = {"linear": 0, "maxprod": 1, "mean": 2}
+GROUP = {"sum": 0, "max": 1, "head": 2}
 
 
 def rep_rows(similarity):
@@ -150,14 +152,15 @@ def rep_rows(similarity):
     return 2 if SIMILARITY[similarity] == 1 else 1
 
 
-def cluster_scores(q_group, cent, dtype, similarity="linear"):
-    """q_group [G][d] (raw bits), cent [n][R][d] (or [n][d] when R = 1) float32 -> fp64 scores [n]."""
+def cluster_scores(q_group, cent, dtype, similarity="linear", group="sum"):
+    """q_group [G][d] (raw bits), cent [n][R][d] (or [n][d] when R = 1) float32 -> fp64 scores [n];
+    the G heads' similarities are summed (group="sum") or their maximum taken (group="max")."""
     q_group, cent = _c(q_group), _c(cent, np.float32)
     G, d = q_group.shape
     n = cent.shape[0]
     out = np.empty(n, np.float64)
-    _ok(lib().mpcref_cluster_scores(G, d, DTYPE_CODE[dtype], SIMILARITY[similarity], _p(q_group), n, _p(cent),
-                                    _p(out)), "mpcref_cluster_scores")
+    _ok(lib().mpcref_cluster_scores(G, d, DTYPE_CODE[dtype], SIMILARITY[similarity], GROUP[group], _p(q_group), n,
+                                    _p(cent), _p(out)), "mpcref_cluster_scores")
     return out
 
 
@@ -231,15 +234,19 @@ def build_clusters(k_cache, dtype, *, cluster, fanout, alpha=0.6, layer0=0, shar
 
 
 def select_clusters(q, cent, scent, dtype, *, Ts, cluster, fanout, k_super, k_clusters, layer0=0,
-                    share_period=1, share_start=2, sel_in=None, similarity="linear"):
+                    share_period=1, share_start=2, sel_in=None, similarity="linear", group="sum"):
+    """-> sel [L][B][H][k_clusters] (ascending cluster ids) and their fp64 scores, with H = Hkv
+    (group "sum" / "max": one selection per kv head) or H = Hq (group "head")."""
     q, cent, scent = _c(q), _c(cent, np.float32), _c(scent, np.float32)
     L, B, Hq, d = q.shape
     Hkv = cent.shape[2]
-    sel = np.zeros((L, B, Hkv, k_clusters), np.int32) if sel_in is None else _c(sel_in, np.int32).copy()
-    score = np.zeros((L, B, Hkv, k_clusters), np.float64)
+    H = Hq if group == "head" else Hkv
+    sel = np.zeros((L, B, H, k_clusters), np.int32) if sel_in is None else _c(sel_in, np.int32).copy()
+    score = np.zeros((L, B, H, k_clusters), np.float64)
     _ok(lib().mpcref_select_clusters(B, layer0, L, Hq, Hkv, d, DTYPE_CODE[dtype], Ts, cluster, fanout,
                                      k_super, k_clusters, share_period, share_start, SIMILARITY[similarity],
-                                     _p(q), _p(cent), _p(scent), _p(sel), _p(score)), "mpcref_select_clusters")
+                                     GROUP[group], _p(q), _p(cent), _p(scent), _p(sel), _p(score)),
+        "mpcref_select_clusters")
     return sel, score
 
 
@@ -252,16 +259,27 @@ def append_state(Ts, n_tail, cluster):
 
 def sparse_decode_attn(q, k_cache, v_cache, sel, dtype, *, cluster, sm_scale, n_tail=0):
     """k_cache / v_cache [L][B][Hkv][Ts + n_tail][d]: clustered rows, then n_tail tail rows that every
-    head attends."""
+    head attends. sel [L][B][Hkv][k] (one list per kv head) or [L][B][Hq][k] (one per query head)."""
     q, k_cache, v_cache, sel = _c(q), _c(k_cache), _c(v_cache), _c(sel, np.int32)
     L, B, Hq, d = q.shape
     Hkv, Ts = k_cache.shape[2], k_cache.shape[3] - n_tail
     out = np.empty((L, B, Hq, d), np.float64)
     lse = np.empty((L, B, Hq), np.float64)
     _ok(lib().mpcref_sparse_decode_attn(B, L, Hq, Hkv, d, DTYPE_CODE[dtype], Ts, n_tail, cluster, _p(q),
-                                        _p(k_cache), _p(v_cache), _p(sel), sel.shape[-1], sm_scale,
+                                        _p(k_cache), _p(v_cache), _p(sel), sel.shape[2], sel.shape[-1], sm_scale,
                                         _p(out), _p(lse)), "mpcref_sparse_decode_attn")
     return out, lse
+
+
+def commonality(idx, m):
+    """idx [L][...][k] top-k index sets per layer -> commonality score of m + 1 adjacent layers
+    (Sec. 3, Observation 3) for every unit of the middle axes (fp64, shape idx.shape[1:-1])."""
+    idx = _c(idx, np.int32)
+    L, k = idx.shape[0], idx.shape[-1]
+    units = int(np.prod(idx.shape[1:-1], dtype=np.int64))
+    out = np.empty(units, np.float64)
+    _ok(lib().mpcref_commonality(L, units, k, m, _p(idx), _p(out)), "mpcref_commonality")
+    return out.reshape(idx.shape[1:-1])
 
 
 def dense_decode_attn(q, k_cache, v_cache, dtype, *, sm_scale):

@@ -15,6 +15,10 @@
 //   mpcref_cluster_mean    pinned (numpy mean in fp64)
 //   mpcref_topk            pinned (numpy lexsort)
 //   mpcref_attend          pinned (torch scaled_dot_product_attention, fp64)
+//   grouped heads          pinned (max / sum of per-head numpy scores; per-head and max-rule
+//                          selections against independent numpy ranking; one-head groups select
+//                          alike in every rule; per-head lists against torch attention)
+//   mpcref_commonality     pinned (worked cases, python set intersections, exact fractions)
 //   the rule functions     pinned by the integers stated for the five workloads
 // The readings of silent passages (GQA aggregation, causal mask and 1/sqrt(d) in static scoring,
 // a recent-token window, integer rounding of budgets, fp32 storage of centroids) are conventions
@@ -241,28 +245,40 @@ float mpcref_centroid(double rmax, double rmin, float alpha) {
   return (float)((double)pa + (double)pb);
 }
 
-// Similarity of the decode query with each cluster representative. Linear (Sec. 3.3, Eq. "sim")
-// and average: sum_i q_i * c_i with the stored representative c. Max-product bound (Sec. 3.3,
-// Eq. 2): sum_i max(q_i r^max_i, q_i r^min_i) over the stored bounds (rows r^max, r^min). Reading
-// for grouped heads: the G query heads of a kv head share one selection scored by the sum of their
-// similarities. `rep` holds n representatives of (similarity == 1 ? 2 : 1) rows of d floats.
-int mpcref_cluster_scores(int32_t G, int32_t d, int32_t dtype, int32_t similarity, const void* q,
+// Similarity of one query head with one cluster representative. Linear (Sec. 3.3, Eq. "sim") and
+// average: sum_i q_i * c_i with the stored representative c. Max-product bound (Sec. 3.3, Eq. 2):
+// sum_i max(q_i r^max_i, q_i r^min_i) over the stored bounds (rows r^max, r^min).
+static double head_similarity(int32_t d, int32_t dtype, int32_t similarity, const void* q, const float* r) {
+  double acc = 0.0;
+  for (int32_t i = 0; i < d; ++i) {
+    const double qi = load(q, i, dtype);
+    if (similarity == 1)
+      acc += std::max(qi * (double)r[i], qi * (double)r[d + i]);
+    else
+      acc += qi * (double)r[i];
+  }
+  return acc;
+}
+
+// Similarity of the G query heads of a kv head with each cluster representative. The paper states
+// the similarity for one query. Readings for grouped heads (group): 0, the heads share one
+// selection scored by the sum of their similarities (for the linear forms, the similarity of the
+// summed query); 1, they share one selection scored by the largest of their similarities. `rep`
+// holds n representatives of (similarity == 1 ? 2 : 1) rows of d floats.
+int mpcref_cluster_scores(int32_t G, int32_t d, int32_t dtype, int32_t similarity, int32_t group, const void* q,
                           int32_t n, const float* rep, double* score) {
-  if (G <= 0 || d <= 0 || n < 0 || !valid_dtype(dtype) || similarity < 0 || similarity > 2 || !q ||
-      (n && (!rep || !score)))
+  if (G <= 0 || d <= 0 || n < 0 || !valid_dtype(dtype) || similarity < 0 || similarity > 2 || group < 0 ||
+      group > 1 || !q || (n && (!rep || !score)))
     return EINVAL;
   const int32_t R = similarity == 1 ? 2 : 1;
+  const size_t es = elt_size(dtype);
   for (int32_t c = 0; c < n; ++c) {
     const float* r = rep + (size_t)c * R * d;
-    double acc = 0.0;
-    for (int32_t g = 0; g < G; ++g)
-      for (int32_t i = 0; i < d; ++i) {
-        const double qi = load(q, (size_t)g * d + i, dtype);
-        if (similarity == 1)
-          acc += std::max(qi * (double)r[i], qi * (double)r[d + i]);
-        else
-          acc += qi * (double)r[i];
-      }
+    double acc = group == 0 ? 0.0 : -INFINITY;
+    for (int32_t g = 0; g < G; ++g) {
+      const double sg = head_similarity(d, dtype, similarity, (const char*)q + (size_t)g * d * es, r);
+      acc = group == 0 ? acc + sg : std::max(acc, sg);
+    }
     score[c] = acc;
   }
   return OK;
@@ -413,14 +429,18 @@ int mpcref_build_clusters(int32_t B, int32_t layer0, int32_t n_layers, int32_t H
 // coarse clusters and keeps k_super; level 2 ranks the fine clusters inside the kept coarse ones
 // and keeps k_clusters, written in ascending order. Non-owner layers copy their owner's selection
 // (Sec. 3.4); a layer whose owner precedes layer0 keeps the `sel` the caller passed in.
+// group: 0 / 1, one selection per kv head scored by the sum / the maximum of its query heads'
+// similarities (sel [n_layers][B][Hkv][k_clusters]); 2, one selection per query head from its own
+// similarity against its kv head's representatives (sel [n_layers][B][Hq][k_clusters]). The paper
+// states the selection for one query head; the grouped forms are readings.
 int mpcref_select_clusters(int32_t B, int32_t layer0, int32_t n_layers, int32_t Hq, int32_t Hkv,
                            int32_t d, int32_t dtype, int32_t Ts, int32_t cluster, int32_t fanout,
                            int32_t k_super, int32_t k_clusters, int32_t share_period,
-                           int32_t share_start, int32_t similarity, const void* q, const float* cent,
-                           const float* scent, int32_t* sel, double* sel_score) {
+                           int32_t share_start, int32_t similarity, int32_t group, const void* q,
+                           const float* cent, const float* scent, int32_t* sel, double* sel_score) {
   if (B <= 0 || layer0 < 0 || n_layers <= 0 || Hq <= 0 || Hkv <= 0 || d <= 0 || Ts <= 0 ||
-      cluster <= 0 || fanout <= 0 || !valid_dtype(dtype) || similarity < 0 || similarity > 2 || !q ||
-      !cent || !scent || !sel)
+      cluster <= 0 || fanout <= 0 || !valid_dtype(dtype) || similarity < 0 || similarity > 2 || group < 0 ||
+      group > 2 || !q || !cent || !scent || !sel)
     return EINVAL;
   const int32_t R = similarity == 1 ? 2 : 1;
   const int32_t C = ceil_div(Ts, cluster), S = ceil_div(C, fanout);
@@ -429,15 +449,18 @@ int mpcref_select_clusters(int32_t B, int32_t layer0, int32_t n_layers, int32_t 
   if (k_clusters > k_super * fanout - (fanout - tail)) return ESHAPE;
   const int32_t G = Hq / Hkv;
   const size_t es = elt_size(dtype);
-  const int64_t units = (int64_t)n_layers * B * Hkv;
+  // selection heads per (layer, sequence); query heads scored together; the kv head of head h
+  const int32_t H = group == 2 ? Hq : Hkv, Gs = group == 2 ? 1 : G, rdiv = group == 2 ? G : 1;
+  const int64_t units = (int64_t)n_layers * B * H;
 #pragma omp parallel for schedule(dynamic)
   for (int64_t u = 0; u < units; ++u) {
-    const int32_t l = (int32_t)(u / ((int64_t)B * Hkv));
+    const int32_t l = (int32_t)(u / ((int64_t)B * H));
     if (mpcref_owner_layer(layer0 + l, share_period, share_start) != layer0 + l) continue;
-    const int32_t b = (int32_t)((u / Hkv) % B), h = (int32_t)(u % Hkv);
-    const char* qg = (const char*)q + (((size_t)l * B + b) * Hq + (size_t)h * G) * d * es;
+    const int32_t b = (int32_t)((u / H) % B), h = (int32_t)(u % H);
+    const char* qg = (const char*)q + (((size_t)l * B + b) * Hq + (size_t)h * Gs) * d * es;
+    const size_t ru = ((size_t)l * B + b) * Hkv + h / rdiv;  // representatives of this kv head
     std::vector<double> s1(S);
-    mpcref_cluster_scores(G, d, dtype, similarity, qg, S, scent + (size_t)u * S * R * d, s1.data());
+    mpcref_cluster_scores(Gs, d, dtype, similarity, group == 1, qg, S, scent + ru * S * R * d, s1.data());
     std::vector<int32_t> top1(k_super);
     mpcref_topk(S, s1.data(), k_super, top1.data());
     std::sort(top1.begin(), top1.end());
@@ -447,7 +470,7 @@ int mpcref_select_clusters(int32_t B, int32_t layer0, int32_t n_layers, int32_t 
     const int32_t n = (int32_t)cand.size();
     std::vector<double> s2(n);
     for (int32_t j = 0; j < n; ++j)
-      mpcref_cluster_scores(G, d, dtype, similarity, qg, 1, cent + ((size_t)u * C + cand[j]) * R * d, &s2[j]);
+      mpcref_cluster_scores(Gs, d, dtype, similarity, group == 1, qg, 1, cent + (ru * C + cand[j]) * R * d, &s2[j]);
     std::vector<int32_t> top2(k_clusters);
     mpcref_topk(n, s2.data(), k_clusters, top2.data());
     std::sort(top2.begin(), top2.end());  // positions in the ascending candidate list
@@ -459,7 +482,7 @@ int mpcref_select_clusters(int32_t B, int32_t layer0, int32_t n_layers, int32_t 
   for (int32_t l = 0; l < n_layers; ++l) {
     const int32_t o = mpcref_owner_layer(layer0 + l, share_period, share_start) - layer0;
     if (o == l || o < 0) continue;
-    const size_t n = (size_t)B * Hkv * k_clusters;
+    const size_t n = (size_t)B * H * k_clusters;
     std::memcpy(sel + (size_t)l * n, sel + (size_t)o * n, n * sizeof(int32_t));
     if (sel_score) std::memcpy(sel_score + (size_t)l * n, sel_score + (size_t)o * n, n * sizeof(double));
   }
@@ -481,17 +504,18 @@ int mpcref_append_state(int32_t Ts, int32_t n_tail, int32_t cluster, int32_t* Ts
   return OK;
 }
 
-// Sparse attention of every query head over the tokens of its kv head's selected clusters, then
-// the n_tail decode-time tokens that follow the clustered ones (k_cache holds Ts + n_tail rows per
-// head).
+// Sparse attention of every query head over the tokens of its selected clusters, then the n_tail
+// decode-time tokens that follow the clustered ones (k_cache holds Ts + n_tail rows per head).
+// sel_heads = Hkv: one list per kv head, shared by its query heads; sel_heads = Hq: one list per
+// query head, over its kv head's rows.
 int mpcref_sparse_decode_attn(int32_t B, int32_t n_layers, int32_t Hq, int32_t Hkv, int32_t d,
                               int32_t dtype, int32_t Ts, int32_t n_tail, int32_t cluster, const void* q,
-                              const void* k_cache, const void* v_cache, const int32_t* sel,
+                              const void* k_cache, const void* v_cache, const int32_t* sel, int32_t sel_heads,
                               int32_t k_clusters, float sm_scale, double* out, double* lse) {
   if (B <= 0 || n_layers <= 0 || Hq <= 0 || Hkv <= 0 || d <= 0 || Ts <= 0 || n_tail < 0 || cluster <= 0 ||
       k_clusters <= 0 || !valid_dtype(dtype) || !q || !k_cache || !v_cache || !sel || !out)
     return EINVAL;
-  if (Hq % Hkv) return ESHAPE;
+  if (Hq % Hkv || (sel_heads != Hkv && sel_heads != Hq)) return ESHAPE;
   const int32_t G = Hq / Hkv, C = ceil_div(Ts, cluster);
   const int32_t rows_per_head = Ts + n_tail;
   const size_t es = elt_size(dtype);
@@ -502,9 +526,10 @@ int mpcref_sparse_decode_attn(int32_t B, int32_t n_layers, int32_t Hq, int32_t H
     const int64_t lb = u / Hq;
     const int32_t h = (int32_t)(u % Hq);
     const int64_t kvu = lb * Hkv + h / G;
+    const int64_t su = sel_heads == Hq ? u : kvu;  // the head's selection list
     std::vector<int32_t> rows;
     for (int32_t j = 0; j < k_clusters; ++j) {
-      const int32_t c = sel[kvu * k_clusters + j];
+      const int32_t c = sel[su * k_clusters + j];
       if (c < 0 || c >= C) {
         rc = EINVAL;
         rows.clear();
@@ -544,6 +569,31 @@ int mpcref_dense_decode_attn(int32_t B, int32_t n_layers, int32_t Hq, int32_t Hk
     mpcref_attend(d, dtype, sm_scale, (const char*)q + (size_t)u * d * es, Ts, rows.data(),
                   (const char*)k_cache + head, (const char*)v_cache + head, out + (size_t)u * d,
                   lse ? lse + u : nullptr);
+  }
+  return OK;
+}
+
+// Commonality score of m + 1 adjacent layers (Sec. 3, Observation 3):
+// (1 / (k (L - m))) * sum_{l=0}^{L-m-1} |intersection of idx_i[:k] for i = l .. l+m|, for every
+// (sequence, head) unit. idx [L][units][k] holds each layer's top-k index set (any order, distinct
+// entries). The paper's sum runs over l = 1 .. L - m with the sets of layers l .. l + m; with
+// layers counted from 0 that is l = 0 .. L - m - 1.
+int mpcref_commonality(int32_t L, int32_t units, int32_t k, int32_t m, const int32_t* idx, double* out) {
+  if (L <= 0 || units <= 0 || k <= 0 || m < 0 || m >= L || !idx || !out) return EINVAL;
+  for (int32_t u = 0; u < units; ++u) {
+    int64_t total = 0;
+    for (int32_t l = 0; l + m < L; ++l) {
+      const int32_t* a = idx + ((size_t)l * units + u) * k;
+      for (int32_t j = 0; j < k; ++j) {
+        bool in_all = true;
+        for (int32_t i = l + 1; i <= l + m && in_all; ++i) {
+          const int32_t* b = idx + ((size_t)i * units + u) * k;
+          in_all = std::find(b, b + k, a[j]) != b + k;
+        }
+        total += in_all;
+      }
+    }
+    out[u] = (double)total / ((double)k * (double)(L - m));
   }
   return OK;
 }

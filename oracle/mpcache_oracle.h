@@ -14,7 +14,8 @@
  *       q_win [n_layers][B][Hq][W][d], k/v [n_layers][B][Hkv][T][d], q [n_layers][B][Hq][d],
  *       kept  [n_layers][B][Hkv][keep], cent [n_layers][B][Hkv][C][R][d], scent [...][S][R][d]
  *       (R = 2 rows r^max, r^min for the max-product bound, else 1),
- *       sel   [n_layers][B][Hkv][k_clusters], out [n_layers][B][Hq][d].
+ *       sel   [n_layers][B][Hkv][k_clusters] (or [..][Hq][..] with one selection per query head),
+ *       out [n_layers][B][Hq][d].
  *   - q-head h reads kv-head h / (Hq / Hkv).
  *   - layer indices passed to the sharing rule are absolute: layer0 + local index.
  *   - return value: 0 ok, 1 invalid argument, 2 inconsistent shape, 3 unsupported.
@@ -49,8 +50,9 @@ int mpcref_cluster_mean(int32_t n_tok, int32_t d, int32_t dtype, const void* k /
                         int32_t first, int32_t count, double* mean);
 float mpcref_centroid(double rmax, double rmin, float alpha);
 /* similarity: 0 linear alpha r^max + (1 - alpha) r^min, 1 max-product bound (rows r^max, r^min),
- * 2 average; representatives have (similarity == 1 ? 2 : 1) rows of d floats. */
-int mpcref_cluster_scores(int32_t G, int32_t d, int32_t dtype, int32_t similarity,
+ * 2 average; representatives have (similarity == 1 ? 2 : 1) rows of d floats. group: the G heads'
+ * similarities are summed (0) or their maximum is taken (1). */
+int mpcref_cluster_scores(int32_t G, int32_t d, int32_t dtype, int32_t similarity, int32_t group,
                           const void* q /*[G][d]*/, int32_t n, const float* rep /*[n][R][d]*/,
                           double* score);
 int mpcref_mp_bound(int32_t d, const double* q, const double* rmax, const double* rmin,
@@ -73,7 +75,7 @@ int mpcref_build_clusters(int32_t B, int32_t layer0, int32_t n_layers, int32_t H
 int mpcref_select_clusters(int32_t B, int32_t layer0, int32_t n_layers, int32_t Hq, int32_t Hkv,
                            int32_t d, int32_t dtype, int32_t Ts, int32_t cluster, int32_t fanout,
                            int32_t k_super, int32_t k_clusters, int32_t share_period,
-                           int32_t share_start, int32_t similarity, const void* q,
+                           int32_t share_start, int32_t similarity, int32_t group, const void* q,
                            const float* cent, const float* scent, int32_t* sel, double* sel_score);
 /* Decode-time growth: (Ts, n_tail) after one appended token (a full tail of `cluster` rows is
  * sealed into a cluster first). Our reading; the paper only states the concatenation. */
@@ -84,10 +86,14 @@ int mpcref_append_state(int32_t Ts, int32_t n_tail, int32_t cluster, int32_t* Ts
 int mpcref_sparse_decode_attn(int32_t B, int32_t n_layers, int32_t Hq, int32_t Hkv, int32_t d,
                               int32_t dtype, int32_t Ts, int32_t n_tail, int32_t cluster, const void* q,
                               const void* k_cache, const void* v_cache, const int32_t* sel,
-                              int32_t k_clusters, float sm_scale, double* out, double* lse);
+                              int32_t sel_heads, int32_t k_clusters, float sm_scale, double* out,
+                              double* lse);
 int mpcref_dense_decode_attn(int32_t B, int32_t n_layers, int32_t Hq, int32_t Hkv, int32_t d,
                              int32_t dtype, int32_t Ts, const void* q, const void* k_cache,
                              const void* v_cache, float sm_scale, double* out, double* lse);
+/* Commonality score of m + 1 adjacent layers' top-k index sets (Sec. 3, Observation 3), per unit:
+ * idx [L][units][k] -> out [units]. */
+int mpcref_commonality(int32_t L, int32_t units, int32_t k, int32_t m, const int32_t* idx, double* out);
 int mpcref_threads(void);
 
 #ifdef __cplusplus

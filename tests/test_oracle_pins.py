@@ -438,6 +438,128 @@ def test_index_sharing_copies_owner_selection():
     np.testing.assert_array_equal(sel[2], alone[4])  # layer 5 follows layer 4
 
 
+# ------------------------------------------------------------------------ grouped query heads
+def _head_scores(qh, rep, similarity):
+    """numpy score of one query head [d] against representatives [n][R][d] (or [n][d])."""
+    rep = rep.astype(np.float64)
+    if similarity == "maxprod":
+        return np.maximum(qh * rep[:, 0], qh * rep[:, 1]).sum(-1)
+    return rep @ qh
+
+
+@pytest.mark.parametrize("similarity", ["linear", "maxprod", "mean"])
+def test_group_max_score_is_the_largest_head_score(similarity):
+    r = rng(41)
+    G, d, n = 4, 16, 9
+    q = to_bits(r.standard_normal((G, d)), "fp16")
+    R = oracle.rep_rows(similarity)
+    rep = r.standard_normal((n, R, d) if R > 1 else (n, d)).astype(np.float32)
+    qf = from_bits(q, "fp16")
+    per_head = np.stack([_head_scores(qf[g], rep, similarity) for g in range(G)])
+    np.testing.assert_allclose(oracle.cluster_scores(q, rep, "fp16", similarity, group="max"), per_head.max(0),
+                               rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(oracle.cluster_scores(q, rep, "fp16", similarity, group="sum"), per_head.sum(0),
+                               rtol=1e-12, atol=1e-12)
+    # one head: the two rules coincide
+    np.testing.assert_array_equal(oracle.cluster_scores(q[:1], rep, "fp16", similarity, group="max"),
+                                  oracle.cluster_scores(q[:1], rep, "fp16", similarity, group="sum"))
+
+
+def _two_level(s1_fn, s2_fn, S, C, f, ks, kc):
+    """Two-level selection by independent numpy ranking: s1_fn() -> [S], s2_fn(cand) -> [len(cand)]."""
+    s1 = s1_fn()
+    sup = np.sort(_lexsort_topk(s1, ks))
+    cand = np.array([c for x in sup for c in range(x * f, min(C, (x + 1) * f))])
+    s2 = s2_fn(cand)
+    return np.sort(cand[_lexsort_topk(s2, kc)])
+
+
+@pytest.mark.parametrize("similarity", ["linear", "maxprod"])
+@pytest.mark.parametrize("group", ["max", "head"])
+def test_grouped_selection_matches_independent_ranking(similarity, group):
+    Ts, s, f, ks, kc, G, C, S = 200, 8, 4, 3, 5, 2, 25, 7
+    k, q, cent, scent = _select_case(42, Ts=Ts, s=s, f=f, similarity=similarity)
+    sel, _ = oracle.select_clusters(q, cent, scent, "bf16", Ts=Ts, cluster=s, fanout=f, k_super=ks, k_clusters=kc,
+                                    similarity=similarity, group=group)
+    qf = from_bits(q, "bf16")
+    L, Hkv = q.shape[0], 2
+    assert sel.shape == ((L, 1, 2 * G, kc) if group == "head" else (L, 1, Hkv, kc))
+    for l in range(L):
+        for h in range(sel.shape[2]):
+            kvh = h // G if group == "head" else h
+            heads = [h] if group == "head" else list(range(h * G, (h + 1) * G))
+
+            def score(rep):
+                return np.max([_head_scores(qf[l, 0, g], rep, similarity) for g in heads], axis=0)
+
+            exp = _two_level(lambda: score(scent[l, 0, kvh]), lambda cand: score(cent[l, 0, kvh, cand]), S, C, f,
+                             ks, kc)
+            np.testing.assert_array_equal(sel[l, 0, h], exp)
+
+
+def test_single_head_groups_select_alike_in_every_rule():
+    Ts, s, f = 200, 8, 4
+    r = rng(43)
+    k = to_bits(r.standard_normal((3, 2, 3, Ts, 16)), "fp16")
+    q = to_bits(r.standard_normal((3, 2, 3, 16)), "fp16")
+    cent, scent = oracle.build_clusters(k, "fp16", cluster=s, fanout=f)
+    kw = dict(Ts=Ts, cluster=s, fanout=f, k_super=4, k_clusters=6)
+    ref, _ = oracle.select_clusters(q, cent, scent, "fp16", group="sum", **kw)
+    for group in ("max", "head"):
+        got, _ = oracle.select_clusters(q, cent, scent, "fp16", group=group, **kw)
+        np.testing.assert_array_equal(got, ref)
+
+
+def test_per_head_selection_is_shared_across_layers():
+    Ts, s, f = 200, 8, 4
+    k, q, cent, scent = _select_case(44, L=8, Ts=Ts, s=s, f=f)
+    kw = dict(Ts=Ts, cluster=s, fanout=f, k_super=3, k_clusters=4, group="head")
+    shared, _ = oracle.select_clusters(q, cent, scent, "bf16", share_period=2, **kw)
+    alone, _ = oracle.select_clusters(q, cent, scent, "bf16", share_period=1, **kw)
+    for l in range(8):
+        np.testing.assert_array_equal(shared[l], alone[oracle.owner_layer(l, 2, 2)])
+
+
+def test_per_head_sparse_attention_uses_each_heads_clusters():
+    L, B, Hq, Hkv, Ts, d, s = 1, 2, 4, 2, 40, 8, 8   # C = 5
+    r = rng(45)
+    k = to_bits(r.standard_normal((L, B, Hkv, Ts, d)), "bf16")
+    v = to_bits(r.standard_normal((L, B, Hkv, Ts, d)), "bf16")
+    q = to_bits(r.standard_normal((L, B, Hq, d)), "bf16")
+    sel = np.array([[[[0, 3], [1, 4], [2, 3], [0, 1]], [[1, 2], [3, 4], [0, 4], [2, 3]]]], np.int32)
+    out, _ = oracle.sparse_decode_attn(q, k, v, sel, "bf16", cluster=s, sm_scale=0.35)
+    qf, kf, vf = (from_bits(x, "bf16") for x in (q, k, v))
+    for b in range(B):
+        for h in range(Hq):
+            rows = [t for c in sel[0, b, h] for t in range(c * s, (c + 1) * s)]
+            ref = _sdpa(qf[0, b, h], kf[0, b, h // 2, rows], vf[0, b, h // 2, rows], float(np.float32(0.35)))
+            np.testing.assert_allclose(out[0, b, h], ref, rtol=1e-12, atol=1e-13)
+
+
+# ------------------------------------------------------------------------ commonality (Sec. 3, Obs. 3)
+def test_commonality_worked_cases():
+    idx = np.array([[[1, 2]], [[2, 3]], [[3, 4]]], np.int32)  # layers {1,2}, {2,3}, {3,4}
+    assert oracle.commonality(idx, 1)[0] == 0.5   # (1 + 1) / (2 * 2)
+    assert oracle.commonality(idx, 2)[0] == 0.0   # empty triple intersection
+    assert oracle.commonality(idx, 0)[0] == 1.0   # every set with itself
+    same = np.tile(np.array([5, 1, 9], np.int32), (6, 2, 1))
+    assert np.all(oracle.commonality(same, 4) == 1.0)
+    disjoint = np.arange(5 * 3, dtype=np.int32).reshape(5, 1, 3)
+    assert oracle.commonality(disjoint, 1)[0] == 0.0
+
+
+def test_commonality_matches_set_intersections():
+    r = rng(46)
+    L, U, k, n = 7, 5, 6, 12
+    idx = np.stack([np.stack([r.choice(n, k, replace=False) for _ in range(U)]) for _ in range(L)]).astype(np.int32)
+    for m in (1, 2, 3):
+        got = oracle.commonality(idx, m)
+        for u in range(U):
+            tot = sum(len(set.intersection(*[set(idx[i, u].tolist()) for i in range(l, l + m + 1)]))
+                      for l in range(L - m))
+            assert got[u] == float(Fraction(tot, k * (L - m)))
+
+
 # ------------------------------------------------------------------------ attention (A9, A12)
 def _sdpa(q, k, v, sm):
     """torch scaled_dot_product_attention in fp64 on the CPU: q [d], k/v [n][d]."""
