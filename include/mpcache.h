@@ -72,6 +72,13 @@ typedef struct {
  * paper's average-based comparison), one row. */
 typedef enum { MPC_SIM_LINEAR = 0, MPC_SIM_MAXPROD = 1, MPC_SIM_MEAN = 2 } mpc_similarity;
 
+/* Grouped query heads (Hq > Hkv). The paper states the selection for a single query head; these are
+ * the readings offered. SUM: the G query heads of a kv head share one selection, scored by the sum
+ * of their similarities (for LINEAR / MEAN the similarity of the summed query). MAX: they share one
+ * selection, scored by the largest of their similarities. HEAD: every query head selects its own
+ * clusters from its own similarity against its kv head's representatives, and attends only them. */
+typedef enum { MPC_GROUP_SUM = 0, MPC_GROUP_MAX = 1, MPC_GROUP_HEAD = 2 } mpc_group;
+
 typedef struct {
   int32_t cluster_size; /* s: tokens per fine cluster                                        */
   int32_t fanout;       /* f: fine clusters per super-cluster                                */
@@ -81,6 +88,7 @@ typedef struct {
   int32_t share_period; /* layers per shared selection (1 = no sharing)                     */
   int32_t share_start;  /* first layer that may share (2 in the paper)                       */
   int32_t similarity;   /* mpc_similarity (MPC_SIM_LINEAR in the paper's method)              */
+  int32_t group;        /* mpc_group (MPC_GROUP_SUM by default)                                */
 } mpc_select_cfg;
 
 typedef struct {
@@ -135,38 +143,44 @@ mpc_status mpc_build_clusters(const mpc_dims* dims, int32_t Ts, const mpc_select
                               const void* k_cache, float* cent, float* scent, void* stream);
 
 /* Query-aware dynamic selection of one decode step (Sec. 3.3; Alg. 3 step 2).
- * Score of a representative for kv head h, summed over the group's q-heads g and channels i and
- * accumulated in fp64: q_{g,i} * c_i (LINEAR, MEAN) or max(q_{g,i} r^max_i, q_{g,i} r^min_i)
- * (MAXPROD, Eq. 2). Level 1 keeps the k_super best super-clusters, level 2 the
- * k_clusters best fine clusters among their members (ties: lower index first); the selection is
- * written in ascending cluster order. Non-owner layers receive their owner's selection; a layer
- * whose owner precedes layer0 is left untouched (the caller copies it).
+ * Similarity of one q-head g with a representative, summed over the channels i and accumulated in
+ * fp64: q_{g,i} * c_i (LINEAR, MEAN) or max(q_{g,i} r^max_i, q_{g,i} r^min_i) (MAXPROD, Eq. 2). The
+ * score of a selection unit combines its q-heads by cfg->group: the sum (SUM) or the maximum (MAX)
+ * over the G heads of kv head h, or the head's own similarity (HEAD, one unit per q-head). Level 1
+ * keeps the k_super best super-clusters, level 2 the k_clusters best fine clusters among their
+ * members (ties: lower index first); the selection is written in ascending cluster order.
+ * Non-owner layers receive their owner's selection; a layer whose owner precedes layer0 is left
+ * untouched (the caller copies it).
  *   q [L][B][Hq][d];  cent / scent as produced by mpc_build_clusters (Ccap / Scap slots, the
  *   first C / S used);
- *   sel [L][B][Hkv][k_clusters] int32 out;  sel_score same shape, float, optional (score rounded
- *   to fp32). ws may be NULL (no workspace needed). Limits: S <= 1024, k_super * f <= 1024. */
+ *   sel [L][B][H][k_clusters] int32 out, H = Hq for MPC_GROUP_HEAD, else Hkv;  sel_score same
+ *   shape, float, optional (score rounded to fp32). ws may be NULL (no workspace needed).
+ *   Limits: S <= 1024, k_super * f <= 1024. */
 mpc_status mpc_select_clusters(const mpc_dims* dims, int32_t Ts, const mpc_select_cfg* cfg,
                                const void* q, const float* cent, const float* scent,
                                int32_t* sel, float* sel_score, void* ws, size_t ws_bytes,
                                void* stream);
 
 /* Sparse attention over the selected clusters (Alg. 1 steps 3-4; Alg. 3 step 2):
- * o_h = softmax(sm_scale * q_h K'^T) V' with K', V' the kept-cache rows of the clusters in
- * sel[l][b][h / G] (tokens past Ts in a partial last cluster are skipped), followed by the n_tail
- * unclustered rows [Ts, Ts + n_tail) that decoding appended (mpc_append_kv), which every head
- * attends in full.
- *   q [L][B][Hq][d];  k_cache, v_cache [L][B][Hkv][Tcap][d];  sel [L][B][Hkv][k_clusters] int32
- *   (entries outside [0, C) contribute nothing);  n_tail >= 0, and Ts % s == 0 when n_tail > 0;
+ * o_h = softmax(sm_scale * q_h K'^T) V' with K', V' the rows of kv head h / G of the kept cache
+ * that belong to the clusters of h's selection list (tokens past Ts in a partial last cluster are
+ * skipped), followed by the n_tail unclustered rows [Ts, Ts + n_tail) that decoding appended
+ * (mpc_append_kv), which every head attends in full. The list of h is sel[l][b][h / G] when
+ * sel_heads = Hkv (one list per kv head), sel[l][b][h] when sel_heads = Hq (one per q-head, as
+ * MPC_GROUP_HEAD selects).
+ *   q [L][B][Hq][d];  k_cache, v_cache [L][B][Hkv][Tcap][d];  sel [L][B][sel_heads][k_clusters]
+ *   int32 (entries outside [0, C) contribute nothing);  n_tail >= 0, and Ts % s == 0 when
+ *   n_tail > 0;
  *   out [L][B][Hq][d] (dtype);  lse [L][B][Hq] float, optional (natural-log log-sum-exp of the
  *   scaled scores). fp32 accumulation; 16-bit types take exact pairwise products summed in fp32.
  *   Limits: k_clusters + ceil(n_tail / s) <= 1024, Tcap * d * element size <= 2 GiB.
  *   ws: mpc_workspace_bytes(MPC_OP_DECODE_ATTN, dims, Ts, NULL) bytes (split-K partials and
- *   per-unit arrival counters, used when there are fewer (layer, sequence, kv head) units than
- *   twice the compute units), zero-filled before its first use; every completed call leaves the
- *   counters at zero (calls sharing it must not overlap). May be NULL when that size is 0. */
+ *   per-unit arrival counters, used when there are fewer (layer, sequence, list) units than the
+ *   compute units), zero-filled before its first use; every completed call leaves the counters at
+ *   zero (calls sharing it must not overlap). May be NULL when that size is 0. */
 mpc_status mpc_sparse_decode_attn(const mpc_dims* dims, int32_t Ts, int32_t n_tail, int32_t cluster_size,
                                   const void* q, const void* k_cache, const void* v_cache,
-                                  const int32_t* sel, int32_t k_clusters, float sm_scale,
+                                  const int32_t* sel, int32_t sel_heads, int32_t k_clusters, float sm_scale,
                                   void* out, float* lse, void* ws, size_t ws_bytes, void* stream);
 
 /* One decode step in one launch: mpc_select_clusters followed by mpc_sparse_decode_attn (same
@@ -174,13 +188,13 @@ mpc_status mpc_sparse_decode_attn(const mpc_dims* dims, int32_t Ts, int32_t n_ta
  * owner's selection is published instead of after a kernel boundary.
  *   q [L][B][Hq][d]; cent, scent from mpc_build_clusters; k_cache, v_cache [L][B][Hkv][Tcap][d];
  *   n_tail: unclustered rows after Ts, attended in full (as in mpc_sparse_decode_attn);
- *   sel [L][B][Hkv][cfg->k_clusters] int32 out (in for layers owned before layer0);
- *   sel_score optional; out [L][B][Hq][d]; lse optional.
+ *   sel [L][B][H][cfg->k_clusters] int32 out (in for layers owned before layer0), H as in
+ *   mpc_select_clusters; sel_score optional; out [L][B][Hq][d]; lse optional.
  *   ws: mpc_workspace_bytes(MPC_OP_DECODE_STEP, dims, Ts, cfg) bytes, zero-filled before its first
  *   use; every completed call leaves it ready for the next (calls sharing it must not overlap).
- * Blocks whose attention is split over several workgroups per unit, or whose selection and
- * attention together need more LDS than one workgroup has, run the two kernels one after the other
- * instead (same results). */
+ * Blocks whose attention is split over several workgroups per unit, whose selection and attention
+ * together need more LDS than one workgroup has, or that select per q-head (MPC_GROUP_HEAD) run the
+ * two kernels one after the other instead (same results). */
 mpc_status mpc_decode_step(const mpc_dims* dims, int32_t Ts, int32_t n_tail, const mpc_select_cfg* cfg,
                            const void* q, const float* cent, const float* scent,
                            const void* k_cache, const void* v_cache, float sm_scale, int32_t* sel,
@@ -205,6 +219,16 @@ mpc_status mpc_decode_step(const mpc_dims* dims, int32_t Ts, int32_t n_tail, con
 mpc_status mpc_append_kv(const mpc_dims* dims, int32_t Ts, int32_t n_tail, const mpc_select_cfg* cfg,
                          const void* k_new, const void* v_new, void* k_cache, void* v_cache,
                          float* cent, float* scent, void* stream);
+
+/* Commonality score of m + 1 adjacent layers (Sec. 3, Observation 3), the paper's measure of how
+ * far adjacent layers agree on their top-k sets:
+ *   out[u] = (1 / (k (L - m))) * sum_{l=0}^{L-m-1} | intersection over i = l .. l+m of idx[i][u] |
+ * for every unit u (e.g. a (sequence, head) pair). idx [L][units][k] int32 holds each layer's
+ * top-k set (distinct entries; any order), e.g. per-layer selections made without sharing
+ * (share_period = 1). out [units] double. Counts are exact integers; out is their quotient rounded
+ * once. Requires 0 <= m < L, k <= 1024. No workspace. */
+mpc_status mpc_commonality(int32_t L, int32_t units, int32_t k, int32_t m, const int32_t* idx, double* out,
+                           void* stream);
 
 /* Owner layer of absolute layer `l` under the sharing rule above. */
 int32_t mpc_owner_layer(int32_t l, int32_t period, int32_t start);

@@ -26,7 +26,7 @@ class MpcSelectCfg(ctypes.Structure):
     _fields_ = [("cluster_size", ctypes.c_int32), ("fanout", ctypes.c_int32),
                 ("k_super", ctypes.c_int32), ("k_clusters", ctypes.c_int32),
                 ("alpha", ctypes.c_float), ("share_period", ctypes.c_int32),
-                ("share_start", ctypes.c_int32), ("similarity", ctypes.c_int32)]
+                ("share_start", ctypes.c_int32), ("similarity", ctypes.c_int32), ("group", ctypes.c_int32)]
 
 
 class MpcEvictCfg(ctypes.Structure):
@@ -44,7 +44,7 @@ class MpcError(RuntimeError):
 
 _LIB = None
 EXPORTS = ("mpc_workspace_bytes", "mpc_static_evict", "mpc_build_clusters", "mpc_select_clusters",
-           "mpc_sparse_decode_attn", "mpc_decode_step", "mpc_append_kv", "mpc_owner_layer",
+           "mpc_sparse_decode_attn", "mpc_decode_step", "mpc_append_kv", "mpc_commonality", "mpc_owner_layer",
            "mpc_status_string", "mpc_last_error")
 
 
@@ -61,12 +61,13 @@ def lib():
         L.mpc_static_evict.argtypes = [P(MpcDims), I, P(MpcEvictCfg)] + [V] * 8 + [V, ctypes.c_size_t, V]
         L.mpc_build_clusters.argtypes = [P(MpcDims), I, P(MpcSelectCfg), V, V, V, V]
         L.mpc_select_clusters.argtypes = [P(MpcDims), I, P(MpcSelectCfg)] + [V] * 5 + [V, ctypes.c_size_t, V]
-        L.mpc_sparse_decode_attn.argtypes = [P(MpcDims), I, I, I, V, V, V, V, I, F, V, V, V, ctypes.c_size_t, V]
+        L.mpc_sparse_decode_attn.argtypes = [P(MpcDims), I, I, I, V, V, V, V, I, I, F, V, V, V, ctypes.c_size_t, V]
         L.mpc_decode_step.argtypes = [P(MpcDims), I, I, P(MpcSelectCfg)] + [V] * 5 + [F] + [V] * 4 + [
             V, ctypes.c_size_t, V]
         L.mpc_append_kv.argtypes = [P(MpcDims), I, I, P(MpcSelectCfg)] + [V] * 7
+        L.mpc_commonality.argtypes = [I, I, I, I, V, V, V]
         for fn in ("mpc_static_evict", "mpc_build_clusters", "mpc_select_clusters", "mpc_sparse_decode_attn",
-                   "mpc_decode_step", "mpc_append_kv"):
+                   "mpc_decode_step", "mpc_append_kv", "mpc_commonality"):
             getattr(L, fn).restype = ctypes.c_int
         L.mpc_owner_layer.argtypes = [I, I, I]
         L.mpc_owner_layer.restype = I
@@ -140,6 +141,7 @@ def mpc_static_evict(q_win, k, v, kept_idx, k_out, v_out, *, keep, local_keep, s
 
 
 SIMILARITY = {"linear": 0, "maxprod": 1, "mean": 2}
+GROUP = {"sum": 0, "max": 1, "head": 2}
 
 
 def rep_rows(similarity):
@@ -148,10 +150,17 @@ def rep_rows(similarity):
 
 
 def select_cfg(cluster, fanout, k_super, k_clusters, alpha=0.6, share_period=1, share_start=2,
-               similarity="linear"):
+               similarity="linear", group="sum"):
+    """group: "sum" / "max" (the q-heads of a kv head share one selection scored by the sum / the
+    maximum of their similarities) or "head" (one selection per q-head)."""
     return MpcSelectCfg(cluster_size=cluster, fanout=fanout, k_super=k_super, k_clusters=k_clusters,
                         alpha=alpha, share_period=share_period, share_start=share_start,
-                        similarity=SIMILARITY[similarity])
+                        similarity=SIMILARITY[similarity], group=GROUP[group])
+
+
+def sel_heads(cfg, n_q_heads, n_kv_heads):
+    """Selection lists per (layer, sequence) under the config's group rule."""
+    return n_q_heads if cfg.group == GROUP["head"] else n_kv_heads
 
 
 def _slots(cap, cfg):
@@ -179,7 +188,7 @@ def mpc_build_clusters(k_cache, cent, scent, cfg, *, Ts=None, layer0=0, stream=N
 
 def mpc_select_clusters(q, cent, scent, sel, cfg, *, Ts, sel_score=None, layer0=0, stream=None):
     """q [L][B][Hq][d], cent / scent with Ccap / Scap slots (the first ceil(Ts / s) used) ->
-    sel [L][B][Hkv][k_clusters] (int32, ascending)."""
+    sel [L][B][H][k_clusters] (int32, ascending), H = Hq for the "head" group rule, else Hkv."""
     _contig(q, cent, scent, sel, sel_score)
     dims = dims_of(q, cent, layer0)
     dims.head_dim = q.shape[-1]
@@ -187,6 +196,8 @@ def mpc_select_clusters(q, cent, scent, sel, cfg, *, Ts, sel_score=None, layer0=
     dims.kv_capacity = cent.shape[3] * cfg.cluster_size
     if scent.shape[3] != _slots(dims.kv_capacity, cfg)[1]:
         raise ValueError("scent must have ceil(Ccap / fanout) super-cluster slots")
+    if sel.shape[2] != sel_heads(cfg, q.shape[2], cent.shape[2]):
+        raise ValueError("sel must have one list per q-head for the head rule, per kv head otherwise")
     _check("mpc_select_clusters", lib().mpc_select_clusters(
         ctypes.byref(dims), Ts, ctypes.byref(cfg), _ptr(q), _ptr(cent), _ptr(scent), _ptr(sel), _ptr(sel_score),
         None, 0, _stream(stream)))
@@ -194,16 +205,17 @@ def mpc_select_clusters(q, cent, scent, sel, cfg, *, Ts, sel_score=None, layer0=
 
 def mpc_sparse_decode_attn(q, k_cache, v_cache, sel, out, *, cluster_size, sm_scale, Ts=None, n_tail=0, lse=None,
                            ws=None, layer0=0, stream=None):
-    """q [L][B][Hq][d], k/v [L][B][Hkv][Tcap][d], sel [L][B][Hkv][k] -> out [L][B][Hq][d]. Clustered rows
-    [0, Ts) (Ts = Tcap - n_tail by default) and tail rows [Ts, Ts + n_tail)."""
+    """q [L][B][Hq][d], k/v [L][B][Hkv][Tcap][d], sel [L][B][H][k] (H = Hkv: one list per kv head;
+    H = Hq: one per q-head) -> out [L][B][Hq][d]. Clustered rows [0, Ts) (Ts = Tcap - n_tail by
+    default) and tail rows [Ts, Ts + n_tail)."""
     _contig(q, k_cache, v_cache, sel, out, lse, ws)
     dims = dims_of(q, k_cache, layer0)
     Ts = k_cache.shape[3] - n_tail if Ts is None else Ts
     if ws is None:
         ws = workspace(workspace_bytes(MPC_OP_DECODE_ATTN, dims, Ts), q.device)
     _check("mpc_sparse_decode_attn", lib().mpc_sparse_decode_attn(
-        ctypes.byref(dims), Ts, n_tail, cluster_size, _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(sel), sel.shape[-1],
-        sm_scale, _ptr(out), _ptr(lse), _ptr(ws), ws.numel(), _stream(stream)))
+        ctypes.byref(dims), Ts, n_tail, cluster_size, _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(sel), sel.shape[2],
+        sel.shape[-1], sm_scale, _ptr(out), _ptr(lse), _ptr(ws), ws.numel(), _stream(stream)))
 
 
 def mpc_decode_step(q, cent, scent, k_cache, v_cache, sel, out, cfg, *, sm_scale, Ts=None, n_tail=0, sel_score=None,
@@ -211,7 +223,7 @@ def mpc_decode_step(q, cent, scent, k_cache, v_cache, sel, out, cfg, *, sm_scale
     """Selection of every owner head then sparse attention of every head, in one call.
 
     q [L][B][Hq][d], cent/scent as built, k/v [L][B][Hkv][Tcap][d] (clustered rows [0, Ts), Ts = Tcap - n_tail
-    by default, then the tail) -> sel [L][B][Hkv][k], out [L][B][Hq][d].
+    by default, then the tail) -> sel [L][B][H][k] (H as for mpc_select_clusters), out [L][B][Hq][d].
     ws must come from workspace() (zero-filled) and be reused by later calls of the same shape.
     """
     _contig(q, cent, scent, k_cache, v_cache, sel, out, sel_score, lse, ws)
@@ -223,6 +235,19 @@ def mpc_decode_step(q, cent, scent, k_cache, v_cache, sel, out, cfg, *, sm_scale
         ctypes.byref(dims), Ts, n_tail, ctypes.byref(cfg), _ptr(q), _ptr(cent), _ptr(scent), _ptr(k_cache), _ptr(v_cache),
         sm_scale, _ptr(sel), _ptr(sel_score), _ptr(out), _ptr(lse), _ptr(ws), ws.numel(), _stream(stream)))
     return ws
+
+
+def mpc_commonality(idx, out, m, stream=None):
+    """idx [L][...][k] int32 top-k sets per layer -> out [...] float64: commonality score of m + 1
+    adjacent layers (Sec. 3, Observation 3) for every unit of the middle axes."""
+    _contig(idx, out)
+    if idx.dtype != torch.int32 or out.dtype != torch.float64:
+        raise TypeError("idx must be int32 and out float64")
+    L, k = idx.shape[0], idx.shape[-1]
+    units = idx[0, ..., 0].numel()
+    if out.numel() != units:
+        raise ValueError("out must hold one value per unit")
+    _check("mpc_commonality", lib().mpc_commonality(L, units, k, m, _ptr(idx), _ptr(out), _stream(stream)))
 
 
 def append_state(Ts, n_tail, cluster_size):

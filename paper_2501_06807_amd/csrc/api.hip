@@ -1,10 +1,12 @@
 // C ABI of the MPCache hot path: argument validation, workspace layout, kernel dispatch.
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
 
 #include "append.h"
 #include "clusters.h"
+#include "commonality.h"
 #include "common.h"
 #include "decode_attn.h"
 #include "evict.h"
@@ -86,13 +88,15 @@ EvictWs evict_ws(const mpc_dims* d, int T, int W) {
 }
 
 // Decode workspace: split-K partials, sized for the largest split count any token budget gives,
-// then one arrival counter per unit (zero between launches).
+// then one arrival counter per unit (zero between launches). The attention's work units are the
+// selection lists: one per kv head, or one per q-head (then each unit serves one q-head).
 struct DecodeWs {
   size_t cnt, total;
 };
-DecodeWs decode_ws(const mpc_dims* d) {
-  const int units = d->n_layers * d->batch * d->n_kv_heads;
-  const int G = d->n_q_heads / d->n_kv_heads;
+DecodeWs decode_ws(const mpc_dims* d, bool per_q_head) {
+  const int heads = per_q_head ? d->n_q_heads : d->n_kv_heads;
+  const int units = d->n_layers * d->batch * heads;
+  const int G = d->n_q_heads / heads;
   const mpc::DecodePlan p = mpc::decode_plan(units, 1 << 30, d->head_dim, elt_size(d->dtype));
   DecodeWs w{0, 0};
   if (p.splits <= 1) return w;
@@ -100,7 +104,8 @@ DecodeWs decode_ws(const mpc_dims* d) {
   w.total = w.cnt + align256((size_t)units * sizeof(int));
   return w;
 }
-size_t decode_ws_bytes(const mpc_dims* d) { return decode_ws(d).total; }
+// enough for either layout, so that one size serves every selection rule
+size_t decode_ws_bytes(const mpc_dims* d) { return std::max(decode_ws(d, false).total, decode_ws(d, true).total); }
 
 // Fused decode-step workspace: the error word, per-owner-head state and consumer counts, then the
 // split-K partials used when the block is too small for the fused kernel.
@@ -290,6 +295,7 @@ mpc_status prepare_select(const mpc_dims* dims, int32_t Ts, const mpc_select_cfg
   if (!q || !cent || !scent || !sel) return fail(MPC_EINVAL, "a required tensor pointer is NULL");
   if (cfg->similarity < MPC_SIM_LINEAR || cfg->similarity > MPC_SIM_MEAN)
     return fail(MPC_EINVAL, "unknown similarity %d", cfg->similarity);
+  if (cfg->group < MPC_GROUP_SUM || cfg->group > MPC_GROUP_HEAD) return fail(MPC_EINVAL, "unknown group rule %d", cfg->group);
   const int C = ceil_div(Ts, cfg->cluster_size), S = ceil_div(C, cfg->fanout);
   if (cfg->k_super > S) return fail(MPC_ESHAPE, "k_super %d > super-clusters %d", cfg->k_super, S);
   const int tail = C - (S - 1) * cfg->fanout;
@@ -298,9 +304,8 @@ mpc_status prepare_select(const mpc_dims* dims, int32_t Ts, const mpc_select_cfg
     return fail(MPC_ESHAPE, "k_clusters %d exceeds the smallest candidate set %d", cfg->k_clusters, min_cand);
   if (S > mpc::kSelMaxSuper || (int64_t)cfg->k_super * cfg->fanout > mpc::kSelMaxCand)
     return fail(MPC_EUNSUPPORTED, "selection sizes beyond the kernel limits");
-  const int qrows = cfg->similarity == MPC_SIM_MAXPROD ? dims->n_q_heads / dims->n_kv_heads : 1;
-  if (mpc::select_smem_bytes(dims->head_dim, S, cfg->k_super * cfg->fanout, qrows) > mpc::kMaxLds)
-    return fail(MPC_EUNSUPPORTED, "selection sizes need more LDS than a workgroup has");
+  const bool per_q_head = cfg->group == MPC_GROUP_HEAD;
+  const int Hsel = per_q_head ? dims->n_q_heads : dims->n_kv_heads;
   if (dims->n_layers > mpc::kMaxLayers) return fail(MPC_EUNSUPPORTED, "at most %d layers per call", mpc::kMaxLayers);
   int rows = 0;
   if ((s = cache_rows(dims, Ts, &rows)) != MPC_OK) return s;
@@ -315,6 +320,8 @@ mpc_status prepare_select(const mpc_dims* dims, int32_t Ts, const mpc_select_cfg
   a.n_layers = dims->n_layers;
   a.Hq = dims->n_q_heads;
   a.Hkv = dims->n_kv_heads;
+  a.Hsel = Hsel;
+  a.rep_div = per_q_head ? dims->n_q_heads / dims->n_kv_heads : 1;
   a.C = C;
   a.S = S;
   a.cs = ceil_div(rows, cfg->cluster_size);
@@ -326,14 +333,20 @@ mpc_status prepare_select(const mpc_dims* dims, int32_t Ts, const mpc_select_cfg
   a.period = cfg->share_period;
   a.start = cfg->share_start;
   a.similarity = cfg->similarity;
+  a.group = cfg->group;
   a.own = mpc::owner_table(a.layer0, a.n_layers, a.period, a.start);
+  if (mpc::select_smem_bytes(dims->head_dim, S, a.NC, mpc::select_query_rows(a)) > mpc::kMaxLds)
+    return fail(MPC_EUNSUPPORTED, "selection sizes need more LDS than a workgroup has");
   *out = a;
   return MPC_OK;
 }
 
+// Attention arguments; *units and *G receive the work units (selection lists) of the launch and the
+// q-heads each serves.
 mpc_status prepare_decode(const mpc_dims* dims, int32_t Ts, int32_t n_tail, int32_t cluster_size, const void* q,
-                          const void* k_cache, const void* v_cache, const int32_t* sel, int32_t k_clusters,
-                          float sm_scale, void* out, float* lse, mpc::DecodeArgs* da, mpc::DecodePlan* plan) {
+                          const void* k_cache, const void* v_cache, const int32_t* sel, int32_t sel_heads,
+                          int32_t k_clusters, float sm_scale, void* out, float* lse, mpc::DecodeArgs* da,
+                          mpc::DecodePlan* plan, int* units_out, int* G_out) {
   mpc_status s = check_dims(dims);
   if (s != MPC_OK) return s;
   if (Ts <= 0 || cluster_size <= 0 || k_clusters <= 0)
@@ -342,8 +355,13 @@ mpc_status prepare_decode(const mpc_dims* dims, int32_t Ts, int32_t n_tail, int3
   if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache))
     return fail(MPC_EINVAL, "tensor bases must be 16-byte aligned");
   if (!std::isfinite(sm_scale)) return fail(MPC_EINVAL, "bad sm_scale");
-  const int G = dims->n_q_heads / dims->n_kv_heads;
-  if (G != 1 && G != 2 && G != 4 && G != 8) return fail(MPC_EUNSUPPORTED, "group size %d not in {1,2,4,8}", G);
+  const int Gkv = dims->n_q_heads / dims->n_kv_heads;
+  if (Gkv != 1 && Gkv != 2 && Gkv != 4 && Gkv != 8)
+    return fail(MPC_EUNSUPPORTED, "group size %d not in {1,2,4,8}", Gkv);
+  if (sel_heads != dims->n_kv_heads && sel_heads != dims->n_q_heads)
+    return fail(MPC_ESHAPE, "sel_heads %d is neither n_kv_heads nor n_q_heads", sel_heads);
+  const bool per_q_head = sel_heads != dims->n_kv_heads;
+  const int G = per_q_head ? 1 : Gkv;  // q-heads per work unit
   const int C = ceil_div(Ts, cluster_size);
   if (k_clusters > C) return fail(MPC_ESHAPE, "k_clusters %d > clusters %d", k_clusters, C);
   if (n_tail < 0) return fail(MPC_EINVAL, "n_tail must be >= 0");
@@ -354,7 +372,7 @@ mpc_status prepare_decode(const mpc_dims* dims, int32_t Ts, int32_t n_tail, int3
   const int n_list = k_clusters + ceil_div(n_tail, cluster_size);
   if (n_list > 1024) return fail(MPC_EUNSUPPORTED, "k_clusters plus tail clusters above 1024");
   if ((int64_t)n_list * cluster_size >= ((int64_t)1 << 30)) return fail(MPC_EUNSUPPORTED, "too many tokens");
-  const int units = dims->n_layers * dims->batch * dims->n_kv_heads;
+  const int units = dims->n_layers * dims->batch * sel_heads;
   *plan = mpc::decode_plan(units, n_list * cluster_size, dims->head_dim, elt_size(dims->dtype));
   mpc::DecodeArgs a{};
   a.q = q;
@@ -372,10 +390,14 @@ mpc_status prepare_decode(const mpc_dims* dims, int32_t Ts, int32_t n_tail, int3
   a.C = C;
   a.k_sel = k_clusters;
   a.Hq = dims->n_q_heads;
-  a.Hkv = dims->n_kv_heads;
+  a.Hkv = sel_heads;
+  a.cache_heads = dims->n_kv_heads;
+  a.cache_div = per_q_head ? Gkv : 1;
   a.splits = plan->splits;
   a.qscale = (float)((double)sm_scale * 1.4426950408889634);
   *da = a;
+  *units_out = units;
+  *G_out = G;
   return MPC_OK;
 }
 
@@ -401,22 +423,21 @@ mpc_status mpc_select_clusters(const mpc_dims* dims, int32_t Ts, const mpc_selec
 
 mpc_status mpc_sparse_decode_attn(const mpc_dims* dims, int32_t Ts, int32_t n_tail, int32_t cluster_size,
                                   const void* q, const void* k_cache, const void* v_cache,
-                                  const int32_t* sel, int32_t k_clusters, float sm_scale,
+                                  const int32_t* sel, int32_t sel_heads, int32_t k_clusters, float sm_scale,
                                   void* out, float* lse, void* ws, size_t ws_bytes, void* stream) {
   mpc::DecodeArgs a{};
   mpc::DecodePlan plan{};
-  mpc_status s = prepare_decode(dims, Ts, n_tail, cluster_size, q, k_cache, v_cache, sel, k_clusters, sm_scale, out,
-                                lse, &a, &plan);
+  int units = 0, G = 0;
+  mpc_status s = prepare_decode(dims, Ts, n_tail, cluster_size, q, k_cache, v_cache, sel, sel_heads, k_clusters,
+                                sm_scale, out, lse, &a, &plan, &units, &G);
   if (s != MPC_OK) return s;
   const size_t need = decode_ws_bytes(dims);
   if (plan.splits > 1 && (!ws || ws_bytes < need))
     return fail(MPC_EWORKSPACE, "sparse decode attention needs %zu workspace bytes", need);
   if (plan.splits > 1) {
     a.part = (float*)ws;
-    a.cnt = (int*)((char*)ws + decode_ws(dims).cnt);
+    a.cnt = (int*)((char*)ws + decode_ws(dims, G == 1 && sel_heads != dims->n_kv_heads).cnt);
   }
-  const int units = dims->n_layers * dims->batch * dims->n_kv_heads;
-  const int G = dims->n_q_heads / dims->n_kv_heads;
   clear_stale_error();
   if ((s = launched(mpc::launch_sparse_decode(a, dims->dtype, dims->head_dim, G, units, plan, (hipStream_t)stream),
                     "sparse decode attention")) != MPC_OK)
@@ -434,20 +455,20 @@ mpc_status mpc_decode_step(const mpc_dims* dims, int32_t Ts, int32_t n_tail, con
   if (s != MPC_OK) return s;
   mpc::DecodeArgs da{};
   mpc::DecodePlan plan{};
-  s = prepare_decode(dims, Ts, n_tail, cfg->cluster_size, q, k_cache, v_cache, sel, cfg->k_clusters, sm_scale, out, lse,
-                     &da, &plan);
+  int units = 0, G = 0;
+  s = prepare_decode(dims, Ts, n_tail, cfg->cluster_size, q, k_cache, v_cache, sel, sa.Hsel, cfg->k_clusters,
+                     sm_scale, out, lse, &da, &plan, &units, &G);
   if (s != MPC_OK) return s;
   const StepWs lay = step_ws(dims, cfg);
   if (!ws || ws_bytes < lay.total)
     return fail(MPC_EWORKSPACE, "decode step needs %zu workspace bytes", lay.total);
-  const int units = dims->n_layers * dims->batch * dims->n_kv_heads;
-  const int G = dims->n_q_heads / dims->n_kv_heads;
+  const bool per_q_head = sa.Hsel != dims->n_kv_heads;
   hipStream_t st = (hipStream_t)stream;
   clear_stale_error();
   const mpc::FusedPlan fp = mpc::fused_plan(sa, dims->head_dim);
-  if (plan.splits > 1 || !mpc::fused_fits(fp, dims->head_dim, G)) {  // the two kernels in sequence
+  if (per_q_head || plan.splits > 1 || !mpc::fused_fits(fp, dims->head_dim, G)) {  // two kernels in sequence
     da.part = (float*)((char*)ws + lay.part);
-    da.cnt = (int*)((char*)ws + lay.part + decode_ws(dims).cnt);
+    da.cnt = (int*)((char*)ws + lay.part + decode_ws(dims, per_q_head).cnt);
     if (sa.own.n > 0 &&
         (s = launched(mpc::launch_select(sa, dims->dtype, dims->head_dim, st), "select")) != MPC_OK)
       return s;
@@ -464,6 +485,19 @@ mpc_status mpc_decode_step(const mpc_dims* dims, int32_t Ts, int32_t n_tail, con
   f.cons = (int*)((char*)ws + lay.cons);
   if ((s = launched(mpc::launch_decode_step(f, fp, dims->dtype, dims->head_dim, G, st), "decode step")) != MPC_OK)
     return s;
+  return ok();
+}
+
+mpc_status mpc_commonality(int32_t L, int32_t units, int32_t k, int32_t m, const int32_t* idx, double* out,
+                           void* stream) {
+  if (L <= 0 || units <= 0 || k <= 0 || m < 0) return fail(MPC_EINVAL, "L, units, k must be positive and m >= 0");
+  if (m >= L) return fail(MPC_ESHAPE, "m %d must be below the layer count %d", m, L);
+  if (k > mpc::kCommonMaxK) return fail(MPC_EUNSUPPORTED, "k %d above %d", k, mpc::kCommonMaxK);
+  if ((int64_t)L * units * k >= ((int64_t)1 << 31)) return fail(MPC_EUNSUPPORTED, "index tensor too large");
+  if (!idx || !out) return fail(MPC_EINVAL, "a required tensor pointer is NULL");
+  clear_stale_error();
+  mpc_status s = launched(mpc::launch_commonality(L, units, k, m, idx, out, (hipStream_t)stream), "commonality");
+  if (s != MPC_OK) return s;
   return ok();
 }
 

@@ -8,14 +8,18 @@ constexpr int kMaxSplits = 16;   // split-K limit (workspace bound)
 
 struct DecodeArgs {
   const void* q;       // [L][B][Hq][d]
-  const void* k;       // [L][B][Hkv][rows][d]
+  const void* k;       // [L][B][cache_heads][rows][d]
   const void* v;
-  const int32_t* sel;  // [L][B][Hkv][k_sel]
+  const int32_t* sel;  // [L][B][Hkv][k_sel] (one list per unit)
   void* out;           // [L][B][Hq][d]
   float* lse;          // [L][B][Hq] or null
   float* part;         // split-K partials [units][splits][G][d + 2]
   int* cnt;            // split-K arrival counters [units], zero between launches
-  int Ts, s, C, k_sel, Hq, Hkv, splits;  // C = ceil(Ts / s) selectable clusters
+  int Ts, s, C, k_sel, Hq, splits;  // C = ceil(Ts / s) selectable clusters
+  int Hkv;          // selection lists (work units) per (layer, sequence): the kv heads, or the
+                    // q-heads when every q-head has its own list (then G = 1 per unit)
+  int cache_heads;  // kv heads of the cache per (layer, sequence)
+  int cache_div;    // unit head h reads the rows of cache head h / cache_div
   int rows;            // allocated rows per (layer, sequence, kv head)
   int n_tail;          // rows [Ts, Ts + n_tail) attended by every head (Ts % s == 0 if n_tail > 0)
   float qscale;        // sm_scale * log2(e)

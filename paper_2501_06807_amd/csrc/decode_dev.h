@@ -8,6 +8,13 @@ namespace dev {
 
 constexpr int kMaxSel = 1024;
 
+// Byte offset of a unit's K/V block: (layer, sequence) of the unit, then its cache head.
+template <int D, class DT>
+__device__ __forceinline__ size_t cache_offset(const DecodeArgs& a, int unit) {
+  const size_t cu = (size_t)(unit / a.Hkv) * a.cache_heads + (unit % a.Hkv) / a.cache_div;
+  return cu * a.rows * D * DT::kElt;
+}
+
 // The unit's cluster list in LDS: its selected clusters, with ids outside [0, C) replaced by -1
 // (they contribute nothing), then the clusters C, C + 1, ... that hold the tail rows
 // [Ts, Ts + n_tail) (Ts is a multiple of s when there is a tail). Returns the list length.
@@ -138,8 +145,8 @@ __device__ __forceinline__ void attend_unit(const DecodeArgs& a, int unit, int s
   const int n_slot = n_list * a.s, rows_end = a.Ts + a.n_tail;
   const int chunk = (n_slot + a.splits - 1) / a.splits;
   const int lo = split * chunk, hi = min(n_slot, lo + chunk);
-  const char* kbase = (const char*)a.k + (size_t)unit * a.rows * D * DT::kElt;
-  const char* vbase = (const char*)a.v + (size_t)unit * a.rows * D * DT::kElt;
+  const char* kbase = (const char*)a.k + cache_offset<D, DT>(a, unit);
+  const char* vbase = (const char*)a.v + cache_offset<D, DT>(a, unit);
 
   float m[G], l[G], acc[G][EPL];
 #pragma unroll
@@ -338,8 +345,8 @@ __device__ __forceinline__ void attend_unit_g4(const DecodeArgs& a, int unit, in
   const int n_slot = n_list * a.s, rows_end = a.Ts + a.n_tail;
   const int chunk = (n_slot + a.splits - 1) / a.splits;
   const int lo = split * chunk, hi = min(n_slot, lo + chunk);
-  const char* kbase = (const char*)a.k + (size_t)unit * a.rows * D * DT::kElt;
-  const char* vbase = (const char*)a.v + (size_t)unit * a.rows * D * DT::kElt;
+  const char* kbase = (const char*)a.k + cache_offset<D, DT>(a, unit);
+  const char* vbase = (const char*)a.v + cache_offset<D, DT>(a, unit);
 
   // slot cursors (cluster position, row), advanced by STEP slots per step without a division:
   // [0] the score-layout token of this lane, [1 + u] its row-layout rows

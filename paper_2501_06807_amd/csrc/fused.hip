@@ -22,7 +22,7 @@ namespace {
 constexpr int kFusedWaves = 8;
 constexpr int kSpinLimit = 1 << 20;  // polls (each ~0.1-1 us) before a unit gives up
 
-template <class DT, int D, int G, bool MP>
+template <class DT, int D, int G, bool MP, bool GMAX>
 __global__ __launch_bounds__(kFusedWaves* kWave) void k_decode_step(FusedArgs f) {
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ int s_mode;  // 1 select then attend, 2 attend, 0 gave up
@@ -61,7 +61,7 @@ __global__ __launch_bounds__(kFusedWaves* kWave) void k_decode_step(FusedArgs f)
   if (mode == 1) {
     // one row pass in flight per wave and the query in LDS keep the selection's registers near
     // the attention's
-    dev::select_block<DT, D, kFusedWaves, true, 1, MP, false>(sa, head, smem);
+    dev::select_block<DT, D, kFusedWaves, true, 1, MP, false, GMAX>(sa, head, smem);
     __builtin_amdgcn_s_waitcnt(0);  // this thread's selection stores have completed
     __syncthreads();
     if (tid == 0) __hip_atomic_store(&f.state[head], 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -85,10 +85,20 @@ __global__ __launch_bounds__(kFusedWaves* kWave) void k_decode_step(FusedArgs f)
 template <class DT, int D, int G>
 hipError_t launch_g(const FusedArgs& f, size_t smem, hipStream_t st) {
   const dim3 grid(f.s.n_layers * f.s.B * f.s.Hkv), block(kFusedWaves * kWave);
-  if (f.s.similarity == MPC_SIM_MAXPROD)
-    hipLaunchKernelGGL((k_decode_step<DT, D, G, true>), grid, block, smem, st, f);
+  const bool mp = f.s.similarity == MPC_SIM_MAXPROD;
+  if constexpr (G > 1) {
+    if (f.s.group == MPC_GROUP_MAX) {
+      if (mp)
+        hipLaunchKernelGGL((k_decode_step<DT, D, G, true, true>), grid, block, smem, st, f);
+      else
+        hipLaunchKernelGGL((k_decode_step<DT, D, G, false, true>), grid, block, smem, st, f);
+      return hipGetLastError();
+    }
+  }
+  if (mp)
+    hipLaunchKernelGGL((k_decode_step<DT, D, G, true, false>), grid, block, smem, st, f);
   else
-    hipLaunchKernelGGL((k_decode_step<DT, D, G, false>), grid, block, smem, st, f);
+    hipLaunchKernelGGL((k_decode_step<DT, D, G, false, false>), grid, block, smem, st, f);
   return hipGetLastError();
 }
 
@@ -115,7 +125,7 @@ hipError_t launch_dt(const FusedArgs& f, int D, int G, size_t smem, hipStream_t 
 FusedPlan fused_plan(const SelectArgs& s, int D) {
   FusedPlan p{};
   p.units = s.n_layers * s.B * s.Hkv;
-  p.smem = dev::select_smem_bytes_dev(D, s.S, s.NC, s.similarity == MPC_SIM_MAXPROD ? s.Hq / s.Hkv : 1);
+  p.smem = dev::select_smem_bytes_dev(D, s.S, s.NC, select_query_rows(s));
   return p;
 }
 

@@ -147,14 +147,50 @@ __device__ __forceinline__ void tile_dot_mp(const RowTile<2 * D, PASS>& t, int n
   }
 }
 
+// Largest per-head similarity of a loaded tile over the G heads, qh = [G][D] (LDS): the dot
+// product (MPB false) or the max-product bound of two-row representatives (MPB true). Each head's
+// sum is complete (quad-reduced) before the maximum is taken.
+template <int D, int PASS, bool MPB>
+__device__ __forceinline__ void tile_dot_gmax(const RowTile<MPB ? 2 * D : D, PASS>& t, int n, int r0,
+                                              const double* qh, int G, double* scores, uint32_t* img,
+                                              unsigned long long* ck) {
+  constexpr int ROWS = kWave / 4;
+  const int lane = threadIdx.x % kWave, rq = lane >> 2, qk = lane & 3;
+#pragma unroll
+  for (int p = 0; p < PASS; ++p) {
+    double best = -INFINITY;
+    for (int g = 0; g < G; ++g) {
+      const double* qg = qh + g * D;
+      double acc = 0.0;
+#pragma unroll
+      for (int c = 0; c < D / 16; ++c) {
+        const double2 q01 = *(const double2*)(qg + c * 16 + qk * 4);
+        const double2 q23 = *(const double2*)(qg + c * 16 + qk * 4 + 2);
+        const float4 x = t.x[p][c];
+        if constexpr (MPB) {
+          const float4 lo = t.x[p][c + D / 16];
+          acc += fmax(q01.x * (double)x.x, q01.x * (double)lo.x) + fmax(q01.y * (double)x.y, q01.y * (double)lo.y) +
+                 fmax(q23.x * (double)x.z, q23.x * (double)lo.z) + fmax(q23.y * (double)x.w, q23.y * (double)lo.w);
+        } else {
+          acc += q01.x * (double)x.x + q01.y * (double)x.y + q23.x * (double)x.z + q23.y * (double)x.w;
+        }
+      }
+      best = fmax(best, group_sum<4>(acc));
+    }
+    put_score(best, t.valid[p], r0 + p * ROWS + rq, n, scores, img, ck);
+  }
+}
+
 // Scoring of one mode: dot-product modes (linear, average) take the group's summed query (from
 // registers if QREG, else from LDS), the max-product bound the G separate queries (LDS) and
-// two-row representatives (one row pass in flight).
-template <int D, int PASS, bool MP, bool QREG = true>
+// two-row representatives (one row pass in flight). GMAX: the maximum over the G heads' own
+// similarities instead of their sum (separate queries in LDS).
+template <int D, int PASS, bool MP, bool QREG = true, bool GMAX = false>
 struct Scoring {
   static constexpr int RW = MP ? 2 * D : D;  // floats per representative
   static constexpr int P = MP ? 1 : PASS;    // row passes per wave
-  static constexpr bool kReg = QREG && !MP;
+  static constexpr bool kSep = MP || GMAX;   // one query row per head
+  static constexpr bool kReg = QREG && !kSep;
   using Tile = RowTile<RW, P>;
   struct Empty {};
   struct Query {
@@ -170,7 +206,9 @@ struct Scoring {
   }
   __device__ static void dot(const Tile& t, int n, int r0, const Query& q, double* scores, uint32_t* img,
                              unsigned long long* ck) {
-    if constexpr (MP)
+    if constexpr (GMAX)
+      tile_dot_gmax<D, P, MP>(t, n, r0, q.lds, q.G, scores, img, ck);
+    else if constexpr (MP)
       tile_dot_mp<D, P>(t, n, r0, q.lds, q.G, scores, img, ck);
     else if constexpr (kReg)
       tile_dot<D, P>(t, n, r0, q.reg, scores, img, ck);
@@ -179,10 +217,10 @@ struct Scoring {
   }
 };
 
-// Query rows kept in LDS: the group sum (dot modes) or each of the G heads (bound), fp64.
-template <class DT, int D, bool MP>
+// Query rows kept in LDS: the group sum (SEP false) or each of the G heads (SEP true), fp64.
+template <class DT, int D, bool SEP>
 __device__ __forceinline__ void load_query(const void* q, size_t q0, int G, double* dst, int t0, int nt) {
-  if constexpr (MP) {
+  if constexpr (SEP) {
     for (int i = t0; i < G * D; i += nt) dst[i] = (double)load_elt<DT>(q, q0 + (size_t)i);
   } else {
     for (int i = t0; i < D; i += nt) {
@@ -318,8 +356,8 @@ __device__ __forceinline__ void emit_selection(const SelectArgs& a, const int* t
   const int abs_l = a.layer0 + l;
   int l_end = l + 1;  // layers [l, l_end) of the call use this selection
   while (l_end < a.n_layers && owner_layer(a.layer0 + l_end, a.period, a.start) == abs_l) ++l_end;
-  const size_t stride = (size_t)a.B * a.Hkv * a.k_clusters;
-  const size_t o0 = (((size_t)l * a.B + b) * a.Hkv + h) * a.k_clusters;
+  const size_t stride = (size_t)a.B * a.Hsel * a.k_clusters;
+  const size_t o0 = (((size_t)l * a.B + b) * a.Hsel + h) * a.k_clusters;
   for (int j = t0; j < a.k_clusters; j += nt) {
     const int i = top[j], p = ascending_pos(top, a.k_clusters, j);
     const int c = cand[i];
@@ -358,14 +396,15 @@ __host__ __device__ inline BlockLds block_lds(int D, int S, int NC, int qrows) {
 // COH: write the selection with device-coherent stores (read by another workgroup of the launch).
 // PASS: row passes per wave in flight (registers against memory parallelism). MP: max-product
 // bound scores (two-row representatives), else dot-product scores. QREG: keep the summed query in
-// registers (faster) rather than reading it from LDS at every row (fewer registers).
-template <class DT, int D, int NW, bool COH, int PASS = 2, bool MP = false, bool QREG = true>
+// registers (faster) rather than reading it from LDS at every row (fewer registers). GMAX: the
+// unit's score is the maximum of its q-heads' similarities, not their sum.
+template <class DT, int D, int NW, bool COH, int PASS = 2, bool MP = false, bool QREG = true, bool GMAX = false>
 __device__ void select_block(const SelectArgs& a, int ou, unsigned char* smem) {
-  using SC = Scoring<D, PASS, MP, QREG>;
+  using SC = Scoring<D, PASS, MP, QREG, GMAX>;
   constexpr int NT = NW * kWave;
   constexpr int TILE = NW * (kWave / 4) * SC::P;  // rows per workgroup pass
-  const int G = a.Hq / a.Hkv;
-  const BlockLds lay = block_lds(D, a.S, a.NC, MP ? G : 1);
+  const int G = a.Hq / a.Hsel;  // q-heads of the unit
+  const BlockLds lay = block_lds(D, a.S, a.NC, SC::kSep ? G : 1);
   double* qsum = (double*)(smem + lay.qsum);
   double* s1 = (double*)(smem + lay.s1);
   double* s2 = (double*)(smem + lay.s2);
@@ -378,9 +417,9 @@ __device__ void select_block(const SelectArgs& a, int ou, unsigned char* smem) {
   int* cand = (int*)(smem + lay.cand);
   __shared__ int bnd1[2], bnd2[2];
 
-  const int BH = a.B * a.Hkv;
-  const int l = a.own.l[ou / BH], b = (ou / a.Hkv) % a.B, h = ou % a.Hkv;
-  const size_t unit = (size_t)l * BH + ou % BH;
+  const int BH = a.B * a.Hsel;
+  const int l = a.own.l[ou / BH], b = (ou / a.Hsel) % a.B, h = ou % a.Hsel;
+  const size_t unit = ((size_t)l * a.B + b) * a.Hkv + h / a.rep_div;  // representatives' kv head
   const int tid = threadIdx.x, w = tid / kWave;
   const float* scent = a.scent + unit * a.ss * SC::RW;
   const float* cent = a.cent + unit * a.cs * SC::RW;
@@ -390,7 +429,7 @@ __device__ void select_block(const SelectArgs& a, int ou, unsigned char* smem) {
   const int r1 = w * (TILE / NW);
   if (r1 < a.S) tile_load<SC::RW, SC::P>(scent, nullptr, a.S, r1, tile);
   const size_t q0 = (((size_t)l * a.B + b) * a.Hq + (size_t)h * G) * D;
-  load_query<DT, D, MP>(a.q, q0, G, qsum, tid, NT);
+  load_query<DT, D, SC::kSep>(a.q, q0, G, qsum, tid, NT);
   if (tid < 2) {
     bnd1[tid] = -1;
     bnd2[tid] = -1;
@@ -496,16 +535,16 @@ __host__ __device__ inline size_t wave_region_bytes(int D, int S, int NC, int qr
 }
 
 // Selection of owner heads ou0 + w, one per wave w (`smem`: waves x wave_region_bytes()).
-template <class DT, int D, bool COH, bool MP = false>
+template <class DT, int D, bool COH, bool MP = false, bool GMAX = false>
 __device__ void select_waves(const SelectArgs& a, int ou0, unsigned char* smem) {
-  using SC = Scoring<D, 2, MP>;
+  using SC = Scoring<D, 2, MP, true, GMAX>;
   constexpr int TILE = (kWave / 4) * SC::P;  // rows per wave pass
   const int lane = threadIdx.x % kWave, w = threadIdx.x / kWave;
-  const int BH = a.B * a.Hkv;
-  const int ou = ou0 + w;  // (owner index * B + b) * Hkv + h
+  const int BH = a.B * a.Hsel;
+  const int ou = ou0 + w;  // (owner index * B + b) * Hsel + h
   if (ou >= a.own.n * BH) return;
-  const int G = a.Hq / a.Hkv;
-  const WaveLds lay = wave_lds(D, a.S, a.NC, MP ? G : 1);
+  const int G = a.Hq / a.Hsel;  // q-heads of the unit
+  const WaveLds lay = wave_lds(D, a.S, a.NC, SC::kSep ? G : 1);
   unsigned char* base = smem + (size_t)w * lay.total;
   double* qsum = (double*)(base + lay.qsum);
   double* s1 = (double*)(base + lay.s1);
@@ -515,8 +554,8 @@ __device__ void select_waves(const SelectArgs& a, int ou0, unsigned char* smem) 
   int* top = (int*)(base + lay.top);
   int* cand = (int*)(base + lay.cand);
 
-  const int l = a.own.l[ou / BH], b = (ou / a.Hkv) % a.B, h = ou % a.Hkv;
-  const size_t unit = (size_t)l * BH + ou % BH;
+  const int l = a.own.l[ou / BH], b = (ou / a.Hsel) % a.B, h = ou % a.Hsel;
+  const size_t unit = ((size_t)l * a.B + b) * a.Hkv + h / a.rep_div;  // representatives' kv head
   const float* scent = a.scent + unit * a.ss * SC::RW;
   const float* cent = a.cent + unit * a.cs * SC::RW;
 
@@ -524,7 +563,7 @@ __device__ void select_waves(const SelectArgs& a, int ou0, unsigned char* smem) 
   typename SC::Tile tile;
   tile_load<SC::RW, SC::P>(scent, nullptr, a.S, 0, tile);
   const size_t q0 = (((size_t)l * a.B + b) * a.Hq + (size_t)h * G) * D;
-  load_query<DT, D, MP>(a.q, q0, G, qsum, lane, kWave);
+  load_query<DT, D, SC::kSep>(a.q, q0, G, qsum, lane, kWave);
   wave_sync();
   typename SC::Query qr;
   SC::prepare(qr, qsum, G);

@@ -19,7 +19,7 @@ class MPCachePath:
     def __init__(self, *, n_layers, batch, n_q_heads, n_kv_heads, head_dim, dtype, T, window, keep,
                  local_keep, cluster, fanout, k_super, k_clusters, share_period, share_start=2,
                  alpha=0.6, causal=True, layer0=0, device="cuda", keep_scores=False, similarity="linear",
-                 capacity=None):
+                 group="sum", capacity=None):
         self.L, self.B, self.Hq, self.Hkv, self.d = n_layers, batch, n_q_heads, n_kv_heads, head_dim
         self.dtype, self.T, self.W, self.keep = dtype, T, window, keep
         self.local_keep, self.causal, self.layer0 = local_keep, causal, layer0
@@ -33,7 +33,9 @@ class MPCachePath:
         self.S = -(-self.C // fanout)
         n_c = -(-self.rows // cluster)
         self.Ts, self.n_tail = keep, 0
-        self.cfg = L.select_cfg(cluster, fanout, k_super, k_clusters, alpha, share_period, share_start, similarity)
+        self.cfg = L.select_cfg(cluster, fanout, k_super, k_clusters, alpha, share_period, share_start, similarity,
+                                group)
+        self.Hsel = L.sel_heads(self.cfg, n_q_heads, n_kv_heads)  # selection lists per (layer, sequence)
         R = L.rep_rows(similarity)
         rep = (R, head_dim) if R > 1 else (head_dim,)
         dev = torch.device(device)
@@ -43,8 +45,8 @@ class MPCachePath:
         self.v_s = torch.empty_like(self.k_s)
         self.cent = torch.zeros(*kv_shape, n_c, *rep, dtype=torch.float32, device=dev)
         self.scent = torch.zeros(*kv_shape, -(-n_c // fanout), *rep, dtype=torch.float32, device=dev)
-        self.sel = torch.zeros(*kv_shape, k_clusters, dtype=torch.int32, device=dev)
-        self.sel_score = torch.zeros(*kv_shape, k_clusters, dtype=torch.float32, device=dev)
+        self.sel = torch.zeros(n_layers, batch, self.Hsel, k_clusters, dtype=torch.int32, device=dev)
+        self.sel_score = torch.zeros(n_layers, batch, self.Hsel, k_clusters, dtype=torch.float32, device=dev)
         self.out = torch.empty(n_layers, batch, n_q_heads, head_dim, dtype=dtype, device=dev)
         self.lse = torch.empty(n_layers, batch, n_q_heads, dtype=torch.float32, device=dev)
         self.token_score = (torch.zeros(*kv_shape, T, dtype=torch.float32, device=dev)
@@ -77,8 +79,8 @@ class MPCachePath:
         self._select_args = (ctypes.byref(kvd), Ts, ctypes.byref(self.cfg))
         self._select_tail = (P(self.cent), P(self.scent), P(self.sel), P(self.sel_score), None, 0)
         self._attend_args = (ctypes.byref(kvd), Ts, nt, self.cluster)
-        self._attend_mid = (P(self.k_s), P(self.v_s), P(self.sel), self.k_clusters, self.sm_scale, P(self.out),
-                            P(self.lse), P(self.ws_decode), self.ws_decode.numel())
+        self._attend_mid = (P(self.k_s), P(self.v_s), P(self.sel), self.Hsel, self.k_clusters, self.sm_scale,
+                            P(self.out), P(self.lse), P(self.ws_decode), self.ws_decode.numel())
         self._step_args = (ctypes.byref(kvd), Ts, nt, ctypes.byref(self.cfg))
         self._step_tail = (P(self.cent), P(self.scent), P(self.k_s), P(self.v_s), self.sm_scale, P(self.sel),
                            P(self.sel_score), P(self.out), P(self.lse), P(self.ws_step), self.ws_step.numel())

@@ -89,22 +89,53 @@ def test_unknown_similarity_is_rejected_before_any_launch():
     assert s == L.MPC_EINVAL and "similarity" in msg
 
 
+def test_unknown_group_rule_is_rejected_before_any_launch():
+    d = _dims()
+    cfg = L.select_cfg(32, 4, 2, 6)
+    cfg.group = 3
+    s, msg = _status("mpc_select_clusters", ctypes.byref(d), 300, ctypes.byref(cfg), FAKE, FAKE, FAKE, FAKE, None,
+                     None, 0, None)
+    assert s == L.MPC_EINVAL and "group" in msg
+
+
+def test_commonality_validation():
+    call = lambda L_, u, k, m, idx=FAKE, out=FAKE: _status("mpc_commonality", L_, u, k, m, idx, out, None)
+    s, msg = call(4, 3, 5, 4)
+    assert s == L.MPC_ESHAPE and "m " in msg          # m must be below L
+    assert call(4, 3, 5, -1)[0] == L.MPC_EINVAL
+    assert call(0, 3, 5, 0)[0] == L.MPC_EINVAL
+    assert call(4, 3, 1025, 1)[0] == L.MPC_EUNSUPPORTED
+    assert call(4, 3, 5, 1, idx=None)[0] == L.MPC_EINVAL
+
+
 def test_decode_validation_and_workspace():
     d = _dims(n_layers=1, n_q_heads=8, n_kv_heads=8)
-    s, _ = _status("mpc_sparse_decode_attn", ctypes.byref(d), 256, 0, 16, FAKE, FAKE, FAKE, FAKE, 17, 0.1,
+    s, _ = _status("mpc_sparse_decode_attn", ctypes.byref(d), 256, 0, 16, FAKE, FAKE, FAKE, FAKE, 8, 17, 0.1,
                    FAKE, None, None, 0, None)
     assert s == L.MPC_ESHAPE  # 17 clusters > C = 16
     d3 = _dims(n_layers=1, n_q_heads=24, n_kv_heads=8)
-    s, _ = _status("mpc_sparse_decode_attn", ctypes.byref(d3), 256, 0, 16, FAKE, FAKE, FAKE, FAKE, 4, 0.1,
+    s, _ = _status("mpc_sparse_decode_attn", ctypes.byref(d3), 256, 0, 16, FAKE, FAKE, FAKE, FAKE, 8, 4, 0.1,
                    FAKE, None, None, 0, None)
     assert s == L.MPC_EUNSUPPORTED  # group of 3
+    # one list per kv head (2) or per q-head (8); anything else is a shape error
+    d4 = _dims(n_layers=1, n_q_heads=8, n_kv_heads=2)
+    s, msg = _status("mpc_sparse_decode_attn", ctypes.byref(d4), 256, 0, 16, FAKE, FAKE, FAKE, FAKE, 4, 4, 0.1,
+                     FAKE, None, None, 0, None)
+    assert s == L.MPC_ESHAPE and "sel_heads" in msg
     # few units and enough tokens -> split-K -> a workspace is required (validation fails before
     # any launch, so the fake pointers are never used)
     need = L.workspace_bytes(L.MPC_OP_DECODE_ATTN, d, 256)
     assert need > 0
-    s, msg = _status("mpc_sparse_decode_attn", ctypes.byref(d), 256, 0, 16, FAKE, FAKE, FAKE, FAKE, 16, 0.1,
+    s, msg = _status("mpc_sparse_decode_attn", ctypes.byref(d), 256, 0, 16, FAKE, FAKE, FAKE, FAKE, 8, 16, 0.1,
                      FAKE, None, None, 0, None)
     assert s == L.MPC_EWORKSPACE and str(need) in msg
+    # the workspace size serves one list per kv head and one per q-head alike
+    g = _dims(n_layers=1, n_q_heads=8, n_kv_heads=2)
+    need_g = L.workspace_bytes(L.MPC_OP_DECODE_ATTN, g, 256)
+    for heads in (2, 8):
+        s, msg = _status("mpc_sparse_decode_attn", ctypes.byref(g), 256, 0, 16, FAKE, FAKE, FAKE, FAKE, heads, 16,
+                         0.1, FAKE, None, None, 0, None)
+        assert s == L.MPC_EWORKSPACE and str(need_g) in msg
     # many units -> no split -> no workspace
     big = _dims(n_layers=32, batch=4, n_q_heads=32, n_kv_heads=32)
     assert L.workspace_bytes(L.MPC_OP_DECODE_ATTN, big, 9824) == 0
@@ -188,7 +219,7 @@ def test_append_validation():
 def test_capacity_and_tail_validation():
     d = _dims(n_layers=1, n_q_heads=8, n_kv_heads=8)
     attn = lambda dd, Ts, nt, k=4: _status("mpc_sparse_decode_attn", ctypes.byref(dd), Ts, nt, 16, FAKE, FAKE,
-                                           FAKE, FAKE, k, 0.1, FAKE, None, None, 0, None)
+                                           FAKE, FAKE, 8, k, 0.1, FAKE, None, None, 0, None)
     assert attn(d, 250, 3)[0] == L.MPC_ESHAPE             # a tail after a partial cluster
     assert attn(d, 256, -2)[0] == L.MPC_EINVAL
     assert attn(_dims(n_layers=1, n_q_heads=8, n_kv_heads=8, kv_capacity=260), 256, 5)[0] == L.MPC_ESHAPE
