@@ -39,6 +39,9 @@ def parse():
     p.add_argument("--similarity", choices=("linear", "maxprod", "mean"), default="linear",
                    help="cluster similarity: the paper's linear form (default), the max-product bound (Eq. 2) "
                         "or the cluster average")
+    p.add_argument("--group", choices=("sum", "max", "head"), default="sum",
+                   help="grouped q-heads: one selection per kv head scored by the sum (default) or the maximum of "
+                        "its q-heads' similarities, or one selection per q-head")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--copy-calibration", action="store_true",
                    help="accepted for recorded profiling commands; the 1 GiB reference copy always runs")
@@ -74,16 +77,17 @@ def measured_traffic(kernel, workload, digest):
 def decode_bytes(w, owners, sel, C, S, rep_rows=1):
     """Algorithmic bytes of one decode step: reads of representatives (rep_rows rows of d floats
     each), queries, gathered K/V rows and selections; writes of selections and outputs. Every
-    byte is counted once."""
-    G, d, e = w.group, w.head_dim, w.elt
+    byte is counted once. sel [L][B][H][k] has one list per kv head or one per q-head."""
+    d, e = w.head_dim, w.elt
+    H = sel.shape[2]  # selection lists per (layer, sequence)
+    Gu = w.n_q_heads // H  # q-heads per list
     n_own = len(owners)
-    sel_read = n_own * w.batch * w.n_kv_heads * ((S + w.k_super * w.fanout) * rep_rows * d * 4 + G * d * e)
-    sel_write = w.n_layers * w.batch * w.n_kv_heads * w.k_clusters * 8
+    sel_read = n_own * w.batch * H * ((S + w.k_super * w.fanout) * rep_rows * d * 4 + Gu * d * e)
+    sel_write = w.n_layers * w.batch * H * w.k_clusters * 8
     # exact gathered token count (a partial last cluster holds fewer rows)
     last = w.keep - (C - 1) * w.cluster
-    n_tok = int(w.n_layers * w.batch * w.n_kv_heads * w.k_clusters * w.cluster
-                - (sel == C - 1).sum() * (w.cluster - last))
-    attn_read = n_tok * d * e * 2 + w.n_layers * w.batch * (w.n_q_heads * d * e + w.n_kv_heads * w.k_clusters * 4)
+    n_tok = int(w.n_layers * w.batch * H * w.k_clusters * w.cluster - (sel == C - 1).sum() * (w.cluster - last))
+    attn_read = n_tok * d * e * 2 + w.n_layers * w.batch * (w.n_q_heads * d * e + H * w.k_clusters * 4)
     attn_write = w.n_layers * w.batch * w.n_q_heads * (d * e + 4)
     return sel_read + sel_write, attn_read + attn_write
 
@@ -94,7 +98,7 @@ def prefill_flops(w, n_owner):
     return n_owner * w.batch * w.n_q_heads * rows * 2 * w.head_dim
 
 
-def cpu_baseline(w, n_steps_sample, similarity="linear", min_seconds=10.0, max_seconds=30.0):
+def cpu_baseline(w, n_steps_sample, similarity="linear", group="sum", min_seconds=10.0, max_seconds=30.0):
     """The oracle's decode step (selection + sparse attention) on a sample of the workload: one
     sharing block of layers (2..2+P-1), every sequence and head, `n_steps_sample` fresh queries,
     repeated until at least `min_seconds` of CPU work (stopping at the first pass past
@@ -124,7 +128,7 @@ def cpu_baseline(w, n_steps_sample, similarity="linear", min_seconds=10.0, max_s
             sel, _ = oracle.select_clusters(q, cent, scent, w.dtype, Ts=w.keep, cluster=w.cluster, fanout=w.fanout,
                                             k_super=w.k_super, k_clusters=w.k_clusters, layer0=layer0,
                                             share_period=w.share_period, share_start=w.share_start,
-                                            similarity=similarity)
+                                            similarity=similarity, group=group)
             oracle.sparse_decode_attn(q, k, v, sel, w.dtype, cluster=w.cluster, sm_scale=sm)
             steps += 1
             if time.perf_counter() - t0 > max_seconds:
@@ -137,6 +141,35 @@ def cpu_baseline(w, n_steps_sample, similarity="linear", min_seconds=10.0, max_s
             "sample": f"{ws.name}: layers {layer0}..{layer0 + n_l - 1} (one sharing block), all {w.batch} "
                       f"sequences x {w.n_kv_heads} kv heads, {steps} decode steps over {len(qs)} distinct "
                       f"queries (selection + sparse attention), fp64, {dt:.2f} s total"}
+
+
+def commonality(w, path, q, args, M, torch, dev, mk):
+    """Commonality score (m = 1, 2, 3) of the per-layer selections made without sharing, and the
+    commonality kernel's time."""
+    cfg = M.select_cfg(w.cluster, w.fanout, w.k_super, w.k_clusters, 0.6, 1, w.share_start,
+                       similarity=args.similarity, group=args.group)
+    cent = torch.zeros_like(path.cent)
+    scent = torch.zeros_like(path.scent)
+    M.mpc_build_clusters(path.k_s, cent, scent, cfg, Ts=w.keep)
+    sel = torch.zeros_like(path.sel)
+    M.mpc_select_clusters(q, cent, scent, sel, cfg, Ts=w.keep)
+    out = torch.zeros(sel.shape[1] * sel.shape[2], dtype=torch.float64, device=dev)
+    res = {}
+    for m in (1, 2, 3):
+        M.mpc_commonality(sel, out, m)
+        res[f"m{m}"] = round(out.mean().item(), 4)
+    a, b = mk(), mk()
+    a.record()
+    for _ in range(10):
+        M.mpc_commonality(sel, out, 1)
+    b.record()
+    torch.cuda.synchronize()
+    res["kernel_us"] = round(a.elapsed_time(b) / 10 * 1e3, 3)
+    res["chance_level"] = round(w.k_clusters / path.C, 4)
+    res["note"] = ("mean over (sequence, selection list) of the share of top-k clusters common to m+1 adjacent "
+                   "layers, each layer selecting on its own (no sharing); the workloads' decode queries are "
+                   "independent across layers, so it stays near chance (k / C)")
+    return res
 
 
 def main():
@@ -182,7 +215,7 @@ def main():
                          head_dim=w.head_dim, dtype=synth.torch_dtype(w.dtype), T=w.T, window=w.window,
                          keep=w.keep, local_keep=w.local_keep, cluster=w.cluster, fanout=w.fanout,
                          k_super=w.k_super, k_clusters=w.k_clusters, share_period=w.share_period,
-                         share_start=w.share_start, similarity=args.similarity)
+                         share_start=w.share_start, similarity=args.similarity, group=args.group)
     torch.cuda.synchronize()
 
     fused = args.decode_mode == "fused"
@@ -289,6 +322,10 @@ def main():
                        "(last decode step, every layer, sequence and query head)"}
     del all_sel, out_all, lse_all, ws_all
 
+    # commonality of adjacent layers' unshared selections (Sec. 3, Observation 3) on the last
+    # step's queries: representatives of every layer, one selection per layer, then the score
+    common = commonality(w, path, qs[E - 1], args, M, torch, dev, mk)
+
     owners = [l for l in range(w.n_layers) if M.owner_layer(l, w.share_period, w.share_start) == l]
     sel_b, att_b = decode_bytes(w, owners, path.sel.cpu().numpy(), path.C, path.S, M.rep_rows(args.similarity))
     step_b = sel_b + att_b
@@ -327,7 +364,7 @@ def main():
                    "q_heads": w.n_q_heads, "kv_heads": w.n_kv_heads, "head_dim": w.head_dim, "prompt_tokens": w.T,
                    "window_rows": w.window, "kept_tokens": w.keep, "cluster": w.cluster, "fanout": w.fanout,
                    "k_super": w.k_super, "k_clusters": w.k_clusters, "share_period": w.share_period,
-                   "similarity": args.similarity, "decode_steps_per_pass": E},
+                   "similarity": args.similarity, "group": args.group, "decode_steps_per_pass": E},
         "decode_step": {"mode": args.decode_mode, "us": round(dec_us, 3), "algorithmic_bytes": step_b,
                         "achieved_GBps": round(dec_gbs, 1), "frac_of_hbm_peak": round(dec_gbs / HBM_PEAK_GBS, 4)},
         "kernels": {"select_us": round(sel_us, 3), "attention_us": round(att_us, 3),
@@ -338,6 +375,7 @@ def main():
         "decode_step_other_mode": alt,
         "decode_step_cache": cache,
         "selection_quality": quality,
+        "commonality": common,
         "roofline": roofline,
         "copy_ceiling": {"GBps": round(copy_gbs, 1), "frac_of_peak": round(copy_gbs / HBM_PEAK_GBS, 4),
                          "note": "1 GiB device-to-device copy, read + write bytes"},
@@ -349,7 +387,7 @@ def main():
                     "note": "static eviction (two score passes, top-k, gather) + cluster build, all layers"},
     }
     if not args.no_cpu_baseline:
-        rec["cpu_baseline"] = cpu_baseline(w, min(E, 64), args.similarity)
+        rec["cpu_baseline"] = cpu_baseline(w, min(E, 64), args.similarity, args.group)
     print(json.dumps(rec), flush=True)
 
 
