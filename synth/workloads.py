@@ -1,4 +1,6 @@
-"""The five synthetic workloads (C1..C5) with every integer the method needs written out.
+"""The synthetic workloads with every integer the method needs written out: the five stated
+workloads C1..C5, and X1, short summarization prompts with the paper's small clusters (cluster
+size 8 at the coarse level and 4 at the fine level, i.e. fine clusters of 4 tokens, fan-out 2).
 
 Budgets are given as ratios in the workload descriptions; the integers below follow the rounding
 readings documented with the oracle (window rows, kept tokens as whole clusters, level-1 keeps
@@ -95,6 +97,14 @@ WORKLOADS = {
         local_keep=32, cluster=64, fanout=8, k_super=32, k_clusters=10, share_period=4, steps=32,
         static_ratio=0.25, dynamic_ratio=0.02, seed=SEED_BASE + 4, n_outlier=4, outlier_scale=8.0,
         rope=True, n_sinks=8, hh_count=64, hh_span=128, hh_lo=8, hh_hi=131072 - 32),
+    # short summarization prompts (the paper's XSUM setting: coarse clusters of 8 tokens over fine
+    # clusters of 4, a 10% budget, pairs of layers sharing), 8 independent sequences
+    "X1": Workload(
+        name="xsum-llama2-7b-32L-32H-d128-B8-T1024-bf16", n_layers=32, batch=8, n_q_heads=32,
+        n_kv_heads=32, head_dim=128, dtype="bf16", T=1024, window=204, keep=512, local_keep=32,
+        cluster=4, fanout=2, k_super=32, k_clusters=12, share_period=2, steps=64, static_ratio=0.5,
+        dynamic_ratio=0.10, seed=SEED_BASE + 5, seq_stride=1000, n_outlier=4, outlier_scale=8.0,
+        rope=True),
 }
 
 

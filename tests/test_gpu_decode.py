@@ -24,6 +24,7 @@ CASES = {
     "C3": dict(n_layers=6, layer0=0, heads=8),
     "C4": dict(n_layers=3, layer0=4, heads=4),
     "C5": dict(n_layers=6, layer0=0, heads=None),
+    "X1": dict(n_layers=4, layer0=0, heads=8),
 }
 
 

@@ -35,6 +35,8 @@ CASES = {
     # the other similarity measures in one launch (four heads per group for the bound)
     "C5-L32-maxprod": ("C5", dict(keep=8192, k_super=8), 0, "maxprod"),
     "C3-L8-mean": ("C3", dict(n_layers=8), 0, "mean"),
+    # clusters of 4 tokens, fan-out 2: 1280 owner heads (one wave each), 2048 attention units
+    "X1-L8": ("X1", dict(n_layers=8), 0),
 }
 
 

@@ -96,6 +96,7 @@ CASES = {
     "C4": dict(n_layers=1, batch=2, n_q_heads=2, n_kv_heads=2, T=4096, window=409, keep=1216),
     "C5": dict(n_layers=1, n_q_heads=8, n_kv_heads=2, T=4096, window=409, keep=1024, hh_count=8,
                hh_hi=4096 - 32),
+    "X1": dict(n_layers=2, batch=2, n_q_heads=4, n_kv_heads=4),
 }
 
 

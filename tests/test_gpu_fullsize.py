@@ -16,7 +16,7 @@ from gpu_util import assert_out_close, assert_sets_tie_equal, boundary_score, ra
 
 pytestmark = pytest.mark.gpu
 
-FULL = ["C3", "C4", "C5"]
+FULL = ["C3", "C4", "C5", "X1"]
 
 
 def _path(w, T, keep_scores=False):
@@ -84,15 +84,15 @@ def test_fullsize_static_eviction(name):
         b, hq, t = rng.integers(w.batch), rng.integers(w.n_q_heads), rng.integers(w.window)
         ref = oracle.row_lse(qw_h[b, hq, t], int(t), w.window, k_h[b, hq // G], w.dtype, sm)
         assert abs(lse[b, hq, t] - ref) <= 2e-6 * max(1.0, abs(ref)), (l, b, hq, t, lse[b, hq, t], ref)
-    if name == "C3":
-        # full oracle token scores for two heads of that layer
+    if name in ("C3", "X1"):
+        # full oracle token scores for two heads of that layer (sequence 0)
         for h in (0, w.n_kv_heads - 1):
             ref = oracle.token_scores(qw_h[0, h * G:(h + 1) * G], k_h[0, h], w.dtype, sm)
             got = path.token_score[l, 0, h].cpu().numpy()
             np.testing.assert_allclose(got, ref, rtol=2e-5)
             kept_r = oracle.static_topk(ref, w.keep, loc)
             bnd = boundary_score(ref[:w.T - loc], n_sel)
-            assert_sets_tie_equal(path.kept[l, 0, h].cpu().numpy(), kept_r, ref, bnd, f"C3 layer {l} head {h}")
+            assert_sets_tie_equal(path.kept[l, 0, h].cpu().numpy(), kept_r, ref, bnd, f"{name} layer {l} head {h}")
     say("  sampled rows ok")
 
 

@@ -14,6 +14,7 @@ pytestmark = pytest.mark.gpu
     ("C2", dict(n_layers=3), (1,)),
     ("C3", dict(n_layers=2, n_q_heads=4, n_kv_heads=4, T=2048, window=409), (0, 1)),
     ("C5", dict(n_layers=2, n_q_heads=8, n_kv_heads=2, T=8192, window=819, hh_count=16, hh_hi=8192 - 32), (1,)),
+    ("X1", dict(n_layers=2, batch=2, n_q_heads=4, n_kv_heads=4), (1,)),
 ])
 def test_device_generator_matches_host(name, over, layers):
     w = synth.get(name).with_(**over)

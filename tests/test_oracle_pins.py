@@ -34,7 +34,7 @@ def test_owner_layer_skips_first_two_layers():
     assert [oracle.owner_layer(l, 1, 2) for l in range(5)] == list(range(5))
 
 
-@pytest.mark.parametrize("name", ["C1", "C2", "C3", "C4", "C5"])
+@pytest.mark.parametrize("name", ["C1", "C2", "C3", "C4", "C5", "X1"])
 def test_workload_integers_follow_the_rules(name):
     w = synth.get(name)
     assert w.window == oracle.window_rows(w.T)
@@ -48,7 +48,7 @@ def test_workload_integers_follow_the_rules(name):
 def test_workload_derived_sizes():
     # cluster / super-cluster counts and owner-layer counts of the five workloads
     exp = {"C1": (16, 4, 1), "C2": (64, 16, 7), "C3": (128, 16, 10), "C4": (307, 39, 10),
-           "C5": (512, 64, 10)}
+           "C5": (512, 64, 10), "X1": (128, 64, 17)}
     for name, (C, S, n_own) in exp.items():
         w = synth.get(name)
         assert -(-w.keep // w.cluster) == C
