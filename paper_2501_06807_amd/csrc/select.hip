@@ -14,7 +14,8 @@
 namespace mpc {
 namespace {
 
-constexpr int kWaveHeads = 4;  // heads (waves) per workgroup of the standalone wave variant
+constexpr int kWaveHeads = 4;     // heads (waves) per workgroup of the wave variant, by default
+constexpr int kWaveHeadsMax = 8;  // and at most (when that spreads the heads evenly over the CUs)
 
 template <class DT, int D, int NW, bool MP, bool GMAX>
 __global__ __launch_bounds__(NW* kWave) void k_select(SelectArgs a) {
@@ -23,17 +24,25 @@ __global__ __launch_bounds__(NW* kWave) void k_select(SelectArgs a) {
 }
 
 template <class DT, int D, bool MP, bool GMAX>
-__global__ __launch_bounds__(kWaveHeads* kWave) void k_select_wave(SelectArgs a) {
+__global__ __launch_bounds__(kWaveHeadsMax* kWave) void k_select_wave(SelectArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
-  dev::select_waves<DT, D, false, MP, GMAX>(a, blockIdx.x * kWaveHeads, smem);
+  dev::select_waves<DT, D, false, MP, GMAX>(a, blockIdx.x * (blockDim.x / kWave), smem);
+}
+
+// Heads per workgroup: one workgroup per CU when the heads fit at most kWaveHeadsMax per CU (every
+// CU then runs the same number of heads; with a fixed 4 per workgroup, 1280 heads made 320
+// workgroups and a quarter of the CUs ran two), else 4.
+int wave_heads(int units) {
+  const int per_cu = (units + kNumCU - 1) / kNumCU;
+  return per_cu > kWaveHeads && per_cu <= kWaveHeadsMax ? per_cu : kWaveHeads;
 }
 
 template <class DT, int D, bool MP, bool GMAX>
-void launch_wave(const SelectArgs& a, hipStream_t st) {
+void launch_wave(const SelectArgs& a, int hpw, hipStream_t st) {
   const int units = a.own.n * a.B * a.Hsel;
-  const dim3 grid((units + kWaveHeads - 1) / kWaveHeads);
-  const size_t smem = kWaveHeads * dev::wave_region_bytes(D, a.S, a.NC, select_query_rows(a));
-  hipLaunchKernelGGL((k_select_wave<DT, D, MP, GMAX>), grid, dim3(kWaveHeads * kWave), smem, st, a);
+  const dim3 grid((units + hpw - 1) / hpw);
+  const size_t smem = hpw * dev::wave_region_bytes(D, a.S, a.NC, select_query_rows(a));
+  hipLaunchKernelGGL((k_select_wave<DT, D, MP, GMAX>), grid, dim3(hpw * kWave), smem, st, a);
 }
 
 template <class DT, int D, bool MP, bool GMAX>
@@ -51,9 +60,10 @@ void launch_block(const SelectArgs& a, int units, int nw, hipStream_t st) {
 template <class DT, int D, bool MP, bool GMAX>
 void launch_plan(const SelectArgs& a, hipStream_t st) {
   const int units = a.own.n * a.B * a.Hsel;
+  const int hpw = wave_heads(units);
   if (units >= 512 && a.S <= dev::kWaveMaxSuper && a.NC <= dev::kWaveMaxCand &&
-      kWaveHeads * dev::wave_region_bytes(D, a.S, a.NC, select_query_rows(a)) <= kMaxLds)
-    launch_wave<DT, D, MP, GMAX>(a, st);
+      hpw * dev::wave_region_bytes(D, a.S, a.NC, select_query_rows(a)) <= kMaxLds)
+    launch_wave<DT, D, MP, GMAX>(a, hpw, st);
   else
     launch_block<DT, D, MP, GMAX>(a, units, units <= kNumCU ? 8 : 4, st);
 }

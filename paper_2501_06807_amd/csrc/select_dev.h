@@ -271,14 +271,29 @@ __device__ __forceinline__ int count_above(const unsigned long long* key, int j0
 // ceil(n / 32) * (k + 1) entries; ends with a barrier.
 constexpr int kSlice = 32;
 
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+}
+
+// Synchronisation of the threads that rank one set: a whole workgroup, or one wave.
+struct BlockSync {
+  __device__ static void sync() { __syncthreads(); }
+};
+struct WaveSync {
+  __device__ static void sync() { wave_sync(); }
+};
+
 __host__ __device__ inline bool use_tournament(int n, int k) {
   return n > 2 * kSlice && ((n + kSlice - 1) / kSlice) * (k + 1) * 2 <= n;
 }
 
-template <int NT>
+// NT threads rank the set (a workgroup with SY = BlockSync, or one wave with NT = 64 and
+// SY = WaveSync); bnd[] must hold -1 on entry.
+template <int NT, class SY = BlockSync>
 __device__ void block_topk(const unsigned long long* ck, int n, int k, unsigned long long* list_k, int* list_i,
                            int* top, int* bnd) {
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x % NT;
   if (!use_tournament(n, k)) {
     for (int i = tid; i < n; i += NT) {
       const int r = count_above(ck, 0, n, ck[i]);
@@ -286,7 +301,7 @@ __device__ void block_topk(const unsigned long long* ck, int n, int k, unsigned 
       if (r == k - 1) bnd[0] = i;
       if (r == k) bnd[1] = i;
     }
-    __syncthreads();
+    SY::sync();
     return;
   }
   const int m = (n + kSlice - 1) / kSlice * (k + 1);
@@ -294,7 +309,7 @@ __device__ void block_topk(const unsigned long long* ck, int n, int k, unsigned 
     list_k[c] = 0ull;
     list_i[c] = -1;
   }
-  __syncthreads();
+  SY::sync();
   for (int i = tid; i < n; i += NT) {
     const int s0 = i / kSlice * kSlice;
     const int r = count_above(ck, s0, min(n, s0 + kSlice), ck[i]);
@@ -303,7 +318,7 @@ __device__ void block_topk(const unsigned long long* ck, int n, int k, unsigned 
       list_i[i / kSlice * (k + 1) + r] = i;
     }
   }
-  __syncthreads();
+  SY::sync();
   for (int c = tid; c < m; c += NT) {
     const int i = list_i[c];
     if (i < 0) continue;
@@ -312,19 +327,19 @@ __device__ void block_topk(const unsigned long long* ck, int n, int k, unsigned 
     if (r == k - 1) bnd[0] = i;
     if (r == k) bnd[1] = i;
   }
-  __syncthreads();
+  SY::sync();
 }
 
 // When the images of the entries at composite ranks k-1 and k tie, the composite order inside that
 // image group (index only) may differ from the exact (score desc, index asc) order: the group's
 // members re-rank themselves exactly and take the top slots from the group's first rank on.
 // Uniform across the workgroup (reads LDS only); ends with a barrier when it does anything.
-template <int NT>
+template <int NT, class SY = BlockSync>
 __device__ void repair_top(const double* sc, const uint32_t* img, int n, int k, const int* bnd, int* top) {
   const int a = bnd[0], b = bnd[1];
   if (a < 0 || b < 0 || img[a] != img[b]) return;
   const uint32_t t = img[a];
-  for (int i = threadIdx.x; i < n; i += NT) {
+  for (int i = threadIdx.x % NT; i < n; i += NT) {
     if (img[i] != t) continue;
     int first = 0, r = 0;
     for (int j = 0; j < n; ++j) {
@@ -333,7 +348,7 @@ __device__ void repair_top(const double* sc, const uint32_t* img, int n, int k, 
     }
     if (first + r < k) top[first + r] = i;
   }
-  __syncthreads();
+  SY::sync();
 }
 
 // Position of top[j] among top[0, k) in ascending entry order (entries are distinct).
@@ -473,48 +488,9 @@ __device__ void select_block(const SelectArgs& a, int ou, unsigned char* smem) {
 constexpr int kWaveMaxSuper = 256;        // limits of the wave variant's LDS region
 constexpr int kWaveMaxCand = 256;
 
-__device__ __forceinline__ void wave_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-}
-
-// Top k of n entries by composite key within one wave: lanes count the keys above each entry
-// (top[rank] = entry for rank < k), then the image-tied boundary group is re-ranked exactly as in
-// repair_top().
-__device__ void wave_topk(const double* sc, const uint32_t* img, const unsigned long long* ck, int n, int k,
-                          int* top) {
-  const int lane = threadIdx.x % kWave;
-  int bnd0 = -1, bnd1 = -1;
-  for (int i = lane; i < n; i += kWave) {
-    const int r = count_above(ck, 0, n, ck[i]);
-    if (r < k) top[r] = i;
-    if (r == k - 1) bnd0 = i;
-    if (r == k) bnd1 = i;
-  }
-  // each boundary entry is held by exactly one lane: a max-reduction publishes it to all lanes
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    bnd0 = max(bnd0, __shfl_xor(bnd0, o));
-    bnd1 = max(bnd1, __shfl_xor(bnd1, o));
-  }
-  wave_sync();
-  if (bnd0 < 0 || bnd1 < 0 || img[bnd0] != img[bnd1]) return;
-  const uint32_t t = img[bnd0];
-  for (int i = lane; i < n; i += kWave) {
-    if (img[i] != t) continue;
-    int first = 0, r = 0;
-    for (int j = 0; j < n; ++j) {
-      first += img[j] > t;
-      if (j != i && img[j] == t) r += (sc[j] > sc[i]) | ((sc[j] == sc[i]) & (j < i));
-    }
-    if (first + r < k) top[first + r] = i;
-  }
-  wave_sync();
-}
-
 // LDS region of one wave of the wave-per-head selection (host and device).
 struct WaveLds {
-  size_t qsum, s1, s2, ck, img, top, cand, total;
+  size_t qsum, s1, s2, ck, img, list_k, list_i, top, cand, bnd, total;
 };
 __host__ __device__ inline WaveLds wave_lds(int D, int S, int NC, int qrows) {
   auto al = [](size_t x) { return (x + 15) & ~(size_t)15; };
@@ -525,9 +501,12 @@ __host__ __device__ inline WaveLds wave_lds(int D, int S, int NC, int qrows) {
   o.s2 = al(o.s1 + (size_t)S * 8);
   o.ck = al(o.s2 + (size_t)NC * 8);
   o.img = al(o.ck + (size_t)m * 8);
-  o.top = al(o.img + (size_t)m * 4);
+  o.list_k = al(o.img + (size_t)m * 4);  // a tournament list is at most half its set
+  o.list_i = al(o.list_k + (size_t)m * 4);
+  o.top = al(o.list_i + (size_t)m * 2);
   o.cand = al(o.top + (size_t)m * 4);
-  o.total = al(o.cand + (size_t)NC * 4);
+  o.bnd = al(o.cand + (size_t)NC * 4);
+  o.total = al(o.bnd + 4 * sizeof(int));
   return o;
 }
 __host__ __device__ inline size_t wave_region_bytes(int D, int S, int NC, int qrows) {
@@ -551,8 +530,11 @@ __device__ void select_waves(const SelectArgs& a, int ou0, unsigned char* smem) 
   double* s2 = (double*)(base + lay.s2);
   unsigned long long* ck = (unsigned long long*)(base + lay.ck);
   uint32_t* img = (uint32_t*)(base + lay.img);
+  unsigned long long* list_k = (unsigned long long*)(base + lay.list_k);
+  int* list_i = (int*)(base + lay.list_i);
   int* top = (int*)(base + lay.top);
   int* cand = (int*)(base + lay.cand);
+  int* bnd = (int*)(base + lay.bnd);  // boundary entries of level 1 ([0], [1]) and level 2 ([2], [3])
 
   const int l = a.own.l[ou / BH], b = (ou / a.Hsel) % a.B, h = ou % a.Hsel;
   const size_t unit = ((size_t)l * a.B + b) * a.Hkv + h / a.rep_div;  // representatives' kv head
@@ -564,6 +546,7 @@ __device__ void select_waves(const SelectArgs& a, int ou0, unsigned char* smem) 
   tile_load<SC::RW, SC::P>(scent, nullptr, a.S, 0, tile);
   const size_t q0 = (((size_t)l * a.B + b) * a.Hq + (size_t)h * G) * D;
   load_query<DT, D, SC::kSep>(a.q, q0, G, qsum, lane, kWave);
+  if (lane < 4) bnd[lane] = -1;
   wave_sync();
   typename SC::Query qr;
   SC::prepare(qr, qsum, G);
@@ -575,7 +558,8 @@ __device__ void select_waves(const SelectArgs& a, int ou0, unsigned char* smem) 
     SC::dot(tile, a.S, r0, qr, s1, img, ck);
   }
   wave_sync();
-  wave_topk(s1, img, ck, a.S, a.k_super, top);
+  block_topk<kWave, WaveSync>(ck, a.S, a.k_super, list_k, list_i, top, bnd);
+  repair_top<kWave, WaveSync>(s1, img, a.S, a.k_super, bnd, top);
   for (int j = lane; j < a.k_super; j += kWave) {
     const int sup = top[j], p = ascending_pos(top, a.k_super, j);
     for (int m = 0; m < a.f; ++m) {
@@ -591,7 +575,8 @@ __device__ void select_waves(const SelectArgs& a, int ou0, unsigned char* smem) 
     SC::dot(tile, a.NC, r0, qr, s2, img, ck);
   }
   wave_sync();
-  wave_topk(s2, img, ck, a.NC, a.k_clusters, top);
+  block_topk<kWave, WaveSync>(ck, a.NC, a.k_clusters, list_k, list_i, top, bnd + 2);
+  repair_top<kWave, WaveSync>(s2, img, a.NC, a.k_clusters, bnd + 2, top);
   emit_selection<COH>(a, top, cand, s2, l, b, h, lane, kWave);
 }
 
