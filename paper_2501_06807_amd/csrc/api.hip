@@ -75,7 +75,7 @@ mpc_status launched(hipError_t e, const char* what) {
   return MPC_OK;
 }
 
-// Static eviction workspace: fp64 row bias per window row, then fp32 token scores.
+// Static eviction workspace: the (max, 1 / sum) pair of every window row, then fp32 token scores.
 struct EvictWs {
   size_t rowstat, score, total;
 };
@@ -199,7 +199,7 @@ mpc_status mpc_static_evict(const mpc_dims* dims, int32_t T, const mpc_evict_cfg
   a.kept = kept_idx;
   a.k_out = k_out;
   a.v_out = v_out;
-  a.rowstat = (double*)((char*)ws + lay.rowstat);
+  a.rowstat = (float2*)((char*)ws + lay.rowstat);
   a.score = token_score ? token_score : (float*)((char*)ws + lay.score);
   a.row_lse = row_lse;
   a.B = dims->batch;

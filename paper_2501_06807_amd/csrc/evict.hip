@@ -6,12 +6,14 @@
 // (v_mfma_f32_32x32x{16,16,2}_{bf16,f16,f32}):
 //   pass 1 (k_rowstats): window rows stay in registers as the B operand, key tiles stream
 //     through LDS as the A operand; each lane owns one query column of the 32x32 output, so the
-//     row max and row sum are in-lane reductions. Output per row: the fp64 bias
-//     -(c * max + log2(sum)), c = sm_scale * log2(e).
+//     row max and row sum are in-lane reductions. Output per row: the max score m and 1 / sum of
+//     exp2(c * (s - m)), c = sm_scale * log2(e).
 //   pass 2 (k_colsum): keys stay in registers as the B operand, window-row tiles (all query heads
 //     of the group) stream through LDS as the A operand; each lane owns one key column, so the
-//     column sum is in-lane. p = exp2(c * s + bias) is formed with c and the bias as unevaluated
-//     fp32 pairs (two FMAs), summed over 16 rows in fp32 and accumulated across tiles in fp64.
+//     column sum is in-lane. p = exp2(c * (s - m)) / sum, summed over 16 rows in fp32 and
+//     accumulated across tiles in fp64. The exponent is taken relative to the row max in fp32:
+//     its rounding errors (of s - m and of c) scale with |s - m|, so they are smallest on the
+//     terms that carry the sums.
 // The top-k is a 4-pass, 8-bit LDS radix select on the fp32 score bits followed by an ordered
 // block compaction; the gather copies kept rows with 16-byte lanes.
 #include "evict.h"
@@ -137,7 +139,10 @@ __global__ __launch_bounds__(kRowThreads) void k_rowstats(EvictArgs a) {
   stash(0);
   __syncthreads();
 
-  float m = -INFINITY, bh = 0.f, bl = 0.f;
+  // exponent c * (s - m) in fp32: the rounding of s - m and of c both scale with |s - m|, so they
+  // vanish for the terms that carry the row sum
+  const float cf = a.c_hi;
+  float m = -INFINITY;
   double ell = 0.0;
   for (int it = 0; it < ntile; ++it) {
     const int buf = it & 1;
@@ -167,20 +172,16 @@ __global__ __launch_bounds__(kRowThreads) void k_rowstats(EvictArgs a) {
     if (tmax > m) {
       if (ell > 0.0) ell *= exp2(((double)m - (double)tmax) * a.c64);
       m = tmax;
-      const double nb = -a.c64 * (double)m;
-      bh = (float)nb;
-      bl = (float)(nb - (double)bh);
     }
     float ps = 0.f;
     if (full) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) ps += fast_exp2(fmaf(a.c_hi, acc[r], bh) + fmaf(a.c_lo, acc[r], bl));
+      for (int r = 0; r < 16; ++r) ps += fast_exp2(cf * (acc[r] - m));
     } else {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int j = j0 + acc_row(r, lane);
-        if (j < a.T && (!a.causal || j <= pos))
-          ps += fast_exp2(fmaf(a.c_hi, acc[r], bh) + fmaf(a.c_lo, acc[r], bl));
+        if (j < a.T && (!a.causal || j <= pos)) ps += fast_exp2(cf * (acc[r] - m));
       }
     }
     ell += (double)ps;
@@ -194,9 +195,8 @@ __global__ __launch_bounds__(kRowThreads) void k_rowstats(EvictArgs a) {
   if (ell > 0.0) L += ell * exp2(((double)m - (double)mx) * a.c64);
   if (eo > 0.0) L += eo * exp2(((double)mo - (double)mx) * a.c64);
   if (hl == 0 && tvalid) {
-    const double nb = -(a.c64 * (double)mx) - log2(L);
-    a.rowstat[(size_t)qunit * a.W + t] = nb;
-    if (a.row_lse) a.row_lse[(size_t)qunit * a.W + t] = (float)(-nb * 0.69314718055994531);
+    a.rowstat[(size_t)qunit * a.W + t] = make_float2(mx, (float)(1.0 / L));
+    if (a.row_lse) a.row_lse[(size_t)qunit * a.W + t] = (float)((a.c64 * (double)mx + log2(L)) * 0.69314718055994531);
   }
 }
 
@@ -207,7 +207,7 @@ __global__ __launch_bounds__(256) void k_colsum(EvictArgs a) {
   constexpr int KS = D / M::K;
   constexpr int NB = kColWaveKeys / 32;
   __shared__ __align__(16) unsigned char s_q[2][TL::BYTES];
-  __shared__ float s_bh[2][32], s_bl[2][32];
+  __shared__ float s_mx[2][32], s_il[2][32];  // row max and 1 / row sum of the staged rows
 
   const int n_kb = (a.T + kColBlockKeys - 1) / kColBlockKeys;
   const int id = xcd_remap(blockIdx.x, gridDim.x);
@@ -220,6 +220,7 @@ __global__ __launch_bounds__(256) void k_colsum(EvictArgs a) {
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, c32 = lane & 31, hl = lane >> 5;
 
   const int jw = kb * kColBlockKeys + w * kColWaveKeys;
+  const float cf = a.c_hi;
   const char* kh = (const char*)a.k + (size_t)kvunit * a.T * TL::RB;
   typename M::Op kf[NB][KS];
 #pragma unroll
@@ -237,7 +238,7 @@ __global__ __launch_bounds__(256) void k_colsum(EvictArgs a) {
   const size_t qunit0 = ((size_t)l * a.B + b) * a.Hq + (size_t)h * G;
 
   uint4 pre[TL::PER];
-  double pre_b = 0.0;
+  float2 pre_b = make_float2(0.f, 0.f);
   auto fetch = [&](int tile) {
     const int g = tile / n_t, t0 = t_start + (tile % n_t) * 32;
     const char* qb = (const char*)a.q_win + ((qunit0 + g) * a.W) * TL::RB;
@@ -250,7 +251,7 @@ __global__ __launch_bounds__(256) void k_colsum(EvictArgs a) {
     }
     if (tid < 32) {
       const int t = t0 + tid;
-      pre_b = t < a.W ? a.rowstat[(qunit0 + g) * a.W + t] : 0.0;
+      pre_b = t < a.W ? a.rowstat[(qunit0 + g) * a.W + t] : make_float2(0.f, 0.f);
     }
   };
   auto stash = [&](int buf) {
@@ -260,9 +261,8 @@ __global__ __launch_bounds__(256) void k_colsum(EvictArgs a) {
       if (ch < TL::CHUNKS) *(uint4*)&s_q[buf][(ch / TL::CH) * TL::RS + (ch % TL::CH) * 16] = pre[i];
     }
     if (tid < 32) {
-      const float hi = (float)pre_b;
-      s_bh[buf][tid] = hi;
-      s_bl[buf][tid] = (float)(pre_b - (double)hi);
+      s_mx[buf][tid] = pre_b.x;
+      s_il[buf][tid] = pre_b.y;
     }
   };
   fetch(0);
@@ -276,14 +276,14 @@ __global__ __launch_bounds__(256) void k_colsum(EvictArgs a) {
     const int buf = it & 1;
     if (it + 1 < ntile) fetch(it + 1);
     const int t0 = t_start + (it % n_t) * 32;
-    float bhr[16], blr[16];
+    float mxr[16], ilr[16];
     int trow[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int rr = acc_row(r, lane);
       trow[r] = t0 + rr;
-      bhr[r] = s_bh[buf][rr];
-      blr[r] = s_bl[buf][rr];
+      mxr[r] = s_mx[buf][rr];
+      ilr[r] = s_il[buf][rr];
     }
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
@@ -300,12 +300,12 @@ __global__ __launch_bounds__(256) void k_colsum(EvictArgs a) {
       float ps = 0.f;
       if (full) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) ps += fast_exp2(fmaf(a.c_hi, acc[r], bhr[r]) + fmaf(a.c_lo, acc[r], blr[r]));
+        for (int r = 0; r < 16; ++r) ps = fmaf(fast_exp2(cf * (acc[r] - mxr[r])), ilr[r], ps);
       } else {
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           if (trow[r] < a.W && (!a.causal || j <= a.T - a.W + trow[r]))
-            ps += fast_exp2(fmaf(a.c_hi, acc[r], bhr[r]) + fmaf(a.c_lo, acc[r], blr[r]));
+            ps = fmaf(fast_exp2(cf * (acc[r] - mxr[r])), ilr[r], ps);
         }
       }
       cacc[nb] += (double)ps;
