@@ -142,6 +142,19 @@ mpc_status mpc_static_evict(const mpc_dims* dims, int32_t T, const mpc_evict_cfg
 mpc_status mpc_build_clusters(const mpc_dims* dims, int32_t Ts, const mpc_select_cfg* cfg,
                               const void* k_cache, float* cent, float* scent, void* stream);
 
+/* Prefill in one call: look-once static eviction (Sec. 3.2; Alg. 3 step 1) followed by the
+ * cluster representatives of the kept cache (Sec. 3.3), with the kept rows of the selection's
+ * owner layers gathered and summarised in the same pass over them. Results are those of
+ * mpc_static_evict(dims, T, ecfg, ...) followed by mpc_build_clusters(dims, ecfg->keep, scfg,
+ * k_out, cent, scent), bit for bit; the arguments keep their meaning, layout and ownership there.
+ * Owner layers of the eviction follow ecfg's sharing rule, those of the representatives scfg's
+ * (the two may differ). ws: mpc_workspace_bytes(MPC_OP_STATIC_EVICT, dims, T, ecfg) bytes.
+ * Errors: any error either call would report for these arguments, before anything runs. */
+mpc_status mpc_prefill(const mpc_dims* dims, int32_t T, const mpc_evict_cfg* ecfg, const mpc_select_cfg* scfg,
+                       const void* q_win, const void* k, const void* v, int32_t* kept_idx, void* k_out,
+                       void* v_out, float* cent, float* scent, float* token_score, float* row_lse, void* ws,
+                       size_t ws_bytes, void* stream);
+
 /* Query-aware dynamic selection of one decode step (Sec. 3.3; Alg. 3 step 2).
  * Similarity of one q-head g with a representative, summed over the channels i and accumulated in
  * fp64: q_{g,i} * c_i (LINEAR, MEAN) or max(q_{g,i} r^max_i, q_{g,i} r^min_i) (MAXPROD, Eq. 2). The

@@ -43,7 +43,7 @@ class MpcError(RuntimeError):
 
 
 _LIB = None
-EXPORTS = ("mpc_workspace_bytes", "mpc_static_evict", "mpc_build_clusters", "mpc_select_clusters",
+EXPORTS = ("mpc_workspace_bytes", "mpc_static_evict", "mpc_build_clusters", "mpc_prefill", "mpc_select_clusters",
            "mpc_sparse_decode_attn", "mpc_decode_step", "mpc_append_kv", "mpc_commonality", "mpc_owner_layer",
            "mpc_status_string", "mpc_last_error")
 
@@ -60,13 +60,14 @@ def lib():
         L.mpc_workspace_bytes.restype = ctypes.c_size_t
         L.mpc_static_evict.argtypes = [P(MpcDims), I, P(MpcEvictCfg)] + [V] * 8 + [V, ctypes.c_size_t, V]
         L.mpc_build_clusters.argtypes = [P(MpcDims), I, P(MpcSelectCfg), V, V, V, V]
+        L.mpc_prefill.argtypes = [P(MpcDims), I, P(MpcEvictCfg), P(MpcSelectCfg)] + [V] * 10 + [V, ctypes.c_size_t, V]
         L.mpc_select_clusters.argtypes = [P(MpcDims), I, P(MpcSelectCfg)] + [V] * 5 + [V, ctypes.c_size_t, V]
         L.mpc_sparse_decode_attn.argtypes = [P(MpcDims), I, I, I, V, V, V, V, I, I, F, V, V, V, ctypes.c_size_t, V]
         L.mpc_decode_step.argtypes = [P(MpcDims), I, I, P(MpcSelectCfg)] + [V] * 5 + [F] + [V] * 4 + [
             V, ctypes.c_size_t, V]
         L.mpc_append_kv.argtypes = [P(MpcDims), I, I, P(MpcSelectCfg)] + [V] * 7
         L.mpc_commonality.argtypes = [I, I, I, I, V, V, V]
-        for fn in ("mpc_static_evict", "mpc_build_clusters", "mpc_select_clusters", "mpc_sparse_decode_attn",
+        for fn in ("mpc_static_evict", "mpc_build_clusters", "mpc_prefill", "mpc_select_clusters", "mpc_sparse_decode_attn",
                    "mpc_decode_step", "mpc_append_kv", "mpc_commonality"):
             getattr(L, fn).restype = ctypes.c_int
         L.mpc_owner_layer.argtypes = [I, I, I]
@@ -174,16 +175,40 @@ def mpc_build_clusters(k_cache, cent, scent, cfg, *, Ts=None, layer0=0, stream=N
     max-product bound, else 1 and the R axis may be omitted)."""
     _contig(k_cache, cent, scent)
     dims = dims_of(k_cache, k_cache, layer0)
+    Ts = k_cache.shape[3] if Ts is None else Ts
+    _check_reps(k_cache, cent, scent, cfg)
+    _check("mpc_build_clusters", lib().mpc_build_clusters(
+        ctypes.byref(dims), Ts, ctypes.byref(cfg), _ptr(k_cache), _ptr(cent), _ptr(scent), _stream(stream)))
+
+
+def _check_reps(k_cache, cent, scent, cfg):
     L, B, Hkv, cap, d = k_cache.shape
-    Ts = cap if Ts is None else Ts
     C, S = _slots(cap, cfg)
     R = 2 if cfg.similarity == SIMILARITY["maxprod"] else 1
     if cent.numel() != L * B * Hkv * C * R * d or scent.numel() != L * B * Hkv * S * R * d:
         raise ValueError(f"cent / scent must hold [L][B][Hkv][C or S][{R}][d] floats")
     if cent.dtype != torch.float32 or scent.dtype != torch.float32:
         raise TypeError("cent / scent must be float32")
-    _check("mpc_build_clusters", lib().mpc_build_clusters(
-        ctypes.byref(dims), Ts, ctypes.byref(cfg), _ptr(k_cache), _ptr(cent), _ptr(scent), _stream(stream)))
+
+
+def mpc_prefill(q_win, k, v, kept_idx, k_out, v_out, cent, scent, cfg, *, keep, local_keep, sm_scale, causal=True,
+                layer0=0, share_period=1, share_start=2, token_score=None, row_lse=None, ws=None, stream=None):
+    """mpc_static_evict then mpc_build_clusters over the kept rows (Ts = keep) in one call, with the
+    selection owners' rows gathered inside the build; the eviction's sharing rule is
+    share_period / share_start, the representatives' that of cfg."""
+    _contig(q_win, k, v, kept_idx, k_out, v_out, cent, scent, token_score, row_lse, ws)
+    _check_reps(k_out, cent, scent, cfg)
+    dims = dims_of(q_win, k, layer0)
+    dims.kv_capacity = k_out.shape[3]
+    T, W = k.shape[3], q_win.shape[3]
+    ecfg = MpcEvictCfg(window=W, keep=keep, local_keep=local_keep, sm_scale=sm_scale, causal=int(causal),
+                       share_period=share_period, share_start=share_start)
+    if ws is None:
+        ws = workspace(workspace_bytes(MPC_OP_STATIC_EVICT, dims, T, ecfg), k.device)
+    _check("mpc_prefill", lib().mpc_prefill(
+        ctypes.byref(dims), T, ctypes.byref(ecfg), ctypes.byref(cfg), _ptr(q_win), _ptr(k), _ptr(v), _ptr(kept_idx),
+        _ptr(k_out), _ptr(v_out), _ptr(cent), _ptr(scent), _ptr(token_score), _ptr(row_lse), _ptr(ws), ws.numel(),
+        _stream(stream)))
 
 
 def mpc_select_clusters(q, cent, scent, sel, cfg, *, Ts, sel_score=None, layer0=0, stream=None):

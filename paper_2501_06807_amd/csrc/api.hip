@@ -160,10 +160,13 @@ size_t mpc_workspace_bytes(int32_t op, const mpc_dims* dims, int32_t T_or_Ts, co
   return 0;
 }
 
-mpc_status mpc_static_evict(const mpc_dims* dims, int32_t T, const mpc_evict_cfg* cfg,
-                            const void* q_win, const void* k, const void* v, int32_t* kept_idx,
-                            void* k_out, void* v_out, float* token_score, float* row_lse,
-                            void* ws, size_t ws_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+mpc_status prepare_evict(const mpc_dims* dims, int32_t T, const mpc_evict_cfg* cfg, const void* q_win,
+                         const void* k, const void* v, int32_t* kept_idx, void* k_out, void* v_out,
+                         float* token_score, float* row_lse, void* ws, size_t ws_bytes, mpc::EvictArgs* out) {
   mpc_status s = check_dims(dims);
   if (s != MPC_OK) return s;
   if (!cfg) return fail(MPC_EINVAL, "cfg is NULL");
@@ -219,20 +222,23 @@ mpc_status mpc_static_evict(const mpc_dims* dims, int32_t T, const mpc_evict_cfg
   a.c64 = (double)cfg->sm_scale * 1.4426950408889634;
   a.c_hi = (float)a.c64;
   a.c_lo = (float)(a.c64 - (double)a.c_hi);
-  hipStream_t st = (hipStream_t)stream;
-  const int D = dims->head_dim, dt = dims->dtype;
-  clear_stale_error();
+  *out = a;
+  return MPC_OK;
+}
+
+// Scoring passes and top-k for the owner layers, then the gather of every layer not in `skip`.
+mpc_status launch_evict(const mpc::EvictArgs& a, int dt, int D, hipStream_t st) {
+  mpc_status s;
   if (a.own.n > 0) {
     if ((s = launched(mpc::launch_rowstats(a, dt, D, st), "row statistics")) != MPC_OK) return s;
     if ((s = launched(mpc::launch_colsum(a, dt, D, st), "column sums")) != MPC_OK) return s;
     if ((s = launched(mpc::launch_topk(a, st), "top-k")) != MPC_OK) return s;
   }
-  if ((s = launched(mpc::launch_gather(a, dt, D, st), "gather")) != MPC_OK) return s;
-  return ok();
+  return launched(mpc::launch_gather(a, dt, D, st), "gather");
 }
 
-mpc_status mpc_build_clusters(const mpc_dims* dims, int32_t Ts, const mpc_select_cfg* cfg,
-                              const void* k_cache, float* cent, float* scent, void* stream) {
+mpc_status prepare_build(const mpc_dims* dims, int32_t Ts, const mpc_select_cfg* cfg, const void* k_cache,
+                         float* cent, float* scent, mpc::BuildArgs* out) {
   mpc_status s = check_dims(dims);
   if (s != MPC_OK) return s;
   if (!cfg) return fail(MPC_EINVAL, "cfg is NULL");
@@ -273,9 +279,64 @@ mpc_status mpc_build_clusters(const mpc_dims* dims, int32_t Ts, const mpc_select
   if ((int64_t)a.n_layers * a.B * a.Hkv * a.S >= ((int64_t)1 << 31))
     return fail(MPC_EUNSUPPORTED, "grid too large");
   a.own = mpc::owner_table(a.layer0, a.n_layers, a.period, a.start);
+  *out = a;
+  return MPC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+mpc_status mpc_static_evict(const mpc_dims* dims, int32_t T, const mpc_evict_cfg* cfg,
+                            const void* q_win, const void* k, const void* v, int32_t* kept_idx,
+                            void* k_out, void* v_out, float* token_score, float* row_lse,
+                            void* ws, size_t ws_bytes, void* stream) {
+  mpc::EvictArgs a;
+  mpc_status s = prepare_evict(dims, T, cfg, q_win, k, v, kept_idx, k_out, v_out, token_score, row_lse, ws,
+                               ws_bytes, &a);
+  if (s != MPC_OK) return s;
+  clear_stale_error();
+  if ((s = launch_evict(a, dims->dtype, dims->head_dim, (hipStream_t)stream)) != MPC_OK) return s;
+  return ok();
+}
+
+mpc_status mpc_build_clusters(const mpc_dims* dims, int32_t Ts, const mpc_select_cfg* cfg,
+                              const void* k_cache, float* cent, float* scent, void* stream) {
+  mpc::BuildArgs a;
+  mpc_status s = prepare_build(dims, Ts, cfg, k_cache, cent, scent, &a);
+  if (s != MPC_OK) return s;
   if (a.own.n == 0) return ok();
   clear_stale_error();
   if ((s = launched(mpc::launch_build(a, dims->dtype, dims->head_dim, (hipStream_t)stream), "build")) != MPC_OK)
+    return s;
+  return ok();
+}
+
+mpc_status mpc_prefill(const mpc_dims* dims, int32_t T, const mpc_evict_cfg* ecfg, const mpc_select_cfg* scfg,
+                       const void* q_win, const void* k, const void* v, int32_t* kept_idx, void* k_out,
+                       void* v_out, float* cent, float* scent, float* token_score, float* row_lse, void* ws,
+                       size_t ws_bytes, void* stream) {
+  mpc::EvictArgs a;
+  mpc_status s = prepare_evict(dims, T, ecfg, q_win, k, v, kept_idx, k_out, v_out, token_score, row_lse, ws,
+                               ws_bytes, &a);
+  if (s != MPC_OK) return s;
+  mpc::BuildArgs b;
+  if ((s = prepare_build(dims, ecfg->keep, scfg, k_out, cent, scent, &b)) != MPC_OK) return s;
+  // the selection's owner layers gather their rows inside the build; the gather takes the rest
+  for (int i = 0; i < b.own.n; ++i) a.skip[b.own.l[i] >> 6] |= 1ull << (b.own.l[i] & 63);
+  b.g.kept = kept_idx;
+  b.g.k_src = k;
+  b.g.v_src = v;
+  b.g.k_dst = k_out;
+  b.g.v_dst = v_out;
+  b.g.T = T;
+  b.g.keep = ecfg->keep;
+  b.g.period = ecfg->share_period;
+  b.g.start = ecfg->share_start;
+  hipStream_t st = (hipStream_t)stream;
+  clear_stale_error();
+  if ((s = launch_evict(a, dims->dtype, dims->head_dim, st)) != MPC_OK) return s;
+  if (b.own.n > 0 && (s = launched(mpc::launch_build(b, dims->dtype, dims->head_dim, st), "build")) != MPC_OK)
     return s;
   return ok();
 }

@@ -7,7 +7,9 @@
 // Each wave streams the rows of one fine cluster at a time with coalesced 16-byte loads (LPR
 // lanes per row), reduces max / min over its row groups with cross-lane shuffles, writes the fine
 // representative and folds the bounds into its super-cluster bounds; the waves' super bounds meet
-// in LDS. Max / min are exact,
+// in LDS. In prefill mode a wave first reads the kept positions of up to 64 rows of its cluster
+// (one coalesced load) and takes each row's position from its lane; every row it reads from the
+// prompt cache is also written, with its value row, to the kept cache. Max / min are exact,
 // the linear representative is two fp32 products and one fp32 sum with no contraction, and the
 // average's fp64 sums of 16-bit keys are exact, so their order does not matter.
 #include "clusters.h"
@@ -15,7 +17,7 @@
 namespace mpc {
 namespace {
 
-template <class DT, int D, int NW, int SIM>
+template <class DT, int D, int NW, int SIM, bool GATHER>
 __global__ __launch_bounds__(NW* kWave) void k_build(BuildArgs a) {
 #pragma clang fp contract(off)
   constexpr int EPL = DT::kVec;
@@ -32,7 +34,18 @@ __global__ __launch_bounds__(NW* kWave) void k_build(BuildArgs a) {
   const size_t unit = (size_t)l * a.B * a.Hkv + ou % (a.B * a.Hkv);
   const int tid = threadIdx.x, lane = tid % kWave, w = tid / kWave;
   const int rg = lane / LPR, li = lane % LPR;
-  const char* kh = (const char*)a.k + (size_t)unit * a.rows * D * DT::kElt;
+  constexpr int RB = D * DT::kElt;  // bytes per row
+  const char* kh = (const char*)a.k + (size_t)unit * a.rows * RB;
+  // prefill mode: the unit's kept set, prompt rows and kept-cache rows
+  size_t src_set = 0, dst_set = 0, src_rows = 0, dst_rows = 0;
+  if constexpr (GATHER) {
+    const int o = owner_layer(a.layer0 + l, a.g.period, a.g.start) - a.layer0;
+    const int src_l = o >= 0 ? o : l;  // an owner before the block: the set is already in place
+    src_set = (unit - (size_t)(l - src_l) * a.B * a.Hkv) * a.g.keep;
+    dst_set = unit * a.g.keep;
+    src_rows = unit * a.g.T;
+    dst_rows = unit * a.rows;
+  }
 
   float smax[EPL], smin[EPL];
   double ssum[EPL];
@@ -53,9 +66,9 @@ __global__ __launch_bounds__(NW* kWave) void k_build(BuildArgs a) {
       csum[e] = 0.0;
     }
     const int r_end = min(a.Ts, (c + 1) * a.s);
-    for (int r = c * a.s + rg; r < r_end; r += RPW) {
+    auto fold = [&](const uint4 raw) {
       float x[EPL];
-      unpack<DT>(ldg16(kh + ((size_t)r * D + li * EPL) * DT::kElt), x);
+      unpack<DT>(raw, x);
 #pragma unroll
       for (int e = 0; e < EPL; ++e) {
         if constexpr (MEAN) {
@@ -65,6 +78,31 @@ __global__ __launch_bounds__(NW* kWave) void k_build(BuildArgs a) {
           cmin[e] = fminf(cmin[e], x[e]);
         }
       }
+    };
+    if constexpr (GATHER) {
+      for (int r0 = c * a.s; r0 < r_end; r0 += kWave) {
+        const int n = min(kWave, r_end - r0);
+        int pos = 0;
+        if (lane < n) {
+          pos = a.g.kept[src_set + r0 + lane];
+          if (src_set != dst_set) a.g.kept[dst_set + r0 + lane] = pos;
+          pos = min(max(pos, 0), a.g.T - 1);  // positions supplied by the caller are clamped
+        }
+        for (int j0 = 0; j0 < n; j0 += RPW) {  // wave-uniform trip count: every lane shuffles
+          const int j = j0 + rg;
+          const int p = __shfl(pos, min(j, n - 1));
+          if (j < n) {
+            const size_t so = (src_rows + p) * RB + li * 16, dof = (dst_rows + r0 + j) * RB + li * 16;
+            const uint4 kr = ldg16((const char*)a.g.k_src + so);
+            const uint4 vr = ldg16((const char*)a.g.v_src + so);
+            *(uint4*)((char*)a.g.k_dst + dof) = kr;
+            *(uint4*)((char*)a.g.v_dst + dof) = vr;
+            fold(kr);
+          }
+        }
+      }
+    } else {
+      for (int r = c * a.s + rg; r < r_end; r += RPW) fold(ldg16(kh + (size_t)r * RB + li * 16));
     }
 #pragma unroll
     for (int o = LPR; o < kWave; o <<= 1) {
@@ -139,23 +177,31 @@ __global__ __launch_bounds__(NW* kWave) void k_build(BuildArgs a) {
   }
 }
 
-template <class DT, int D>
+template <class DT, int D, bool GATHER>
 void launch_sim(const BuildArgs& a, int blocks, hipStream_t st) {
   constexpr int NW = 4;
   if (a.similarity == MPC_SIM_MAXPROD)
-    hipLaunchKernelGGL((k_build<DT, D, NW, MPC_SIM_MAXPROD>), dim3(blocks), dim3(NW * kWave), 0, st, a);
+    hipLaunchKernelGGL((k_build<DT, D, NW, MPC_SIM_MAXPROD, GATHER>), dim3(blocks), dim3(NW * kWave), 0, st, a);
   else if (a.similarity == MPC_SIM_MEAN)
-    hipLaunchKernelGGL((k_build<DT, D, NW, MPC_SIM_MEAN>), dim3(blocks), dim3(NW * kWave), 0, st, a);
+    hipLaunchKernelGGL((k_build<DT, D, NW, MPC_SIM_MEAN, GATHER>), dim3(blocks), dim3(NW * kWave), 0, st, a);
   else
-    hipLaunchKernelGGL((k_build<DT, D, NW, MPC_SIM_LINEAR>), dim3(blocks), dim3(NW * kWave), 0, st, a);
+    hipLaunchKernelGGL((k_build<DT, D, NW, MPC_SIM_LINEAR, GATHER>), dim3(blocks), dim3(NW * kWave), 0, st, a);
+}
+
+template <class DT, int D>
+void launch_mode(const BuildArgs& a, int blocks, hipStream_t st) {
+  if (a.g.kept)
+    launch_sim<DT, D, true>(a, blocks, st);
+  else
+    launch_sim<DT, D, false>(a, blocks, st);
 }
 
 template <class DT>
 hipError_t launch_dt(const BuildArgs& a, int D, int blocks, hipStream_t st) {
   if (D == 64)
-    launch_sim<DT, 64>(a, blocks, st);
+    launch_mode<DT, 64>(a, blocks, st);
   else if (D == 128)
-    launch_sim<DT, 128>(a, blocks, st);
+    launch_mode<DT, 128>(a, blocks, st);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

@@ -15,7 +15,8 @@
 //     its rounding errors (of s - m and of c) scale with |s - m|, so they are smallest on the
 //     terms that carry the sums.
 // The top-k is a 4-pass, 8-bit LDS radix select on the fp32 score bits followed by an ordered
-// block compaction; the gather copies kept rows with 16-byte lanes.
+// block compaction; the gather copies kept rows with 16-byte lanes (all layers, or those whose
+// representatives are not built in the same pass).
 #include "evict.h"
 
 namespace mpc {
@@ -435,6 +436,7 @@ __global__ __launch_bounds__(256) void k_gather(EvictArgs a) {
   const int chunk = blockIdx.x % n_chunks;
   const size_t unit = blockIdx.x / n_chunks;
   const int l = (int)(unit / ((size_t)a.B * a.Hkv));
+  if ((a.skip[l >> 6] >> (l & 63)) & 1) return;
   const int o = owner_layer(a.layer0 + l, a.period, a.start) - a.layer0;
   const int src_l = o >= 0 ? o : l;
   const size_t src_unit = unit - (size_t)(l - src_l) * a.B * a.Hkv;

@@ -85,16 +85,19 @@ class MPCachePath:
         self._step_tail = (P(self.cent), P(self.scent), P(self.k_s), P(self.v_s), self.sm_scale, P(self.sel),
                            P(self.sel_score), P(self.out), P(self.lse), P(self.ws_step), self.ws_step.numel())
 
-    def prefill(self, q_win, k, v, stream=None):
+    def prefill(self, q_win, k, v, stream=None, fused=True):
         """Static eviction into rows [0, keep) of the kept cache and the cluster build; the cache
-        state returns to (keep, 0)."""
-        L.mpc_static_evict(q_win, k, v, self.kept, self.k_s, self.v_s, keep=self.keep,
-                           local_keep=self.local_keep, sm_scale=self.sm_scale, causal=self.causal,
-                           layer0=self.layer0, share_period=self.share_period,
-                           share_start=self.share_start, token_score=self.token_score,
-                           row_lse=self.row_lse, ws=self.ws_evict, stream=stream)
-        L.mpc_build_clusters(self.k_s, self.cent, self.scent, self.cfg, Ts=self.keep, layer0=self.layer0,
-                             stream=stream)
+        state returns to (keep, 0). fused: one call (mpc_prefill), else mpc_static_evict then
+        mpc_build_clusters (same results)."""
+        kw = dict(keep=self.keep, local_keep=self.local_keep, sm_scale=self.sm_scale, causal=self.causal,
+                  layer0=self.layer0, share_period=self.share_period, share_start=self.share_start,
+                  token_score=self.token_score, row_lse=self.row_lse, ws=self.ws_evict, stream=stream)
+        if fused:
+            L.mpc_prefill(q_win, k, v, self.kept, self.k_s, self.v_s, self.cent, self.scent, self.cfg, **kw)
+        else:
+            L.mpc_static_evict(q_win, k, v, self.kept, self.k_s, self.v_s, **kw)
+            L.mpc_build_clusters(self.k_s, self.cent, self.scent, self.cfg, Ts=self.keep, layer0=self.layer0,
+                                 stream=stream)
         if (self.Ts, self.n_tail) != (self.keep, 0):
             self.Ts, self.n_tail = self.keep, 0
             self._prepare()

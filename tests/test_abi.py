@@ -20,7 +20,7 @@ def declared_functions():
 def test_library_exports_every_declared_function():
     lib = L.lib()
     names = declared_functions()
-    assert {"mpc_static_evict", "mpc_build_clusters", "mpc_select_clusters",
+    assert {"mpc_static_evict", "mpc_build_clusters", "mpc_prefill", "mpc_select_clusters",
             "mpc_sparse_decode_attn", "mpc_decode_step"} <= set(names)
     for n in names:
         assert hasattr(lib, n), n
@@ -186,6 +186,33 @@ def test_static_evict_validation_and_workspace():
     s, _ = _status("mpc_static_evict", ctypes.byref(d), 1000, ctypes.byref(cfg), misaligned, FAKE, FAKE, FAKE,
                    FAKE, FAKE, None, None, FAKE, need, None)
     assert s == L.MPC_EINVAL
+
+
+def test_prefill_validation():
+    d = _dims(n_layers=4, batch=1, n_q_heads=8, n_kv_heads=2)
+    ecfg = L.MpcEvictCfg(window=100, keep=200, local_keep=32, sm_scale=0.088, causal=1, share_period=2,
+                         share_start=2)
+    need = L.workspace_bytes(L.MPC_OP_STATIC_EVICT, d, 1000, ecfg)
+
+    def call(e, c, ws=FAKE, nb=need, cent=FAKE):
+        return _status("mpc_prefill", ctypes.byref(d), 1000, e, c, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, cent, FAKE,
+                       None, None, ws, nb, None)[0]
+
+    good = L.select_cfg(16, 4, 2, 4, share_period=2)
+    assert call(None, ctypes.byref(good)) == L.MPC_EINVAL
+    assert call(ctypes.byref(ecfg), None) == L.MPC_EINVAL
+    assert call(ctypes.byref(ecfg), ctypes.byref(good), ws=None, nb=0) == L.MPC_EWORKSPACE
+    assert call(ctypes.byref(ecfg), ctypes.byref(good), nb=need - 1) == L.MPC_EWORKSPACE
+    assert call(ctypes.byref(ecfg), ctypes.byref(good), cent=None) == L.MPC_EINVAL
+    assert call(ctypes.byref(ecfg), ctypes.byref(good), cent=ctypes.c_void_p((1 << 20) + 4)) == L.MPC_EINVAL
+    bad_sim = L.select_cfg(16, 4, 2, 4, share_period=2)
+    bad_sim.similarity = 9
+    assert call(ctypes.byref(ecfg), ctypes.byref(bad_sim)) == L.MPC_EINVAL
+    bad_alpha = L.select_cfg(16, 4, 2, 4, alpha=1.5, share_period=2)
+    assert call(ctypes.byref(ecfg), ctypes.byref(bad_alpha)) == L.MPC_EINVAL
+    bad_keep = L.MpcEvictCfg(window=100, keep=2000, local_keep=32, sm_scale=0.088, causal=1, share_period=2,
+                             share_start=2)
+    assert call(ctypes.byref(bad_keep), ctypes.byref(good)) == L.MPC_ESHAPE
 
 
 def test_status_strings():
