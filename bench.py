@@ -92,6 +92,45 @@ def decode_bytes(w, owners, sel, C, S, rep_rows=1):
     return sel_read + sel_write, attn_read + attn_write
 
 
+def measure_read_ceiling(dev, chunk_bytes=16384, per_wg=24, total=2 << 30):
+    """Read rate of a kernel that reads every 16 KB chunk of a 2 GiB buffer once, in random order
+    (the sparse attention's access pattern: whole clusters of rows): the practical ceiling the
+    decode kernels are compared with, beside the published peak."""
+    import ctypes
+
+    import torch
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2501_06807_amd", "libmpc_ceiling.so"))
+    lib.mpc_read_ceiling.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_void_p, ctypes.c_int,
+                                     ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+    n_chunks = total // chunk_bytes
+    grid = n_chunks // per_wg
+    buf = torch.empty(total, dtype=torch.uint8, device=dev).fill_(3)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(7)
+    order = torch.randperm(n_chunks, generator=gen, device=dev, dtype=torch.int32)[:grid * per_wg].contiguous()
+    sink = torch.empty(grid * 256, dtype=torch.int32, device=dev)
+    st = torch.cuda.current_stream(dev)
+
+    def launch():
+        rc = lib.mpc_read_ceiling(buf.data_ptr(), n_chunks, chunk_bytes, order.data_ptr(), grid, per_wg,
+                                  sink.data_ptr(), st.cuda_stream)
+        if rc != 0:
+            raise RuntimeError(f"read-ceiling kernel failed to launch ({rc})")
+
+    launch()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(st)
+    for _ in range(5):
+        launch()
+    b.record(st)
+    torch.cuda.synchronize()
+    gbs = 5 * grid * per_wg * chunk_bytes / (a.elapsed_time(b) * 1e-3) / 1e9
+    del buf, order, sink
+    return {"GBps": round(gbs, 1), "frac_of_peak": round(gbs / HBM_PEAK_GBS, 4),
+            "note": "every 16 KB chunk of 2 GiB read once in random order, 16-byte loads (the sparse "
+                    "attention's pattern)"}
+
+
 def prefill_flops(w, n_owner):
     """One causal pass of window scores q_t . k_j (2d flops each) over the owner layers."""
     rows = sum(w.T - w.window + t + 1 for t in range(w.window))
@@ -203,6 +242,7 @@ def main():
     torch.cuda.synchronize()
     copy_gbs = 2 * (1 << 30) * 5 / (c0.elapsed_time(c1) * 1e-3) / 1e9
     del src, dst
+    read_ceiling = measure_read_ceiling(dev)
 
     # inputs, generated on the device
     sp = synth.spec(w)
@@ -392,6 +432,7 @@ def main():
         "roofline": roofline,
         "copy_ceiling": {"GBps": round(copy_gbs, 1), "frac_of_peak": round(copy_gbs / HBM_PEAK_GBS, 4),
                          "note": "1 GiB device-to-device copy, read + write bytes"},
+        "read_ceiling": dict(read_ceiling, attention_frac_of_ceiling=round(att_gbs / read_ceiling["GBps"], 4)),
         "prefill": {"ms_per_pass": round(mean(pre_ms), 3), "owner_layers": len(owners),
                     "ms_per_owner_layer": round(mean(pre_ms) / len(owners), 3),
                     "algorithmic_TFLOP_per_pass": round(fl / 1e12, 3),

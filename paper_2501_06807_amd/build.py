@@ -1,4 +1,5 @@
-"""Builds paper_2501_06807_amd/libmpcache.so from csrc/*.hip for gfx950 with hipcc."""
+"""Builds paper_2501_06807_amd/libmpcache.so from csrc/*.hip for gfx950 with hipcc, and the
+read-ceiling measurement kernel (libmpc_ceiling.so, used by the bench only)."""
 import concurrent.futures as cf
 import glob
 import os
@@ -7,6 +8,7 @@ import subprocess
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libmpcache.so")
+CEILING_LIB = os.path.join(HERE, "libmpc_ceiling.so")
 BUILD_DIR = os.path.join(ROOT, "_build", "mpcache")
 
 CFLAGS = [
@@ -37,6 +39,9 @@ def build(verbose=False):
             f.result()
     _run(["hipcc", "-shared", "--offload-arch=gfx950", *objs, "-o", LIB + ".tmp"], verbose)
     os.replace(LIB + ".tmp", LIB)
+    _run(["hipcc", *CFLAGS, "-shared", os.path.join(HERE, "ceiling", "read_ceiling.hip"), "-o", CEILING_LIB + ".tmp"],
+         verbose)
+    os.replace(CEILING_LIB + ".tmp", CEILING_LIB)
     return LIB
 
 

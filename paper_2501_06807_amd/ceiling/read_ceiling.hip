@@ -1,0 +1,50 @@
+// Measured read ceiling for the roofline context of the decode kernels (not part of the method):
+// every workgroup reads `per_wg` contiguous chunks of `chunk_bytes`, taken in a caller-given
+// (random) order, with 16-byte coalesced loads, four in flight per thread — the access pattern of
+// the sparse attention, which reads whole clusters of K / V rows. One XOR per thread is written to
+// `sink` so that the loads are kept.
+#include <hip/hip_runtime.h>
+#include <cstdint>
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kInFlight = 4;
+
+__global__ __launch_bounds__(kThreads) void k_read_chunks(const uint4* __restrict__ buf,
+                                                          const int32_t* __restrict__ order, int per_wg,
+                                                          int chunk16, uint32_t* __restrict__ sink) {
+  uint32_t acc = 0;
+  const int n = per_wg * chunk16;  // 16-byte vectors of this workgroup
+  const int32_t* mine = order + (size_t)blockIdx.x * per_wg;
+  int j = threadIdx.x;
+  for (; j + (kInFlight - 1) * kThreads < n; j += kInFlight * kThreads) {
+    uint4 v[kInFlight];
+#pragma unroll
+    for (int u = 0; u < kInFlight; ++u) {
+      const int jj = j + u * kThreads;
+      v[u] = buf[(size_t)mine[jj / chunk16] * chunk16 + jj % chunk16];
+    }
+#pragma unroll
+    for (int u = 0; u < kInFlight; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
+  }
+  for (; j < n; j += kThreads) {
+    const uint4 v = buf[(size_t)mine[j / chunk16] * chunk16 + j % chunk16];
+    acc ^= v.x ^ v.y ^ v.z ^ v.w;
+  }
+  sink[(size_t)blockIdx.x * kThreads + threadIdx.x] = acc;
+}
+
+}  // namespace
+
+// buf: n_chunks * chunk_bytes bytes; order: grid * per_wg chunk ids in [0, n_chunks); sink: grid *
+// 256 words. Returns a hipError_t code (0 = launched).
+extern "C" int mpc_read_ceiling(const void* buf, int64_t n_chunks, int chunk_bytes, const int32_t* order, int grid,
+                                int per_wg, uint32_t* sink, void* stream) {
+  if (!buf || !order || !sink || chunk_bytes <= 0 || chunk_bytes % 16 || grid <= 0 || per_wg <= 0 ||
+      (int64_t)grid * per_wg > n_chunks || (int64_t)per_wg * (chunk_bytes / 16) >= ((int64_t)1 << 31))
+    return (int)hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_read_chunks, dim3(grid), dim3(kThreads), 0, (hipStream_t)stream, (const uint4*)buf, order,
+                     per_wg, chunk_bytes / 16, sink);
+  return (int)hipGetLastError();
+}
