@@ -75,7 +75,8 @@ mpc_status launched(hipError_t e, const char* what) {
   return MPC_OK;
 }
 
-// Static eviction workspace: the (max, 1 / sum) pair of every window row, then fp32 token scores.
+// Static eviction workspace: the (exponent offset, 1 / sum) pair of every window row, then fp32
+// token scores.
 struct EvictWs {
   size_t rowstat, score, total;
 };

@@ -6,8 +6,9 @@ namespace mpc {
 
 constexpr int kNumXcd = 8;       // accelerator dies; workgroup i runs on die i % 8
 constexpr int kRowBlock = 256;  // window rows per row-statistics workgroup (8 waves x 32)
-constexpr int kColWaveKeys = 64;  // keys per wave in the column-sum pass (2 MFMA column blocks)
-constexpr int kColBlockKeys = 4 * kColWaveKeys;
+constexpr int kColWaveKeys = 32;  // keys per wave in the column-sum pass (one MFMA column block)
+constexpr int kColWaves = 8;      // waves per column-sum workgroup (they share each staged row tile)
+constexpr int kColBlockKeys = kColWaves * kColWaveKeys;
 
 struct EvictArgs {
   const void* q_win;   // [L][B][Hq][W][d]
@@ -17,7 +18,7 @@ struct EvictArgs {
   void* k_out;         // [L][B][Hkv][out_rows][d], rows [0, keep) written
   void* v_out;
   float* score;        // [L][B][Hkv][T] accumulated attention (token_score or workspace)
-  float2* rowstat;     // [L][B][Hq][W]: (max score, 1 / sum of exp2(c * (score - max))) per window row
+  float2* rowstat;     // [L][B][Hq][W]: (b = fp32(-c * max score), 1 / sum of exp2(fma(c, score, b)))
   float* row_lse;      // [L][B][Hq][W] natural log-sum-exp, optional
   int B, layer0, n_layers, Hq, Hkv, T, W, keep, local_keep, causal, period, start;
   int out_rows;        // row capacity of k_out / v_out per (layer, sequence, kv head)

@@ -6,13 +6,16 @@
 // (v_mfma_f32_32x32x{16,16,2}_{bf16,f16,f32}):
 //   pass 1 (k_rowstats): window rows stay in registers as the B operand, key tiles stream
 //     through LDS as the A operand; each lane owns one query column of the 32x32 output, so the
-//     row max and row sum are in-lane reductions. Output per row: the max score m and 1 / sum of
-//     exp2(c * (s - m)), c = sm_scale * log2(e).
+//     row max and row sum are in-lane reductions. Output per row: the offset b = fp32(-c * m) of
+//     the row max m and 1 / sum of exp2(fma(c, s, b)), c = fp32(sm_scale * log2(e)).
 //   pass 2 (k_colsum): keys stay in registers as the B operand, window-row tiles (all query heads
 //     of the group) stream through LDS as the A operand; each lane owns one key column, so the
-//     column sum is in-lane. p = exp2(c * (s - m)) / sum, summed over 16 rows in fp32 and
-//     accumulated across tiles in fp64. The exponent is taken relative to the row max in fp32:
-//     its rounding errors (of s - m and of c) scale with |s - m|, so they are smallest on the
+//     column sum is in-lane. p = exp2(fma(c, s, b)) / sum, summed over 16 rows in fp32 and
+//     accumulated across tiles in fp64. Both passes form the exponent with one fused multiply-add
+//     against the same fp32 offset, so the offset's rounding is a common factor of a row's terms
+//     and of its sum and cancels in p; when the running max moves, pass 1 rebases its fp64 sum by
+//     exp2(b_new - b_old), exact from the two fp32 offsets. The remaining error of each exponent
+//     is its own rounding and that of c, both proportional to |c * (s - m)|: smallest on the
 //     terms that carry the sums.
 // The top-k is a 4-pass, 8-bit LDS radix select on the fp32 score bits followed by an ordered
 // block compaction; the gather copies kept rows with 16-byte lanes (all layers, or those whose
@@ -140,11 +143,9 @@ __global__ __launch_bounds__(kRowThreads) void k_rowstats(EvictArgs a) {
   stash(0);
   __syncthreads();
 
-  // exponent c * (s - m) in fp32: the rounding of s - m and of c both scale with |s - m|, so they
-  // vanish for the terms that carry the row sum
   const float cf = a.c_hi;
-  float m = -INFINITY;
-  double ell = 0.0;
+  float m = -INFINITY, nb = INFINITY;  // running max and its offset fp32(-c * m)
+  double ell = 0.0;                    // sum of exp2(fma(c, s, nb)) so far
   for (int it = 0; it < ntile; ++it) {
     const int buf = it & 1;
     if (it + 1 < ntile) fetch(it + 1);
@@ -171,44 +172,50 @@ __global__ __launch_bounds__(kRowThreads) void k_rowstats(EvictArgs a) {
       }
     }
     if (tmax > m) {
-      if (ell > 0.0) ell *= exp2(((double)m - (double)tmax) * a.c64);
+      const float nb_new = -(cf * tmax);
+      if (ell > 0.0) ell *= exp2((double)nb_new - (double)nb);
       m = tmax;
+      nb = nb_new;
     }
     float ps = 0.f;
     if (full) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) ps += fast_exp2(cf * (acc[r] - m));
+      for (int r = 0; r < 16; ++r) ps += fast_exp2(fmaf(cf, acc[r], nb));
     } else {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int j = j0 + acc_row(r, lane);
-        if (j < a.T && (!a.causal || j <= pos)) ps += fast_exp2(cf * (acc[r] - m));
+        if (j < a.T && (!a.causal || j <= pos)) ps += fast_exp2(fmaf(cf, acc[r], nb));
       }
     }
     ell += (double)ps;
     if (it + 1 < ntile) stash(buf ^ 1);
     __syncthreads();
   }
-  const float mo = __shfl_xor(m, 32);
+  // the two half-waves' sums meet at the offset of the larger max (the smaller offset)
   const double eo = __shfl_xor(ell, 32);
-  const float mx = fmaxf(m, mo);
+  const float nbo = __shfl_xor(nb, 32);
+  const float nbx = fminf(nb, nbo);
   double L = 0.0;
-  if (ell > 0.0) L += ell * exp2(((double)m - (double)mx) * a.c64);
-  if (eo > 0.0) L += eo * exp2(((double)mo - (double)mx) * a.c64);
+  if (ell > 0.0) L += ell * exp2((double)nbx - (double)nb);
+  if (eo > 0.0) L += eo * exp2((double)nbx - (double)nbo);
   if (hl == 0 && tvalid) {
-    a.rowstat[(size_t)qunit * a.W + t] = make_float2(mx, (float)(1.0 / L));
-    if (a.row_lse) a.row_lse[(size_t)qunit * a.W + t] = (float)((a.c64 * (double)mx + log2(L)) * 0.69314718055994531);
+    a.rowstat[(size_t)qunit * a.W + t] = make_float2(nbx, (float)(1.0 / L));
+    // log-sum-exp of the scaled scores: log2 of sum exp2(c * s) = log2(L) - offset
+    if (a.row_lse) a.row_lse[(size_t)qunit * a.W + t] = (float)((log2(L) - (double)nbx) * 0.69314718055994531);
   }
 }
 
+constexpr int kColThreads = kColWaves * kWave;
+
 template <class DT, int D>
-__global__ __launch_bounds__(256) void k_colsum(EvictArgs a) {
+__global__ __launch_bounds__(kColThreads) void k_colsum(EvictArgs a) {
   using M = Mma<DT>;
-  using TL = Tile<DT, D>;
+  using TL = Tile<DT, D, kColThreads>;
   constexpr int KS = D / M::K;
   constexpr int NB = kColWaveKeys / 32;
   __shared__ __align__(16) unsigned char s_q[2][TL::BYTES];
-  __shared__ float s_mx[2][32], s_il[2][32];  // row max and 1 / row sum of the staged rows
+  __shared__ float s_nb[2][32], s_il[2][32];  // offset and 1 / sum of the staged rows
 
   const int n_kb = (a.T + kColBlockKeys - 1) / kColBlockKeys;
   const int id = xcd_remap(blockIdx.x, gridDim.x);
@@ -245,7 +252,7 @@ __global__ __launch_bounds__(256) void k_colsum(EvictArgs a) {
     const char* qb = (const char*)a.q_win + ((qunit0 + g) * a.W) * TL::RB;
 #pragma unroll
     for (int i = 0; i < TL::PER; ++i) {
-      const int ch = tid + i * 256;
+      const int ch = tid + i * kColThreads;
       const int row = ch / TL::CH, c16 = ch % TL::CH;
       const int t = t0 + row;
       pre[i] = (ch < TL::CHUNKS && t < a.W) ? ldg16(qb + (size_t)t * TL::RB + c16 * 16) : make_uint4(0, 0, 0, 0);
@@ -258,11 +265,11 @@ __global__ __launch_bounds__(256) void k_colsum(EvictArgs a) {
   auto stash = [&](int buf) {
 #pragma unroll
     for (int i = 0; i < TL::PER; ++i) {
-      const int ch = tid + i * 256;
+      const int ch = tid + i * kColThreads;
       if (ch < TL::CHUNKS) *(uint4*)&s_q[buf][(ch / TL::CH) * TL::RS + (ch % TL::CH) * 16] = pre[i];
     }
     if (tid < 32) {
-      s_mx[buf][tid] = pre_b.x;
+      s_nb[buf][tid] = pre_b.x;
       s_il[buf][tid] = pre_b.y;
     }
   };
@@ -277,13 +284,13 @@ __global__ __launch_bounds__(256) void k_colsum(EvictArgs a) {
     const int buf = it & 1;
     if (it + 1 < ntile) fetch(it + 1);
     const int t0 = t_start + (it % n_t) * 32;
-    float mxr[16], ilr[16];
+    float nbr[16], ilr[16];
     int trow[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int rr = acc_row(r, lane);
       trow[r] = t0 + rr;
-      mxr[r] = s_mx[buf][rr];
+      nbr[r] = s_nb[buf][rr];
       ilr[r] = s_il[buf][rr];
     }
 #pragma unroll
@@ -301,12 +308,12 @@ __global__ __launch_bounds__(256) void k_colsum(EvictArgs a) {
       float ps = 0.f;
       if (full) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) ps = fmaf(fast_exp2(cf * (acc[r] - mxr[r])), ilr[r], ps);
+        for (int r = 0; r < 16; ++r) ps = fmaf(fast_exp2(fmaf(cf, acc[r], nbr[r])), ilr[r], ps);
       } else {
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           if (trow[r] < a.W && (!a.causal || j <= a.T - a.W + trow[r]))
-            ps = fmaf(fast_exp2(cf * (acc[r] - mxr[r])), ilr[r], ps);
+            ps = fmaf(fast_exp2(fmaf(cf, acc[r], nbr[r])), ilr[r], ps);
         }
       }
       cacc[nb] += (double)ps;
@@ -460,7 +467,7 @@ hipError_t launch_pass(const EvictArgs& a, bool rows, hipStream_t st) {
     hipLaunchKernelGGL((k_rowstats<DT, D>), dim3(a.own.n * a.B * a.Hq * n_rb), dim3(kRowThreads), 0, st, a);
   } else {
     const int n_kb = (a.T + kColBlockKeys - 1) / kColBlockKeys;
-    hipLaunchKernelGGL((k_colsum<DT, D>), dim3(a.own.n * a.B * a.Hkv * n_kb), dim3(256), 0, st, a);
+    hipLaunchKernelGGL((k_colsum<DT, D>), dim3(a.own.n * a.B * a.Hkv * n_kb), dim3(kColThreads), 0, st, a);
   }
   return hipGetLastError();
 }
