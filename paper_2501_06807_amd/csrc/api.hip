@@ -220,9 +220,7 @@ mpc_status prepare_evict(const mpc_dims* dims, int32_t T, const mpc_evict_cfg* c
   a.period = cfg->share_period;
   a.start = cfg->share_start;
   a.own = mpc::owner_table(dims->layer0, dims->n_layers, cfg->share_period, cfg->share_start);
-  a.c64 = (double)cfg->sm_scale * 1.4426950408889634;
-  a.c_hi = (float)a.c64;
-  a.c_lo = (float)(a.c64 - (double)a.c_hi);
+  a.c32 = (float)((double)cfg->sm_scale * 1.4426950408889634);
   *out = a;
   return MPC_OK;
 }

@@ -24,8 +24,7 @@ struct EvictArgs {
   int out_rows;        // row capacity of k_out / v_out per (layer, sequence, kv head)
   OwnerTable own;      // owner layers of the block
   uint64_t skip[kMaxLayers / 64];  // layers whose rows the gather leaves to the cluster build (bit l)
-  float c_hi, c_lo;    // sm_scale * log2(e) as an unevaluated fp32 sum
-  double c64;          // the same in fp64
+  float c32;           // fp32(sm_scale * log2(e)), the exponent scale of both scoring passes
 };
 
 hipError_t launch_rowstats(const EvictArgs& a, int dtype, int D, hipStream_t st);

@@ -143,7 +143,7 @@ __global__ __launch_bounds__(kRowThreads) void k_rowstats(EvictArgs a) {
   stash(0);
   __syncthreads();
 
-  const float cf = a.c_hi;
+  const float cf = a.c32;
   float m = -INFINITY, nb = INFINITY;  // running max and its offset fp32(-c * m)
   double ell = 0.0;                    // sum of exp2(fma(c, s, nb)) so far
   for (int it = 0; it < ntile; ++it) {
@@ -228,7 +228,7 @@ __global__ __launch_bounds__(kColThreads) void k_colsum(EvictArgs a) {
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, c32 = lane & 31, hl = lane >> 5;
 
   const int jw = kb * kColBlockKeys + w * kColWaveKeys;
-  const float cf = a.c_hi;
+  const float cf = a.c32;
   const char* kh = (const char*)a.k + (size_t)kvunit * a.T * TL::RB;
   typename M::Op kf[NB][KS];
 #pragma unroll
