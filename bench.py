@@ -160,26 +160,48 @@ def cpu_baseline(w, n_steps_sample, similarity="linear", group="sum", min_second
     sp = synth.spec(w, n_layers=layer0 + n_l)
     qs = [synth.dq_host(sp, e, w.dtype)[layer0:] for e in range(n_steps_sample)]
     sm = 1.0 / math.sqrt(w.head_dim)
-    steps = 0
-    t0 = time.perf_counter()
-    while True:
-        for q in qs:
-            sel, _ = oracle.select_clusters(q, cent, scent, w.dtype, Ts=w.keep, cluster=w.cluster, fanout=w.fanout,
-                                            k_super=w.k_super, k_clusters=w.k_clusters, layer0=layer0,
-                                            share_period=w.share_period, share_start=w.share_start,
-                                            similarity=similarity, group=group)
-            oracle.sparse_decode_attn(q, k, v, sel, w.dtype, cluster=w.cluster, sm_scale=sm)
-            steps += 1
-            if time.perf_counter() - t0 > max_seconds:
-                break
-        dt = time.perf_counter() - t0
-        if dt >= min_seconds:
-            break
-    return {"value": dt / (steps * n_l) * 1e6, "unit": "us/layer", "cores": oracle.threads(),
-            "kind": "oracle",
+
+    def timed(min_s, max_s):
+        steps = 0
+        t0 = time.perf_counter()
+        while True:
+            for q in qs:
+                sel, _ = oracle.select_clusters(q, cent, scent, w.dtype, Ts=w.keep, cluster=w.cluster,
+                                                fanout=w.fanout, k_super=w.k_super, k_clusters=w.k_clusters,
+                                                layer0=layer0, share_period=w.share_period,
+                                                share_start=w.share_start, similarity=similarity, group=group)
+                oracle.sparse_decode_attn(q, k, v, sel, w.dtype, cluster=w.cluster, sm_scale=sm)
+                steps += 1
+                if time.perf_counter() - t0 > max_s:
+                    break
+            dt = time.perf_counter() - t0
+            if dt >= min_s:
+                return dt, steps
+
+    cores = oracle.threads()
+    dt, steps = timed(min_seconds, max_seconds)
+    oracle.set_threads(1)
+    try:
+        dt1, steps1 = timed(min_seconds / 3, max_seconds / 3)
+    finally:
+        oracle.set_threads(cores)
+    return {"value": dt / (steps * n_l) * 1e6, "unit": "us/layer", "cores": cores,
+            "kind": "oracle", "cpu": cpu_model(),
+            "single_core_us_per_layer": round(dt1 / (steps1 * n_l) * 1e6, 1),
             "sample": f"{ws.name}: layers {layer0}..{layer0 + n_l - 1} (one sharing block), all {w.batch} "
                       f"sequences x {w.n_kv_heads} kv heads, {steps} decode steps over {len(qs)} distinct "
-                      f"queries (selection + sparse attention), fp64, {dt:.2f} s total"}
+                      f"queries (selection + sparse attention), fp64, {dt:.2f} s total on {cores} threads; "
+                      f"then {steps1} steps on one thread ({dt1:.2f} s)"}
+
+
+def cpu_model():
+    try:
+        for ln in open("/proc/cpuinfo"):
+            if ln.startswith("model name"):
+                return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 def commonality(w, path, q, args, M, torch, dev, mk):

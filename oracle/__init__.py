@@ -46,6 +46,7 @@ def lib():
             "mpcref_commonality": ([I] * 4 + [V, V], ctypes.c_int),
             "mpcref_dense_decode_attn": ([I] * 7 + [V] * 3 + [F, V, V], ctypes.c_int),
             "mpcref_threads": ([], ctypes.c_int),
+            "mpcref_set_threads": ([I], None),
         }
         for name, (args, res) in sigs.items():
             fn = getattr(L, name)
@@ -98,6 +99,11 @@ def level2_keep(keep, ratio, cluster, n_cand):
 
 def threads():
     return lib().mpcref_threads()
+
+
+def set_threads(n):
+    """Threads of the oracle's parallel loops from now on (timing only)."""
+    lib().mpcref_set_threads(int(n))
 
 
 # ------------------------------------------------------------------ per head

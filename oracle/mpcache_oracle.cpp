@@ -599,3 +599,6 @@ int mpcref_commonality(int32_t L, int32_t units, int32_t k, int32_t m, const int
 }
 
 int mpcref_threads(void) { return omp_get_max_threads(); }
+void mpcref_set_threads(int n) {
+  if (n >= 1) omp_set_num_threads(n);
+}

@@ -95,6 +95,8 @@ int mpcref_dense_decode_attn(int32_t B, int32_t n_layers, int32_t Hq, int32_t Hk
  * idx [L][units][k] -> out [units]. */
 int mpcref_commonality(int32_t L, int32_t units, int32_t k, int32_t m, const int32_t* idx, double* out);
 int mpcref_threads(void);
+/* Threads the OpenMP loops use from now on (n >= 1); for timing on a chosen number of cores. */
+void mpcref_set_threads(int n);
 
 #ifdef __cplusplus
 }
