@@ -131,6 +131,35 @@ def measure_read_ceiling(dev, chunk_bytes=16384, per_wg=24, total=2 << 30):
                     "attention's pattern)"}
 
 
+def measure_mfma_ceiling(dev, grid=2048, iters=2048):
+    """bf16 matrix-core throughput of a kernel that does nothing but chains of the 32x32x16
+    instruction the scoring passes use (four independent accumulators per wave)."""
+    import ctypes
+
+    import torch
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2501_06807_amd", "libmpc_ceiling.so"))
+    lib.mpc_mfma_ceiling.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+    sink = torch.empty(grid * 256, dtype=torch.float32, device=dev)
+    st = torch.cuda.current_stream(dev)
+
+    def launch():
+        rc = lib.mpc_mfma_ceiling(grid, iters, sink.data_ptr(), st.cuda_stream)
+        if rc != 0:
+            raise RuntimeError(f"matrix-core ceiling kernel failed to launch ({rc})")
+
+    launch()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(st)
+    for _ in range(3):
+        launch()
+    b.record(st)
+    torch.cuda.synchronize()
+    flop = 3.0 * grid * 4 * iters * 4 * 32768
+    tf = flop / (a.elapsed_time(b) * 1e-3) / 1e12
+    return {"TFLOPs": round(tf, 1), "frac_of_peak": round(tf / MFMA_PEAK_TFLOPS["bf16"], 4),
+            "note": "chains of v_mfma_f32_32x32x16_bf16 on registers, 4 accumulators per wave, 8192 waves"}
+
+
 def prefill_flops(w, n_owner):
     """One causal pass of window scores q_t . k_j (2d flops each) over the owner layers."""
     rows = sum(w.T - w.window + t + 1 for t in range(w.window))
@@ -265,6 +294,7 @@ def main():
     copy_gbs = 2 * (1 << 30) * 5 / (c0.elapsed_time(c1) * 1e-3) / 1e9
     del src, dst
     read_ceiling = measure_read_ceiling(dev)
+    mfma_ceiling = measure_mfma_ceiling(dev)
 
     # inputs, generated on the device
     sp = synth.spec(w)
@@ -455,6 +485,7 @@ def main():
         "copy_ceiling": {"GBps": round(copy_gbs, 1), "frac_of_peak": round(copy_gbs / HBM_PEAK_GBS, 4),
                          "note": "1 GiB device-to-device copy, read + write bytes"},
         "read_ceiling": dict(read_ceiling, attention_frac_of_ceiling=round(att_gbs / read_ceiling["GBps"], 4)),
+        "mfma_ceiling": mfma_ceiling,
         "prefill": {"ms_per_pass": round(mean(pre_ms), 3), "owner_layers": len(owners),
                     "ms_per_owner_layer": round(mean(pre_ms) / len(owners), 3),
                     "algorithmic_TFLOP_per_pass": round(fl / 1e12, 3),

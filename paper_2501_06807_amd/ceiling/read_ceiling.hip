@@ -1,8 +1,11 @@
-// Measured read ceiling for the roofline context of the decode kernels (not part of the method):
+// Measured ceilings for the roofline context (not part of the method). Read ceiling of the decode
+// kernels:
 // every workgroup reads `per_wg` contiguous chunks of `chunk_bytes`, taken in a caller-given
 // (random) order, with 16-byte coalesced loads, four in flight per thread — the access pattern of
 // the sparse attention, which reads whole clusters of K / V rows. One XOR per thread is written to
-// `sink` so that the loads are kept.
+// `sink` so that the loads are kept. Matrix-core ceiling of the static-scoring passes: every wave
+// runs chains of the bf16 32x32x16 matrix instruction on register operands, four independent
+// accumulators in flight, and writes its accumulators to `sink`.
 #include <hip/hip_runtime.h>
 #include <cstdint>
 
@@ -35,7 +38,44 @@ __global__ __launch_bounds__(kThreads) void k_read_chunks(const uint4* __restric
   sink[(size_t)blockIdx.x * kThreads + threadIdx.x] = acc;
 }
 
+typedef float f32x16 __attribute__((__vector_size__(16 * sizeof(float))));
+typedef __bf16 bf16x8 __attribute__((__vector_size__(8 * sizeof(__bf16))));
+constexpr int kChains = 4;
+
+__global__ __launch_bounds__(kThreads) void k_mfma(int iters, float seed, float* __restrict__ sink) {
+  bf16x8 a, b;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    a[i] = (__bf16)(seed * (float)(threadIdx.x + i));
+    b[i] = (__bf16)(seed * (float)(blockIdx.x - i));
+  }
+  f32x16 acc[kChains];
+#pragma unroll
+  for (int c = 0; c < kChains; ++c)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) acc[c][i] = 0.f;
+#pragma unroll 4
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int c = 0; c < kChains; ++c) acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[c], 0, 0, 0);
+  }
+  float t = 0.f;
+#pragma unroll
+  for (int c = 0; c < kChains; ++c)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) t += acc[c][i];
+  sink[(size_t)blockIdx.x * kThreads + threadIdx.x] = t;
+}
+
 }  // namespace
+
+// grid workgroups of 256 threads, each wave running `iters` x 4 matrix instructions (32768 flop
+// each); sink: grid * 256 floats. Returns a hipError_t code (0 = launched).
+extern "C" int mpc_mfma_ceiling(int grid, int iters, float* sink, void* stream) {
+  if (!sink || grid <= 0 || iters <= 0) return (int)hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_mfma, dim3(grid), dim3(kThreads), 0, (hipStream_t)stream, iters, 1e-3f, sink);
+  return (int)hipGetLastError();
+}
 
 // buf: n_chunks * chunk_bytes bytes; order: grid * per_wg chunk ids in [0, n_chunks); sink: grid *
 // 256 words. Returns a hipError_t code (0 = launched).
