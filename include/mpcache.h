@@ -7,7 +7,10 @@
  *   - query-aware two-level cluster selection with cross-layer index sharing (Sec. 3.3, 3.4;
  *     Alg. 3 step 2);
  *   - gather + softmax attention over the selected clusters (Alg. 1 steps 3-4);
- *   - decode-time growth of the kept cache (App. A.3: each decoded token's k, v are appended).
+ *   - decode-time growth of the kept cache (App. A.3: each decoded token's k, v are appended);
+ *   - the commonality score of adjacent layers' top-k sets (Sec. 3, Observation 3).
+ * mpc_prefill runs the first two steps as one call; mpc_decode_step runs selection and attention
+ * as one launch.
  *
  * Conventions shared by every entry point
  *   - Tensor arguments are DEVICE pointers owned by the caller, contiguous row-major, with
