@@ -97,12 +97,16 @@ CASES = {
     "C5": dict(n_layers=1, n_q_heads=8, n_kv_heads=2, T=4096, window=409, keep=1024, hh_count=8,
                hh_hi=4096 - 32),
     "X1": dict(n_layers=2, batch=2, n_q_heads=4, n_kv_heads=4),
+    # the other element types at the other head dim, ragged window rows and key blocks
+    "C3-fp16": dict(n_layers=1, n_q_heads=4, n_kv_heads=2, dtype="fp16", T=2000, window=400, keep=1024),
+    "C3-fp32": dict(n_layers=1, n_q_heads=2, n_kv_heads=2, dtype="fp32", T=1500, window=300, keep=768),
+    "C2-bf16": dict(n_layers=2, n_q_heads=4, n_kv_heads=2, dtype="bf16", T=1300, window=260, keep=640),
 }
 
 
 @pytest.mark.parametrize("name", list(CASES))
 def test_static_evict_matches_oracle(name):
-    w = synth.get(name).with_(**CASES[name])
+    w = synth.get(name.split("-")[0]).with_(**CASES[name])  # "C3-fp16": workload C3, overridden
     say(f"[evict] {name} L={w.n_layers} B={w.batch} Hq={w.n_q_heads} Hkv={w.n_kv_heads} T={w.T} "
         f"W={w.window} keep={w.keep} {w.dtype}")
     qw, k, v = _prefill(w)
