@@ -127,8 +127,8 @@ def measure_read_ceiling(dev, chunk_bytes=16384, per_wg=24, total=2 << 30):
     gbs = 5 * grid * per_wg * chunk_bytes / (a.elapsed_time(b) * 1e-3) / 1e9
     del buf, order, sink
     return {"GBps": round(gbs, 1), "frac_of_peak": round(gbs / HBM_PEAK_GBS, 4),
-            "note": "every 16 KB chunk of 2 GiB read once in random order, 16-byte loads (the sparse "
-                    "attention's pattern)"}
+            "note": "every 16 KB chunk of 2 GiB read once in random order, 16-byte non-temporal loads (the "
+                    "sparse attention's pattern)"}
 
 
 def measure_mfma_ceiling(dev, grid=2048, iters=2048):

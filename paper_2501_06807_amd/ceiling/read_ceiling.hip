@@ -1,8 +1,8 @@
 // Measured ceilings for the roofline context (not part of the method). Read ceiling of the decode
 // kernels:
 // every workgroup reads `per_wg` contiguous chunks of `chunk_bytes`, taken in a caller-given
-// (random) order, with 16-byte coalesced loads, four in flight per thread — the access pattern of
-// the sparse attention, which reads whole clusters of K / V rows. One XOR per thread is written to
+// (random) order, with 16-byte coalesced non-temporal loads, four in flight per thread — the access
+// pattern of the sparse attention, which reads whole clusters of K / V rows with the same hint. One XOR per thread is written to
 // `sink` so that the loads are kept. Matrix-core ceiling of the static-scoring passes: every wave
 // runs chains of the bf16 32x32x16 matrix instruction on register operands, four independent
 // accumulators in flight, and writes its accumulators to `sink`.
@@ -13,6 +13,12 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kInFlight = 4;
+
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 load_stream(const uint4* p) {
+  const u32x4_t v = __builtin_nontemporal_load((const u32x4_t*)p);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
 
 __global__ __launch_bounds__(kThreads) void k_read_chunks(const uint4* __restrict__ buf,
                                                           const int32_t* __restrict__ order, int per_wg,
@@ -26,13 +32,13 @@ __global__ __launch_bounds__(kThreads) void k_read_chunks(const uint4* __restric
 #pragma unroll
     for (int u = 0; u < kInFlight; ++u) {
       const int jj = j + u * kThreads;
-      v[u] = buf[(size_t)mine[jj / chunk16] * chunk16 + jj % chunk16];
+      v[u] = load_stream(buf + (size_t)mine[jj / chunk16] * chunk16 + jj % chunk16);
     }
 #pragma unroll
     for (int u = 0; u < kInFlight; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
   }
   for (; j < n; j += kThreads) {
-    const uint4 v = buf[(size_t)mine[j / chunk16] * chunk16 + j % chunk16];
+    const uint4 v = load_stream(buf + (size_t)mine[j / chunk16] * chunk16 + j % chunk16);
     acc ^= v.x ^ v.y ^ v.z ^ v.w;
   }
   sink[(size_t)blockIdx.x * kThreads + threadIdx.x] = acc;

@@ -455,6 +455,8 @@ mpc_status prepare_decode(const mpc_dims* dims, int32_t Ts, int32_t n_tail, int3
   a.cache_div = per_q_head ? Gkv : 1;
   a.splits = plan->splits;
   a.qscale = (float)((double)sm_scale * 1.4426950408889634);
+  const long long gathered = 2ll * units * n_list * cluster_size * dims->head_dim * elt_size(dims->dtype);
+  a.stream_kv = gathered > mpc::kStreamKvBytes;
   *da = a;
   *units_out = units;
   *G_out = G;

@@ -130,6 +130,13 @@ __device__ __forceinline__ void store_elt<F16>(void* base, size_t i, float x) {
 
 __device__ __forceinline__ uint4 ldg16(const void* p) { return *(const uint4*)p; }
 
+// The same with the non-temporal hint.
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 ldg16_stream(const void* p) {
+  const u32x4_t v = __builtin_nontemporal_load((const u32x4_t*)p);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
 // Device-coherent (agent-scope) accesses for data exchanged between workgroups of one launch:
 // they go through the coherent path of the per-die L2s without a cache write-back fence.
 __device__ __forceinline__ void st_coherent(float* p, float v) {

@@ -23,7 +23,14 @@ struct DecodeArgs {
   int rows;            // allocated rows per (layer, sequence, kv head)
   int n_tail;          // rows [Ts, Ts + n_tail) attended by every head (Ts % s == 0 if n_tail > 0)
   float qscale;        // sm_scale * log2(e)
+  int stream_kv;       // 1: the gathered K / V rows are loaded with the non-temporal hint
 };
+
+// Gathered K / V bytes of one call above which the rows are loaded with the non-temporal hint:
+// half the 256 MB memory-side cache. Smaller calls keep them cached, since the next decode step
+// selects many of the same clusters again; larger ones would only displace the representatives
+// the next selection reads.
+constexpr long long kStreamKvBytes = 128ll << 20;
 
 struct DecodePlan {
   int waves;   // waves per workgroup

@@ -6,6 +6,16 @@
 namespace mpc {
 namespace dev {
 
+// A gathered K / V row chunk: plain, or with the non-temporal hint (read once per call, so it
+// streams through the caches without displacing what the next call reads again).
+template <bool STREAM>
+__device__ __forceinline__ uint4 kv_load(const void* p) {
+  if constexpr (STREAM)
+    return ldg16_stream(p);
+  else
+    return ldg16(p);
+}
+
 constexpr int kMaxSel = 1024;
 
 // Byte offset of a unit's K/V block: (layer, sequence) of the unit, then its cache head.
@@ -105,8 +115,9 @@ __device__ __forceinline__ void finish_unit(const DecodeArgs& a, int unit, int s
 }
 
 // Attention of one work unit (or one split of it). COH_SEL: read the selection with
-// device-coherent loads (it was written by another workgroup of the same launch).
-template <class DT, int D, int G, int NW, int U, bool COH_SEL>
+// device-coherent loads (it was written by another workgroup of the same launch). STREAM: load the
+// gathered K / V rows with the non-temporal hint.
+template <class DT, int D, int G, int NW, int U, bool COH_SEL, bool STREAM>
 __device__ __forceinline__ void attend_unit(const DecodeArgs& a, int unit, int split) {
   constexpr int EPL = DT::kVec;
   constexpr int LPR = D / EPL;
@@ -180,8 +191,8 @@ __device__ __forceinline__ void attend_unit(const DecodeArgs& a, int unit, int s
       const int r = c * a.s + crow[u];
       ok[u] = (sl < hi) & (c >= 0) & (r < rows_end);
       const unsigned off = (unsigned)(ok[u] ? r : 0) * (unsigned)(D * DT::kElt) + (unsigned)(li * 16);
-      kr[u] = ldg16(kbase + off);
-      vr[u] = ldg16(vbase + off);
+      kr[u] = kv_load<STREAM>(kbase + off);
+      vr[u] = kv_load<STREAM>(vbase + off);
       crow[u] += step_row;
       cpos[u] += step_pos;
       if (crow[u] >= a.s) {
@@ -313,7 +324,7 @@ __device__ __forceinline__ float wave_max(float x) {
   return x;
 }
 
-template <class DT, int D, int NW, bool COH_SEL>
+template <class DT, int D, int NW, bool COH_SEL, bool STREAM>
 __device__ __forceinline__ void attend_unit_g4(const DecodeArgs& a, int unit, int split) {
   constexpr int G = 4;
   constexpr int EPL = 8;              // 16-bit elements per 16-byte vector
@@ -386,13 +397,13 @@ __device__ __forceinline__ void attend_unit_g4(const DecodeArgs& a, int unit, in
     const unsigned koff = row_of(0, base + w * 16 + tk, okk);
     uint4 kr[KK];
 #pragma unroll
-    for (int kk = 0; kk < KK; ++kk) kr[kk] = ldg16(kbase + koff + (kk * 32 + kq * 8) * DT::kElt);
+    for (int kk = 0; kk < KK; ++kk) kr[kk] = kv_load<STREAM>(kbase + koff + (kk * 32 + kq * 8) * DT::kElt);
     uint4 vr[UV];
 #pragma unroll
     for (int u = 0; u < UV; ++u) {
       bool okv;
       const unsigned voff = row_of(1 + u, base + w * 16 + u * RPW + rg, okv);
-      vr[u] = ldg16(vbase + voff + li * 16);  // a masked row contributes p = 0
+      vr[u] = kv_load<STREAM>(vbase + voff + li * 16);  // a masked row contributes p = 0
     }
     f32x4_t sacc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -462,12 +473,12 @@ __device__ __forceinline__ void attend_unit_g4(const DecodeArgs& a, int unit, in
 
 // The attention path of a unit: matrix-core scores for four-head groups of 16-bit rows, the VALU
 // path otherwise.
-template <class DT, int D, int G, int NW, int U, bool COH_SEL>
+template <class DT, int D, int G, int NW, int U, bool COH_SEL, bool STREAM>
 __device__ __forceinline__ void attend(const DecodeArgs& a, int unit, int split) {
   if constexpr (G == 4 && DT::kElt == 2)
-    attend_unit_g4<DT, D, NW, COH_SEL>(a, unit, split);
+    attend_unit_g4<DT, D, NW, COH_SEL, STREAM>(a, unit, split);
   else
-    attend_unit<DT, D, G, NW, U, COH_SEL>(a, unit, split);
+    attend_unit<DT, D, G, NW, U, COH_SEL, STREAM>(a, unit, split);
 }
 
 }  // namespace dev
