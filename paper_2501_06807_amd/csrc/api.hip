@@ -455,8 +455,11 @@ mpc_status prepare_decode(const mpc_dims* dims, int32_t Ts, int32_t n_tail, int3
   a.cache_div = per_q_head ? Gkv : 1;
   a.splits = plan->splits;
   a.qscale = (float)((double)sm_scale * 1.4426950408889634);
-  const long long gathered = 2ll * units * n_list * cluster_size * dims->head_dim * elt_size(dims->dtype);
-  a.stream_kv = gathered > mpc::kStreamKvBytes;
+  // K rows stay cacheable while they fit the memory-side cache together with what the next
+  // selection reads: the fine-cluster representatives of the call's units (C rows of d floats each)
+  const long long k_bytes = 1ll * units * n_list * cluster_size * dims->head_dim * elt_size(dims->dtype);
+  const long long rep_bytes = 1ll * units * C * dims->head_dim * 4;
+  a.stream_k = k_bytes + rep_bytes > mpc::kStreamKBytes;
   *da = a;
   *units_out = units;
   *G_out = G;

@@ -23,14 +23,16 @@ struct DecodeArgs {
   int rows;            // allocated rows per (layer, sequence, kv head)
   int n_tail;          // rows [Ts, Ts + n_tail) attended by every head (Ts % s == 0 if n_tail > 0)
   float qscale;        // sm_scale * log2(e)
-  int stream_kv;       // 1: the gathered K / V rows are loaded with the non-temporal hint
+  int stream_k;        // 1: the gathered K rows too are loaded with the non-temporal hint (V rows
+                       // always are)
 };
 
-// Gathered K / V bytes of one call above which the rows are loaded with the non-temporal hint:
-// half the 256 MB memory-side cache. Smaller calls keep them cached, since the next decode step
-// selects many of the same clusters again; larger ones would only displace the representatives
-// the next selection reads.
-constexpr long long kStreamKvBytes = 128ll << 20;
+// Working set of one decode step above which the gathered K rows are loaded with the non-temporal
+// hint: the 256 MB memory-side cache. The working set is the call's K rows plus the fine-cluster
+// representatives of its units, which the next selection reads. While both fit, the K rows stay
+// cacheable, since later steps select many of the same clusters again; beyond it they would only
+// displace the representatives. V rows are read once, after their scores, and always stream.
+constexpr long long kStreamKBytes = 256ll << 20;
 
 struct DecodePlan {
   int waves;   // waves per workgroup

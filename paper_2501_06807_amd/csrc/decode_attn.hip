@@ -13,15 +13,15 @@
 namespace mpc {
 namespace {
 
-template <class DT, int D, int G, int NW, int U, bool STREAM>
+template <class DT, int D, int G, int NW, int U, bool STREAM_K>
 __global__ __launch_bounds__(NW* kWave) void k_sparse_decode(DecodeArgs a) {
-  dev::attend<DT, D, G, NW, U, false, STREAM>(a, blockIdx.x / a.splits, blockIdx.x % a.splits);
+  dev::attend<DT, D, G, NW, U, false, STREAM_K>(a, blockIdx.x / a.splits, blockIdx.x % a.splits);
 }
 
 template <class DT, int D, int G>
 hipError_t launch_dt_d_g(const DecodeArgs& a, int units, const DecodePlan& p, hipStream_t st) {
   (void)p;
-  if (a.stream_kv)
+  if (a.stream_k)
     hipLaunchKernelGGL((k_sparse_decode<DT, D, G, 8, 4, true>), dim3(units * a.splits), dim3(8 * kWave), 0, st, a);
   else
     hipLaunchKernelGGL((k_sparse_decode<DT, D, G, 8, 4, false>), dim3(units * a.splits), dim3(8 * kWave), 0, st, a);

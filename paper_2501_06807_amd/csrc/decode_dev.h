@@ -115,9 +115,9 @@ __device__ __forceinline__ void finish_unit(const DecodeArgs& a, int unit, int s
 }
 
 // Attention of one work unit (or one split of it). COH_SEL: read the selection with
-// device-coherent loads (it was written by another workgroup of the same launch). STREAM: load the
-// gathered K / V rows with the non-temporal hint.
-template <class DT, int D, int G, int NW, int U, bool COH_SEL, bool STREAM>
+// device-coherent loads (it was written by another workgroup of the same launch). The gathered V
+// rows are loaded with the non-temporal hint; the K rows too when STREAM_K.
+template <class DT, int D, int G, int NW, int U, bool COH_SEL, bool STREAM_K>
 __device__ __forceinline__ void attend_unit(const DecodeArgs& a, int unit, int split) {
   constexpr int EPL = DT::kVec;
   constexpr int LPR = D / EPL;
@@ -191,8 +191,8 @@ __device__ __forceinline__ void attend_unit(const DecodeArgs& a, int unit, int s
       const int r = c * a.s + crow[u];
       ok[u] = (sl < hi) & (c >= 0) & (r < rows_end);
       const unsigned off = (unsigned)(ok[u] ? r : 0) * (unsigned)(D * DT::kElt) + (unsigned)(li * 16);
-      kr[u] = kv_load<STREAM>(kbase + off);
-      vr[u] = kv_load<STREAM>(vbase + off);
+      kr[u] = kv_load<STREAM_K>(kbase + off);
+      vr[u] = kv_load<true>(vbase + off);
       crow[u] += step_row;
       cpos[u] += step_pos;
       if (crow[u] >= a.s) {
@@ -324,7 +324,7 @@ __device__ __forceinline__ float wave_max(float x) {
   return x;
 }
 
-template <class DT, int D, int NW, bool COH_SEL, bool STREAM>
+template <class DT, int D, int NW, bool COH_SEL, bool STREAM_K>
 __device__ __forceinline__ void attend_unit_g4(const DecodeArgs& a, int unit, int split) {
   constexpr int G = 4;
   constexpr int EPL = 8;              // 16-bit elements per 16-byte vector
@@ -397,13 +397,13 @@ __device__ __forceinline__ void attend_unit_g4(const DecodeArgs& a, int unit, in
     const unsigned koff = row_of(0, base + w * 16 + tk, okk);
     uint4 kr[KK];
 #pragma unroll
-    for (int kk = 0; kk < KK; ++kk) kr[kk] = kv_load<STREAM>(kbase + koff + (kk * 32 + kq * 8) * DT::kElt);
+    for (int kk = 0; kk < KK; ++kk) kr[kk] = kv_load<STREAM_K>(kbase + koff + (kk * 32 + kq * 8) * DT::kElt);
     uint4 vr[UV];
 #pragma unroll
     for (int u = 0; u < UV; ++u) {
       bool okv;
       const unsigned voff = row_of(1 + u, base + w * 16 + u * RPW + rg, okv);
-      vr[u] = kv_load<STREAM>(vbase + voff + li * 16);  // a masked row contributes p = 0
+      vr[u] = kv_load<true>(vbase + voff + li * 16);  // a masked row contributes p = 0
     }
     f32x4_t sacc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -473,12 +473,12 @@ __device__ __forceinline__ void attend_unit_g4(const DecodeArgs& a, int unit, in
 
 // The attention path of a unit: matrix-core scores for four-head groups of 16-bit rows, the VALU
 // path otherwise.
-template <class DT, int D, int G, int NW, int U, bool COH_SEL, bool STREAM>
+template <class DT, int D, int G, int NW, int U, bool COH_SEL, bool STREAM_K>
 __device__ __forceinline__ void attend(const DecodeArgs& a, int unit, int split) {
   if constexpr (G == 4 && DT::kElt == 2)
-    attend_unit_g4<DT, D, NW, COH_SEL, STREAM>(a, unit, split);
+    attend_unit_g4<DT, D, NW, COH_SEL, STREAM_K>(a, unit, split);
   else
-    attend_unit<DT, D, G, NW, U, COH_SEL, STREAM>(a, unit, split);
+    attend_unit<DT, D, G, NW, U, COH_SEL, STREAM_K>(a, unit, split);
 }
 
 }  // namespace dev

@@ -66,8 +66,8 @@ __global__ __launch_bounds__(kFusedWaves* kWave) void k_decode_step(FusedArgs f)
     __syncthreads();
     if (tid == 0) __hip_atomic_store(&f.state[head], 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
-  // the rows stream past the caches: the representatives that selections of this same launch are
-  // still reading stay resident
+  // K rows stream past the caches too: the representatives that selections of this same launch
+  // are still reading stay resident
   if (mode != 0) dev::attend<DT, D, G, kFusedWaves, 4, true, true>(f.d, unit, 0);
 
   if (head >= 0) {
