@@ -17,6 +17,16 @@ from gpu_util import assert_out_close, assert_sets_tie_equal, boundary_score, ra
 pytestmark = pytest.mark.gpu
 
 FULL = ["C3", "C4", "C5", "X1"]
+# 128K GQA with four independent sequences: the decode step's working set passes the memory-side
+# cache, so the four-head attention path runs with streamed K rows
+EXTRA_DECODE = {"C5-B4": ("C5", dict(batch=4, seq_stride=1000))}
+
+
+def _workload(name):
+    if name in EXTRA_DECODE:
+        base, over = EXTRA_DECODE[name]
+        return synth.get(base).with_(**over)
+    return synth.get(name)
 
 
 def _path(w, T, keep_scores=False):
@@ -96,9 +106,9 @@ def test_fullsize_static_eviction(name):
     say("  sampled rows ok")
 
 
-@pytest.mark.parametrize("name", FULL)
+@pytest.mark.parametrize("name", FULL + list(EXTRA_DECODE))
 def test_fullsize_decode(name):
-    w = synth.get(name)
+    w = _workload(name)
     say(f"[full decode] {name} {w.name}")
     sp = synth.spec(w, T=w.keep, W=0, planting=False)
     rope = synth.rope_dev(w.keep, w.head_dim, w.rope_base) if w.rope else None
