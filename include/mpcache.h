@@ -127,7 +127,10 @@ size_t mpc_workspace_bytes(int32_t op, const mpc_dims* dims, int32_t T_or_Ts, co
  *   row_lse     [L][B][Hq][W] float, optional out: natural log-sum-exp of each window row's
  *               scaled scores (the softmax normaliser); owner layers only
  *   ws          workspace of mpc_workspace_bytes(MPC_OP_STATIC_EVICT, dims, T, cfg) bytes.
- * Accumulation: fp32 tensor-core dot products, softmax statistics and sums in fp64. */
+ * Accumulation: fp32 matrix-core dot products; each exponent is one fp32 fused multiply-add
+ * against a per-row fp32 offset of the row max, shared by the row sum and the column sums; sums of
+ * 16 terms in fp32, accumulated across tiles in fp64. token_score matches the exact scores within
+ * a relative 2e-5. */
 mpc_status mpc_static_evict(const mpc_dims* dims, int32_t T, const mpc_evict_cfg* cfg,
                             const void* q_win, const void* k, const void* v, int32_t* kept_idx,
                             void* k_out, void* v_out, float* token_score, float* row_lse,
