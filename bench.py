@@ -7,7 +7,10 @@ representatives, then every decode step of the workload (two-level selection wit
 sparse attention over all layers). The reported metric is the decode step's latency per layer
 (select + attention), measured with HIP events on the stream the kernels run on, with its
 effective HBM bandwidth against the 8 TB/s peak. Prefill figures are reported beside it, and so is
-the decode step in the other mode (two kernels, or one launch of mpc_decode_step).
+the decode step in the other mode (two kernels, or one launch of mpc_decode_step). Measured
+ceilings give the fractions a scale: a random-order chunk read (the attention's access pattern), a
+matrix-core throughput kernel, a device copy; the CPU oracle is timed on a bounded sample, on all
+host threads and on one.
 
 Prints one JSON line. Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload C4]
 """
