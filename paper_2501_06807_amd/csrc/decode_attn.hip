@@ -7,7 +7,9 @@
 // Lane layout: a K/V row of d elements is read as 16-byte vectors by LPR consecutive lanes, so a
 // wave reads RPW = 64 / LPR rows per load instruction, fully coalesced. The G query heads of the
 // group are served from the same loaded rows. Scores are kept in log2 units (q is pre-scaled by
-// sm_scale * log2 e) so the softmax uses the hardware exp2.
+// sm_scale * log2 e) so the softmax uses the hardware exp2. V rows are loaded with the
+// non-temporal hint; K rows too when the decode step's working set passes the memory-side cache
+// (DecodeArgs::stream_k, a template variant).
 #include "decode_dev.h"
 
 namespace mpc {

@@ -6,8 +6,8 @@
 namespace mpc {
 namespace dev {
 
-// A gathered K / V row chunk: plain, or with the non-temporal hint (read once per call, so it
-// streams through the caches without displacing what the next call reads again).
+// A gathered K / V row chunk: plain, or with the non-temporal hint, so that a row read once per
+// call streams through the caches without displacing what the next call reads again.
 template <bool STREAM>
 __device__ __forceinline__ uint4 kv_load(const void* p) {
   if constexpr (STREAM)
