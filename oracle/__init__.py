@@ -28,6 +28,7 @@ def lib():
             "mpcref_keep_tokens": ([I, D, I], I),
             "mpcref_level1_keep": ([I, D], I),
             "mpcref_level2_keep": ([I, D, I, I], I),
+            "mpcref_level2_keep_of_prompt": ([I, D, I, I], I),
             "mpcref_token_scores": ([I, I, I, I, I, F, I, V, V, V, V], ctypes.c_int),
             "mpcref_row_lse": ([I, I, I, I, F, I, V, I, V, V], ctypes.c_int),
             "mpcref_static_topk": ([I, V, I, I, V], ctypes.c_int),
@@ -95,6 +96,11 @@ def level1_keep(n_super, final_ratio):
 
 def level2_keep(keep, ratio, cluster, n_cand):
     return lib().mpcref_level2_keep(keep, ratio, cluster, n_cand)
+
+
+def level2_keep_of_prompt(T, ratio, cluster, n_cand):
+    """Level-2 budget with the dynamic ratio read against the prompt length T (Fig. 9 caption)."""
+    return lib().mpcref_level2_keep_of_prompt(T, ratio, cluster, n_cand)
 
 
 def threads():

@@ -122,6 +122,17 @@ int32_t mpcref_level2_keep(int32_t keep, double dynamic_ratio, int32_t cluster, 
   return std::min(n_cand, std::max(1, n));
 }
 
+// The other reading of the same budget: the Fig. 9 caption calls the selection ratio the "final
+// KV cache budget", i.e. a fraction of the prompt. Then eta * T tokens are selected, converted to
+// clusters of size s the same way (rounded down, at least one, at most the candidates). With a
+// static ratio r it selects 1 / r times as many clusters as the post-eviction reading (twice as
+// many on the GPT-2 workload: 16 instead of 8).
+int32_t mpcref_level2_keep_of_prompt(int32_t T, double dynamic_ratio, int32_t cluster, int32_t n_cand) {
+  if (T <= 0 || cluster <= 0 || n_cand <= 0) return 0;
+  const int32_t n = (int32_t)std::floor(dynamic_ratio * T / cluster + 1e-9);
+  return std::min(n_cand, std::max(1, n));
+}
+
 // ------------------------------------------------------------------------------- per head
 
 // Accumulated attention of the window queries (Sec. 3.2; Alg. 3 step 1): row t of the window is

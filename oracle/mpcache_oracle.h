@@ -35,6 +35,9 @@ int32_t mpcref_owner_layer(int32_t layer, int32_t period, int32_t start);
 int32_t mpcref_keep_tokens(int32_t T, double static_ratio, int32_t cluster);
 int32_t mpcref_level1_keep(int32_t n_super, double final_ratio);
 int32_t mpcref_level2_keep(int32_t keep, double dynamic_ratio, int32_t cluster, int32_t n_cand);
+/* Same budget with eta read as a fraction of the prompt length T (Fig. 9 caption), not of the
+ * post-eviction cache. */
+int32_t mpcref_level2_keep_of_prompt(int32_t T, double dynamic_ratio, int32_t cluster, int32_t n_cand);
 
 /* ---- per-head steps ---- */
 int mpcref_token_scores(int32_t G, int32_t d, int32_t T, int32_t W, int32_t dtype, float sm_scale,

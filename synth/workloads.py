@@ -108,5 +108,17 @@ WORKLOADS = {
 }
 
 
+# Level-2 budgets with the dynamic ratio read against the prompt length T instead of the kept cache
+# (the Fig. 9 caption's "final KV cache budget"): floor(eta * T / s) clusters, at most the
+# candidates. The tiny workload states its budget (8 clusters) outright, so it keeps it.
+K_CLUSTERS_OF_PROMPT = {"C1": 8, "C2": 16, "C3": 25, "C4": 51, "C5": 40, "X1": 25}
+
+
 def get(name: str) -> Workload:
+    """A workload by name; a trailing "-T" selects the reading of the dynamic ratio against the
+    prompt length (e.g. "C2-T": 16 clusters per selection instead of 8)."""
+    if name.endswith("-T"):
+        base = name[:-2]
+        w = WORKLOADS[base]
+        return w.with_(name=w.name + "-eta-of-prompt", k_clusters=K_CLUSTERS_OF_PROMPT[base])
     return WORKLOADS[name]

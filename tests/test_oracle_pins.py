@@ -45,6 +45,29 @@ def test_workload_integers_follow_the_rules(name):
     assert w.k_clusters == oracle.level2_keep(w.keep, w.dynamic_ratio, w.cluster, w.k_super * w.fanout)
 
 
+def test_level2_budget_of_the_prompt_reading():
+    # The Fig. 9 caption's "final KV cache budget" reads eta against the prompt: at the GPT-2 workload
+    # (T = 2048, static ratio 50%, eta = 12.5%, s = 16) that is 2048 / 8 / 16 = 16 clusters, twice
+    # the 8 clusters of the post-eviction reading.
+    w = synth.get("C2")
+    assert oracle.level2_keep(w.keep, w.dynamic_ratio, w.cluster, w.k_super * w.fanout) == 8
+    assert oracle.level2_keep_of_prompt(w.T, w.dynamic_ratio, w.cluster, w.k_super * w.fanout) == 16
+    # 128K GQA: 2% of 131072 tokens in clusters of 64 = 40.96 -> 40 clusters (10 under the other reading)
+    assert oracle.level2_keep_of_prompt(131072, 0.02, 64, 256) == 40
+    # rounding down, at least one cluster, at most the candidates
+    assert oracle.level2_keep_of_prompt(1000, 0.001, 16, 8) == 1
+    assert oracle.level2_keep_of_prompt(8192, 0.5, 32, 64) == 64
+    for name in ("C2", "C3", "C4", "C5", "X1"):
+        w = synth.get(name)
+        k = oracle.level2_keep_of_prompt(w.T, w.dynamic_ratio, w.cluster, w.k_super * w.fanout)
+        # the selected tokens are the largest whole-cluster count within eta * T
+        assert k * w.cluster <= w.dynamic_ratio * w.T < (k + 1) * w.cluster
+        assert synth.get(name + "-T").k_clusters == k
+        # with static ratio r the prompt reading selects about 1 / r times as many clusters
+        assert abs(k / w.k_clusters - 1 / w.static_ratio) <= 1 / w.k_clusters * (1 + 1 / w.static_ratio)
+    assert synth.get("C1-T").k_clusters == synth.get("C1").k_clusters == 8
+
+
 def test_workload_derived_sizes():
     # cluster / super-cluster counts and owner-layer counts of the five workloads
     exp = {"C1": (16, 4, 1), "C2": (64, 16, 7), "C3": (128, 16, 10), "C4": (307, 39, 10),
