@@ -10,7 +10,7 @@
  *   - decode-time growth of the kept cache (App. A.3: each decoded token's k, v are appended);
  *   - the commonality score of adjacent layers' top-k sets (Sec. 3, Observation 3).
  * mpc_prefill runs the first two steps as one call; mpc_decode_step runs selection and attention
- * as one launch.
+ * as one launch (mpc_decode_step_status reads its workspace's error word).
  *
  * Conventions shared by every entry point
  *   - Tensor arguments are DEVICE pointers owned by the caller, contiguous row-major, with
@@ -211,6 +211,13 @@ mpc_status mpc_sparse_decode_attn(const mpc_dims* dims, int32_t Ts, int32_t n_ta
  *   mpc_select_clusters; sel_score optional; out [L][B][Hq][d]; lse optional.
  *   ws: mpc_workspace_bytes(MPC_OP_DECODE_STEP, dims, Ts, cfg) bytes, zero-filled before its first
  *   use; every completed call leaves it ready for the next (calls sharing it must not overlap).
+ *   Layout: an int32 error word at offset 0 (sticky; read it with mpc_decode_step_status), then at
+ *   offset 256 one int32 state word per owner head of the block, in (owner layer, sequence, kv head)
+ *   order (0 free, 1 being selected, 2 published), then as many consumer counts.
+ * An attention unit waits for its owner head's selection with a bounded poll. If the bound is
+ * reached (no such case is known: it would take a selection that never gets published), the unit
+ * sets bit 0 of the error word and writes NaN to its out and lse rows instead of attending; the
+ * call still returns MPC_OK, since the status covers only validation and launch.
  * Blocks whose attention is split over several workgroups per unit, whose selection and attention
  * together need more LDS than one workgroup has, or that select per q-head (MPC_GROUP_HEAD) run the
  * two kernels one after the other instead (same results). */
@@ -219,6 +226,13 @@ mpc_status mpc_decode_step(const mpc_dims* dims, int32_t Ts, int32_t n_tail, con
                            const void* k_cache, const void* v_cache, float sm_scale, int32_t* sel,
                            float* sel_score, void* out, float* lse, void* ws, size_t ws_bytes,
                            void* stream);
+
+/* Error word of a decode-step workspace (the one passed to mpc_decode_step): *flags receives it,
+ * bit 0 set when an attention unit gave up waiting for its selection (its outputs are NaN). With
+ * clear != 0 a non-zero word is reset to zero. Reads and writes with blocking copies: call it after
+ * the stream of the decode steps that used `ws` has completed. ws_bytes: the workspace's size.
+ * Errors: MPC_EINVAL for NULL pointers, MPC_EWORKSPACE below 4 bytes, MPC_EHIP if a copy fails. */
+mpc_status mpc_decode_step_status(void* ws, size_t ws_bytes, int32_t clear, int32_t* flags);
 
 /* Decode-time growth of the kept cache (App. A.3: the k, v of each decoded token are appended to
  * the cache). The cache of a block is the pair (Ts, n_tail): clustered rows [0, Ts) with
@@ -233,11 +247,12 @@ mpc_status mpc_decode_step(const mpc_dims* dims, int32_t Ts, int32_t n_tail, con
  *   k_new, v_new [L][B][Hkv][d];  k_cache, v_cache [L][B][Hkv][Tcap][d] in/out;
  *   cent, scent [L][B][Hkv][Ccap / Scap][R][d] float in/out (cfg->similarity gives R).
  * Requires Ts % s == 0 and a row free after sealing (Ts + n_tail + 1 <= Tcap, Tcap =
- * dims->kv_capacity, which must be set). The caller keeps (Ts, n_tail) and passes them to the
- * selection (Ts) and attention (Ts, n_tail) calls. */
+ * dims->kv_capacity, which must be set). The new state is returned in *Ts_out and *n_tail_out
+ * (host pointers, each optional, written only on MPC_OK); the caller passes it to the selection
+ * (Ts) and attention (Ts, n_tail) calls and to the next append. */
 mpc_status mpc_append_kv(const mpc_dims* dims, int32_t Ts, int32_t n_tail, const mpc_select_cfg* cfg,
                          const void* k_new, const void* v_new, void* k_cache, void* v_cache,
-                         float* cent, float* scent, void* stream);
+                         float* cent, float* scent, int32_t* Ts_out, int32_t* n_tail_out, void* stream);
 
 /* Commonality score of m + 1 adjacent layers (Sec. 3, Observation 3), the paper's measure of how
  * far adjacent layers agree on their top-k sets:

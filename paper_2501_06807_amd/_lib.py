@@ -44,7 +44,8 @@ class MpcError(RuntimeError):
 
 _LIB = None
 EXPORTS = ("mpc_workspace_bytes", "mpc_static_evict", "mpc_build_clusters", "mpc_prefill", "mpc_select_clusters",
-           "mpc_sparse_decode_attn", "mpc_decode_step", "mpc_append_kv", "mpc_commonality", "mpc_owner_layer",
+           "mpc_sparse_decode_attn", "mpc_decode_step", "mpc_decode_step_status", "mpc_append_kv", "mpc_commonality",
+           "mpc_owner_layer",
            "mpc_status_string", "mpc_last_error")
 
 
@@ -65,10 +66,11 @@ def lib():
         L.mpc_sparse_decode_attn.argtypes = [P(MpcDims), I, I, I, V, V, V, V, I, I, F, V, V, V, ctypes.c_size_t, V]
         L.mpc_decode_step.argtypes = [P(MpcDims), I, I, P(MpcSelectCfg)] + [V] * 5 + [F] + [V] * 4 + [
             V, ctypes.c_size_t, V]
-        L.mpc_append_kv.argtypes = [P(MpcDims), I, I, P(MpcSelectCfg)] + [V] * 7
+        L.mpc_append_kv.argtypes = [P(MpcDims), I, I, P(MpcSelectCfg)] + [V] * 6 + [P(I), P(I), V]
+        L.mpc_decode_step_status.argtypes = [V, ctypes.c_size_t, I, P(I)]
         L.mpc_commonality.argtypes = [I, I, I, I, V, V, V]
         for fn in ("mpc_static_evict", "mpc_build_clusters", "mpc_prefill", "mpc_select_clusters", "mpc_sparse_decode_attn",
-                   "mpc_decode_step", "mpc_append_kv", "mpc_commonality"):
+                   "mpc_decode_step", "mpc_decode_step_status", "mpc_append_kv", "mpc_commonality"):
             getattr(L, fn).restype = ctypes.c_int
         L.mpc_owner_layer.argtypes = [I, I, I]
         L.mpc_owner_layer.restype = I
@@ -275,12 +277,6 @@ def mpc_commonality(idx, out, m, stream=None):
     _check("mpc_commonality", lib().mpc_commonality(L, units, k, m, _ptr(idx), _ptr(out), _stream(stream)))
 
 
-def append_state(Ts, n_tail, cluster_size):
-    """(Ts, n_tail) after one mpc_append_kv call: a full tail is sealed first, then the new row
-    joins the tail."""
-    return (Ts + cluster_size, 1) if n_tail == cluster_size else (Ts, n_tail + 1)
-
-
 def mpc_append_kv(k_new, v_new, k_cache, v_cache, cent, scent, cfg, *, Ts, n_tail, layer0=0, stream=None):
     """Appends one decoded token: k_new / v_new [L][B][Hkv][d] into k/v [L][B][Hkv][Tcap][d] (sealing a full
     tail into a cluster, whose representatives in cent / scent are rebuilt). Returns the new (Ts, n_tail)."""
@@ -293,7 +289,18 @@ def mpc_append_kv(k_new, v_new, k_cache, v_cache, cent, scent, cfg, *, Ts, n_tai
     C, S = _slots(k_cache.shape[3], cfg)
     if cent.shape[3] != C or scent.shape[3] != S:
         raise ValueError(f"cent / scent must have {C} / {S} slots for a capacity of {k_cache.shape[3]} rows")
+    ts_out, tail_out = ctypes.c_int32(), ctypes.c_int32()
     _check("mpc_append_kv", lib().mpc_append_kv(
         ctypes.byref(dims), Ts, n_tail, ctypes.byref(cfg), _ptr(k_new), _ptr(v_new), _ptr(k_cache), _ptr(v_cache),
-        _ptr(cent), _ptr(scent), _stream(stream)))
-    return append_state(Ts, n_tail, cfg.cluster_size)
+        _ptr(cent), _ptr(scent), ctypes.byref(ts_out), ctypes.byref(tail_out), _stream(stream)))
+    return ts_out.value, tail_out.value
+
+
+def mpc_decode_step_status(ws, clear=False):
+    """Error word of a decode-step workspace (bit 0: a unit gave up waiting for its selection and
+    wrote NaN outputs); blocking, call after the steps' stream has completed."""
+    _contig(ws)
+    flags = ctypes.c_int32()
+    _check("mpc_decode_step_status", lib().mpc_decode_step_status(_ptr(ws), ws.numel() * ws.element_size(),
+                                                                  int(bool(clear)), ctypes.byref(flags)))
+    return flags.value

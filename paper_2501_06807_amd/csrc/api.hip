@@ -568,7 +568,7 @@ mpc_status mpc_commonality(int32_t L, int32_t units, int32_t k, int32_t m, const
 
 mpc_status mpc_append_kv(const mpc_dims* dims, int32_t Ts, int32_t n_tail, const mpc_select_cfg* cfg,
                          const void* k_new, const void* v_new, void* k_cache, void* v_cache,
-                         float* cent, float* scent, void* stream) {
+                         float* cent, float* scent, int32_t* Ts_out, int32_t* n_tail_out, void* stream) {
   mpc_status s = check_dims(dims);
   if (s != MPC_OK) return s;
   if (!cfg) return fail(MPC_EINVAL, "cfg is NULL");
@@ -634,6 +634,24 @@ mpc_status mpc_append_kv(const mpc_dims* dims, int32_t Ts, int32_t n_tail, const
   ap.row = row;
   ap.row_bytes = dims->head_dim * elt_size(dims->dtype);
   if ((s = launched(mpc::launch_append_rows(ap, st), "append")) != MPC_OK) return s;
+  if (Ts_out) *Ts_out = Ts_new;
+  if (n_tail_out) *n_tail_out = seal ? 1 : n_tail + 1;
+  return ok();
+}
+
+mpc_status mpc_decode_step_status(void* ws, size_t ws_bytes, int32_t clear, int32_t* flags) {
+  if (!ws || !flags) return fail(MPC_EINVAL, "ws and flags must not be NULL");
+  if (ws_bytes < sizeof(mpc::FusedSync)) return fail(MPC_EWORKSPACE, "workspace smaller than its error word");
+  clear_stale_error();
+  mpc::FusedSync sync{};
+  if (hipMemcpy(&sync, ws, sizeof(sync), hipMemcpyDeviceToHost) != hipSuccess)
+    return fail(MPC_EHIP, "reading the error word: %s", hipGetErrorString(hipGetLastError()));
+  *flags = sync.error;
+  if (clear && sync.error) {
+    const mpc::FusedSync zero{};
+    if (hipMemcpy(ws, &zero, sizeof(zero), hipMemcpyHostToDevice) != hipSuccess)
+      return fail(MPC_EHIP, "clearing the error word: %s", hipGetErrorString(hipGetLastError()));
+  }
   return ok();
 }
 

@@ -11,7 +11,7 @@
 // is published with another device-coherent store; consumers poll it and read the selection with
 // device-coherent loads, so no L2 write-back fence is needed. The last consumer of a head returns
 // its words to zero for the next launch. A bounded poll turns a lost publication into an error
-// bit, never a hang.
+// bit and NaN outputs of the units that gave up, never a hang.
 #include "decode_dev.h"
 #include "fused.h"
 #include "select_dev.h"
@@ -68,7 +68,14 @@ __global__ __launch_bounds__(kFusedWaves* kWave) void k_decode_step(FusedArgs f)
   }
   // K rows stream past the caches too: the representatives that selections of this same launch
   // are still reading stay resident
-  if (mode != 0) dev::attend<DT, D, G, kFusedWaves, 4, true, true>(f.d, unit, 0);
+  if (mode != 0) {
+    dev::attend<DT, D, G, kFusedWaves, 4, true, true>(f.d, unit, 0);
+  } else {
+    // the selection never arrived: the unit's outputs become NaN, so they cannot pass for a result
+    const float nan = __builtin_nanf("");
+    for (int i = tid; i < G * D; i += kFusedWaves * kWave) store_elt<DT>(f.d.out, (size_t)unit * G * D + i, nan);
+    if (tid < G && f.d.lse) f.d.lse[(size_t)unit * G + tid] = nan;
+  }
 
   if (head >= 0) {
     __syncthreads();

@@ -224,7 +224,7 @@ def test_status_strings():
 def test_append_validation():
     cfg = L.select_cfg(16, 4, 2, 4)
     call = lambda d, Ts, nt, c=cfg: _status("mpc_append_kv", ctypes.byref(d), Ts, nt, ctypes.byref(c), FAKE, FAKE,
-                                            FAKE, FAKE, FAKE, FAKE, None)
+                                            FAKE, FAKE, FAKE, FAKE, None, None, None)
     d = _dims(kv_capacity=300)
     s, msg = call(d, 250, 3)
     assert s == L.MPC_ESHAPE and "multiple" in msg      # Ts not a multiple of s
@@ -238,9 +238,20 @@ def test_append_validation():
     bad = L.select_cfg(16, 4, 2, 4)
     bad.similarity = 5
     assert call(d, 272, 16, bad)[0] == L.MPC_EINVAL
+    ts_out, tail_out = ctypes.c_int32(-5), ctypes.c_int32(-5)
     s, _ = _status("mpc_append_kv", ctypes.byref(d), 272, 16, ctypes.byref(cfg), None, FAKE, FAKE, FAKE, FAKE, FAKE,
-                   None)
+                   ctypes.byref(ts_out), ctypes.byref(tail_out), None)
     assert s == L.MPC_EINVAL                               # k_new is NULL
+    assert (ts_out.value, tail_out.value) == (-5, -5)      # the new state is written only on success
+
+
+def test_decode_step_status_validation():
+    flags = ctypes.c_int32(-5)
+    s, msg = _status("mpc_decode_step_status", None, 1024, 0, ctypes.byref(flags))
+    assert s == L.MPC_EINVAL
+    assert _status("mpc_decode_step_status", FAKE, 1024, 0, None)[0] == L.MPC_EINVAL
+    assert _status("mpc_decode_step_status", FAKE, 2, 1, ctypes.byref(flags))[0] == L.MPC_EWORKSPACE
+    assert flags.value == -5
 
 
 def test_capacity_and_tail_validation():

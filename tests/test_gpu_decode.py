@@ -25,6 +25,10 @@ CASES = {
     "C4": dict(n_layers=3, layer0=4, heads=4),
     "C5": dict(n_layers=6, layer0=0, heads=None),
     "X1": dict(n_layers=4, layer0=0, heads=8),
+    # the dynamic ratio read against the prompt length: 16 clusters per selection at the GPT-2
+    # workload (8 under the post-eviction reading), 40 at the 128K GQA workload (10)
+    "C2-T": dict(n_layers=6, layer0=0, heads=None),
+    "C5-T": dict(n_layers=6, layer0=0, heads=None),
 }
 
 

@@ -37,6 +37,8 @@ CASES = {
     "C3-L8-mean": ("C3", dict(n_layers=8), 0, "mean"),
     # clusters of 4 tokens, fan-out 2: 1280 owner heads (one wave each), 2048 attention units
     "X1-L8": ("X1", dict(n_layers=8), 0),
+    # the dynamic ratio read against the prompt length (40 clusters per selection)
+    "C5-T-L32": ("C5-T", dict(keep=8192, k_super=8), 0),
 }
 
 
@@ -132,3 +134,60 @@ def test_decode_step_equals_two_calls_and_oracle(case):
         worst = assert_out_close(to_f64(o1), ref, w.dtype, case)
         np.testing.assert_allclose(l1.numpy(), lse_ref, rtol=1e-5, atol=1e-5)
         say(f"  step {step}: identical to two calls; tie swaps {swaps}; worst relative error {worst:.2e}")
+
+
+def test_decode_step_unit_that_gives_up_is_reported():
+    """A selection that is never published (forced from the host: one owner head's state word is
+    set to "being selected" before the launch, which no workgroup then computes) makes its consuming
+    units give up after their bounded poll: the error word reports it, those units' outputs are NaN,
+    every other unit matches the normal step, and the head's words are back at zero afterwards.
+    Every workgroup exits normally."""
+    w, layer0, k, v, cent, scent, sim = _setup("C3-L8")
+    import paper_2501_06807_amd as M
+    say("[step give-up] C3-L8: owner head (layer 2, b 0, h 0) marked claimed before the launch")
+    dt = synth.torch_dtype(w.dtype)
+    cfg = M.select_cfg(w.cluster, w.fanout, w.k_super, w.k_clusters, 0.6, w.share_period, similarity=sim)
+    kd, vd = bits_to_torch(k, w.dtype), bits_to_torch(v, w.dtype)
+    cent_d, scent_d = torch.from_numpy(cent).cuda(), torch.from_numpy(scent).cuda()
+    shape_sel = (w.n_layers, w.batch, w.n_kv_heads, w.k_clusters)
+    shape_out = (w.n_layers, w.batch, w.n_q_heads, w.head_dim)
+    sm = 1.0 / math.sqrt(w.head_dim)
+    dims = M.dims_of(torch.empty(shape_out, dtype=dt), kd, layer0)
+    ws = M.workspace(M.workspace_bytes(M.MPC_OP_DECODE_STEP, dims, w.keep, cfg), "cuda")
+    qd = bits_to_torch(_queries(w, layer0, 0), w.dtype)
+    owners = [l for l in range(w.n_layers) if oracle.owner_layer(l, w.share_period, w.share_start) == l]
+    n_heads = len(owners) * w.batch * w.n_kv_heads
+
+    def step():
+        sel = torch.zeros(shape_sel, dtype=torch.int32, device="cuda")
+        out = torch.zeros(shape_out, dtype=dt, device="cuda")
+        lse = torch.zeros(shape_out[:-1], dtype=torch.float32, device="cuda")
+        M.mpc_decode_step(qd, cent_d, scent_d, kd, vd, sel, out, cfg, sm_scale=sm, lse=lse, ws=ws)
+        torch.cuda.synchronize()
+        return out.float().cpu(), lse.cpu()
+
+    o_ref, l_ref = step()
+    assert M.mpc_decode_step_status(ws) == 0
+    # owner index 2 is layer 2, whose head (b 0, h 0) serves layers 2..5
+    o_idx = owners.index(2)
+    head = (o_idx * w.batch + 0) * w.n_kv_heads + 0
+    ws.view(torch.int32)[64 + head] = 1
+    torch.cuda.synchronize()
+    o_bad, l_bad = step()
+    assert M.mpc_decode_step_status(ws) == 1
+    layers = [l for l in range(w.n_layers) if oracle.owner_layer(l, w.share_period, w.share_start) == 2]
+    G = w.group
+    hit = torch.zeros(shape_out[:-1], dtype=torch.bool)
+    for l in layers:
+        hit[l, 0, 0:G] = True
+    assert torch.isnan(o_bad[hit]).all() and torch.isnan(l_bad[hit]).all()
+    assert torch.equal(o_bad[~hit], o_ref[~hit]) and torch.equal(l_bad[~hit], l_ref[~hit])
+    err, words = _sync_state(ws, n_heads)
+    assert err == 1 and not words.any()
+    # clearing the word; the next step is normal again
+    assert M.mpc_decode_step_status(ws, clear=True) == 1
+    assert M.mpc_decode_step_status(ws) == 0
+    o2, l2 = step()
+    assert torch.equal(o2, o_ref) and torch.equal(l2, l_ref)
+    assert M.mpc_decode_step_status(ws) == 0
+    say(f"  {int(hit.sum())} q-head outputs NaN after the give-up; error word cleared; next step identical")
