@@ -45,6 +45,9 @@ def parse():
     p.add_argument("--group", choices=("sum", "max", "head"), default="sum",
                    help="grouped q-heads: one selection per kv head scored by the sum (default) or the maximum of "
                         "its q-heads' similarities, or one selection per q-head")
+    p.add_argument("--extra", default="C3,C5",
+                   help="comma-separated workloads whose decode step is also measured (same pass structure, "
+                        "reported under other_workloads); '' for none")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--copy-calibration", action="store_true",
                    help="accepted for recorded profiling commands; the 1 GiB reference copy always runs")
@@ -265,6 +268,125 @@ def commonality(w, path, q, args, M, torch, dev, mk):
     return res
 
 
+PLANTING = ("sinks k <- k - (k.u)u + 4 sqrt(d) u; heavy hitters k <- 3 sqrt(d) u + 0.3 n, u the unit mean of the "
+            "group's window queries (the stated 0.7 q_mean + 0.3 noise makes them less attended than random keys)")
+
+
+def make_state(w, args, M, synth, dev):
+    """Device-resident inputs of one pass (window queries, prompt K/V, decode queries) and the
+    preallocated path."""
+    sp = synth.spec(w)
+    rope = synth.rope_dev(w.T, w.head_dim, w.rope_base) if w.rope else None
+    q_win = synth.qwin_dev(sp, w.dtype, 0, w.n_layers, rope)
+    k, v = synth.kv_dev(sp, w.dtype, 0, w.n_layers, q_win, rope)
+    del rope
+    E = args.decode_steps or w.steps
+    qs = [synth.dq_dev(sp, w.dtype, e) for e in range(E)]
+    path = M.MPCachePath(n_layers=w.n_layers, batch=w.batch, n_q_heads=w.n_q_heads, n_kv_heads=w.n_kv_heads,
+                         head_dim=w.head_dim, dtype=synth.torch_dtype(w.dtype), T=w.T, window=w.window,
+                         keep=w.keep, local_keep=w.local_keep, cluster=w.cluster, fanout=w.fanout,
+                         k_super=w.k_super, k_clusters=w.k_clusters, share_period=w.share_period,
+                         share_start=w.share_start, similarity=args.similarity, group=args.group)
+    return q_win, k, v, qs, path
+
+
+def timed_passes(path, q_win, k, v, qs, step_fn, steps, warmup, torch):
+    """`warmup` untimed passes, then `steps` timed passes (prefill, then every decode step back to
+    back), with HIP events on the launch stream at the pass boundaries and after the prefill.
+    Returns (prefill ms per pass, decode µs per step, wall seconds of the timed passes)."""
+    E = len(qs)
+    mk = lambda: torch.cuda.Event(enable_timing=True)
+
+    def one_pass(ev=None):
+        if ev:
+            ev[0].record()
+        path.prefill(q_win, k, v)
+        if ev:
+            ev[1].record()
+        for e in range(E):
+            step_fn(qs[e])
+        if ev:
+            ev[2].record()
+
+    for _ in range(warmup):
+        one_pass()
+    torch.cuda.synchronize()
+    evs = [(mk(), mk(), mk()) for _ in range(steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(steps):
+        one_pass(evs[s])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    pre_ms = [a.elapsed_time(b) for a, b, _ in evs]
+    dec_us = sum(b.elapsed_time(c) / E for _, b, c in evs) / steps * 1e3
+    return pre_ms, dec_us, wall
+
+
+def kernel_times(path, qs, torch):
+    """Per-launch averages of the selection and the attention kernel on the path's current state:
+    each launched once per decode step, back to back, between two HIP events (the attention reads
+    each step's own selection)."""
+    E = len(qs)
+    mk = lambda: torch.cuda.Event(enable_timing=True)
+
+    def step_time(fn):
+        a, b = mk(), mk()
+        a.record()
+        for e in range(E):
+            fn(qs[e])
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / E * 1e3
+
+    sels = []
+    for e in range(E):
+        path.select(qs[e])
+        sels.append(path.sel.clone())
+    calls = [path.attend_call(sv) for sv in sels]
+    state = {"it": iter(())}
+
+    def attend_next(q):
+        next(state["it"])(q)
+
+    step_time(path.select)
+    sel_us = step_time(path.select)
+    for _ in range(2):
+        state["it"] = iter(calls)
+        att_us = step_time(attend_next)
+    return sel_us, att_us
+
+
+def step_record(w, path, M, args, dec_us, sel_us, att_us):
+    """Decode-step figures of one workload: latency per layer, algorithmic bytes, bandwidth."""
+    owners = [l for l in range(w.n_layers) if M.owner_layer(l, w.share_period, w.share_start) == l]
+    sel_b, att_b = decode_bytes(w, owners, path.sel.cpu().numpy(), path.C, path.S, M.rep_rows(args.similarity))
+    gbs = (sel_b + att_b) / (dec_us * 1e-6) / 1e9
+    att_gbs = att_b / (att_us * 1e-6) / 1e9
+    return {"workload": f"{w.name}", "us_per_step": round(dec_us, 3), "us_per_layer": round(dec_us / w.n_layers, 4),
+            "algorithmic_bytes": sel_b + att_b, "achieved_GBps": round(gbs, 1),
+            "frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4), "select_us": round(sel_us, 3),
+            "attention_us": round(att_us, 3), "attention_algorithmic_bytes": att_b,
+            "attention_frac_of_hbm_peak": round(att_gbs / HBM_PEAK_GBS, 4)}
+
+
+def extra_workload(name, args, M, synth, torch, dev):
+    """The decode step of another workload, timed with the same pass structure as the headline."""
+    w = synth.get(name)
+    q_win, k, v, qs, path = make_state(w, args, M, synth, dev)
+    torch.cuda.synchronize()
+    step_fn = path.decode_fused if args.decode_mode == "fused" else path.decode
+    pre_ms, dec_us, _ = timed_passes(path, q_win, k, v, qs, step_fn, max(3, args.steps), max(1, args.warmup), torch)
+    del q_win, k, v
+    sel_us, att_us = kernel_times(path, qs, torch)
+    rec = step_record(w, path, M, args, dec_us, sel_us, att_us)
+    rec["prefill_ms_per_pass"] = round(sum(pre_ms) / len(pre_ms), 3)
+    rec["decode_steps_per_pass"] = len(qs)
+    del path, qs
+    torch.cuda.empty_cache()
+    return rec
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -300,17 +422,7 @@ def main():
     mfma_ceiling = measure_mfma_ceiling(dev)
 
     # inputs, generated on the device
-    sp = synth.spec(w)
-    rope = synth.rope_dev(w.T, w.head_dim, w.rope_base) if w.rope else None
-    q_win = synth.qwin_dev(sp, w.dtype, 0, w.n_layers, rope)
-    k, v = synth.kv_dev(sp, w.dtype, 0, w.n_layers, q_win, rope)
-    del rope
-    qs = [synth.dq_dev(sp, w.dtype, e) for e in range(E)]
-    path = M.MPCachePath(n_layers=w.n_layers, batch=w.batch, n_q_heads=w.n_q_heads, n_kv_heads=w.n_kv_heads,
-                         head_dim=w.head_dim, dtype=synth.torch_dtype(w.dtype), T=w.T, window=w.window,
-                         keep=w.keep, local_keep=w.local_keep, cluster=w.cluster, fanout=w.fanout,
-                         k_super=w.k_super, k_clusters=w.k_clusters, share_period=w.share_period,
-                         share_start=w.share_start, similarity=args.similarity, group=args.group)
+    q_win, k, v, qs, path = make_state(w, args, M, synth, dev)
     torch.cuda.synchronize()
 
     fused = args.decode_mode == "fused"
@@ -319,32 +431,9 @@ def main():
     mk = lambda: torch.cuda.Event(enable_timing=True)
     mean = lambda x: sum(x) / len(x)
 
-    def one_pass(ev=None):
-        if ev:
-            ev[0].record()
-        path.prefill(q_win, k, v)
-        if ev:
-            ev[1].record()
-        for e in range(E):
-            step_fn(qs[e])
-        if ev:
-            ev[2].record()
-
-    for _ in range(args.warmup):
-        one_pass()
-    torch.cuda.synchronize()
-
     # timed region: events only at the pass boundaries and after the prefill, so that the decode
     # steps run back to back as a serving loop would issue them
-    evs = [(mk(), mk(), mk()) for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for s in range(args.steps):
-        one_pass(evs[s])
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    pre_ms = [a.elapsed_time(b) for a, b, _ in evs]
-    dec_us = mean([b.elapsed_time(c) / E for _, b, c in evs]) * 1e3
+    pre_ms, dec_us, wall = timed_passes(path, q_win, k, v, qs, step_fn, args.steps, args.warmup, torch)
 
     # the same prefill as two calls (eviction with every layer's gather, then the cluster build
     # re-reading the kept keys); same inputs and results, second of two runs
@@ -367,22 +456,7 @@ def main():
         torch.cuda.synchronize()
         return a.elapsed_time(b) / E * 1e3
 
-    sels = []
-    for e in range(E):
-        path.select(qs[e])
-        sels.append(path.sel.clone())
-    calls = [path.attend_call(sv) for sv in sels]
-    att_fns = iter(())
-
-    def attend_next(q):
-        next(att_fns)(q)
-
-    step_time(path.select)
-    sel_us = step_time(path.select)
-    for _ in range(2):
-        att_fns = iter(calls)
-        att_us = step_time(attend_next)
-    del sels, calls
+    sel_us, att_us = kernel_times(path, qs, torch)
     alt = {}
     for name, fn in modes.items():  # every mode on the same state, E steps back to back
         if name != args.decode_mode:
@@ -451,7 +525,10 @@ def main():
         roofline = {"kernel": "k_sparse_decode (gather + online-softmax attention, all layers per launch)",
                     "bound": "hbm", "achieved": round(att_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                     "frac": round(att_gbs / HBM_PEAK_GBS, 4), "traffic": traffic,
-                    "algorithmic_bytes_per_launch": att_b, "avg_launch_us": round(att_us, 3)}
+                    "algorithmic_bytes_per_launch": att_b, "avg_launch_us": round(att_us, 3),
+                    "whole_step": {"kernels": "k_select + k_sparse_decode", "achieved": round(dec_gbs, 1),
+                                   "frac": round(dec_gbs / HBM_PEAK_GBS, 4), "algorithmic_bytes": step_b,
+                                   "us": round(dec_us, 3)}}
     fl = prefill_flops(w, len(owners))
     pre_tflops = fl / (mean(pre_ms) * 1e-3) / 1e12
 
@@ -472,7 +549,8 @@ def main():
                    "q_heads": w.n_q_heads, "kv_heads": w.n_kv_heads, "head_dim": w.head_dim, "prompt_tokens": w.T,
                    "window_rows": w.window, "kept_tokens": w.keep, "cluster": w.cluster, "fanout": w.fanout,
                    "k_super": w.k_super, "k_clusters": w.k_clusters, "share_period": w.share_period,
-                   "similarity": args.similarity, "group": args.group, "decode_steps_per_pass": E},
+                   "similarity": args.similarity, "group": args.group, "decode_steps_per_pass": E,
+                   **({"planting": PLANTING} if w.n_sinks or w.hh_count else {})},
         "decode_step": {"mode": args.decode_mode, "us": round(dec_us, 3), "algorithmic_bytes": step_b,
                         "achieved_GBps": round(dec_gbs, 1), "frac_of_hbm_peak": round(dec_gbs / HBM_PEAK_GBS, 4)},
         "kernels": {"select_us": round(sel_us, 3), "attention_us": round(att_us, 3),
@@ -498,6 +576,12 @@ def main():
                     "note": "one call (mpc_prefill): two score passes, top-k, gather of the layers without "
                             "representatives, cluster build gathering the other layers' rows; all layers"},
     }
+    extra = [x for x in args.extra.split(",") if x and x != args.workload]
+    if extra:
+        # free the headline workload's prompt and kept caches before the other workloads
+        del q_win, k, v, path, qs, modes, step_fn
+        torch.cuda.empty_cache()
+        rec["other_workloads"] = {x: extra_workload(x, args, M, synth, torch, dev) for x in extra}
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(w, min(E, 64), args.similarity, args.group)
     print(json.dumps(rec), flush=True)
