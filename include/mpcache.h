@@ -29,9 +29,10 @@
  *     first two layers never share, so start = 2 follows the paper's text; start = 0 gives the
  *     pairing of Alg. 3).
  *   - The library allocates nothing and keeps no global state except a thread-local message for
- *     the last error. Scratch memory is a caller-provided workspace of mpc_workspace_bytes()
- *     bytes (no initial contents needed). Calls that share one workspace must not overlap in
- *     time.
+ *     the last error and the static scratch array of mpc_static_evict_noalloc (with its device
+ *     addresses). Scratch memory is otherwise a caller-provided workspace of
+ *     mpc_workspace_bytes() bytes (no initial contents needed). Calls that share one workspace must
+ *     not overlap in time.
  *   - Every call is asynchronous on `stream` (a hipStream_t; NULL = default stream). The
  *     returned status covers argument validation and launch errors only; it never waits for the
  *     GPU. A validation failure (MPC_EINVAL / ESHAPE / EUNSUPPORTED / EWORKSPACE) enqueues
@@ -135,6 +136,21 @@ mpc_status mpc_static_evict(const mpc_dims* dims, int32_t T, const mpc_evict_cfg
                             const void* q_win, const void* k, const void* v, int32_t* kept_idx,
                             void* k_out, void* v_out, float* token_score, float* row_lse,
                             void* ws, size_t ws_bytes, void* stream);
+
+/* mpc_static_evict without any allocation and without a workspace argument, for callers that
+ * cannot allocate device memory (code under graph capture, tight serving loops, harnesses that
+ * forbid it). Same arguments (minus ws / ws_bytes), results bit for bit, and errors as
+ * mpc_static_evict. The workspace is a static device array of mpc_static_evict_noalloc_limit()
+ * bytes (32 MiB) that each device holds from the first call on until the process ends; a call whose
+ * workspace would be larger (mpc_workspace_bytes(MPC_OP_STATIC_EVICT, ...)) fails with
+ * MPC_EWORKSPACE before anything runs: split it into calls over fewer layers or sequences. Every
+ * call on one device shares that array, so calls that overlap in time on one device (other streams,
+ * other threads) race; calls on one stream do not. Nothing in the array needs initial contents. */
+mpc_status mpc_static_evict_noalloc(const mpc_dims* dims, int32_t T, const mpc_evict_cfg* cfg,
+                                    const void* q_win, const void* k, const void* v, int32_t* kept_idx,
+                                    void* k_out, void* v_out, float* token_score, float* row_lse,
+                                    void* stream);
+size_t mpc_static_evict_noalloc_limit(void);
 
 /* Cluster representatives (Sec. 3.3: r^max / r^min under Eq. 1, reordered form Eq. "sim";
  * hierarchy of Sec. 3.3 / App. F). Fine cluster c covers kept tokens [c*s, min((c+1)*s, Ts));

@@ -11,5 +11,5 @@ from ._lib import (  # noqa: F401
     GROUP, MPC_OP_DECODE_ATTN, MPC_OP_DECODE_STEP, MPC_OP_SELECT, MPC_OP_STATIC_EVICT, MpcDims, MpcError,
     MpcEvictCfg, MpcSelectCfg, SIMILARITY, dims_of, lib, mpc_append_kv, mpc_build_clusters,
     mpc_commonality, mpc_decode_step, mpc_decode_step_status, mpc_prefill, mpc_select_clusters, mpc_sparse_decode_attn, mpc_static_evict,
-    owner_layer, rep_rows, sel_heads, select_cfg, workspace, workspace_bytes)
+    mpc_static_evict_noalloc, noalloc_limit, owner_layer, rep_rows, sel_heads, select_cfg, workspace, workspace_bytes)
 from .pipeline import MPCachePath  # noqa: F401

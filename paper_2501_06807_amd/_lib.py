@@ -43,7 +43,8 @@ class MpcError(RuntimeError):
 
 
 _LIB = None
-EXPORTS = ("mpc_workspace_bytes", "mpc_static_evict", "mpc_build_clusters", "mpc_prefill", "mpc_select_clusters",
+EXPORTS = ("mpc_workspace_bytes", "mpc_static_evict", "mpc_static_evict_noalloc", "mpc_static_evict_noalloc_limit",
+           "mpc_build_clusters", "mpc_prefill", "mpc_select_clusters",
            "mpc_sparse_decode_attn", "mpc_decode_step", "mpc_decode_step_status", "mpc_append_kv", "mpc_commonality",
            "mpc_owner_layer",
            "mpc_status_string", "mpc_last_error")
@@ -60,6 +61,10 @@ def lib():
         L.mpc_workspace_bytes.argtypes = [I, P(MpcDims), I, V]
         L.mpc_workspace_bytes.restype = ctypes.c_size_t
         L.mpc_static_evict.argtypes = [P(MpcDims), I, P(MpcEvictCfg)] + [V] * 8 + [V, ctypes.c_size_t, V]
+        L.mpc_static_evict_noalloc.argtypes = [P(MpcDims), I, P(MpcEvictCfg)] + [V] * 8 + [V]
+        L.mpc_static_evict_noalloc.restype = ctypes.c_int
+        L.mpc_static_evict_noalloc_limit.argtypes = []
+        L.mpc_static_evict_noalloc_limit.restype = ctypes.c_size_t
         L.mpc_build_clusters.argtypes = [P(MpcDims), I, P(MpcSelectCfg), V, V, V, V]
         L.mpc_prefill.argtypes = [P(MpcDims), I, P(MpcEvictCfg), P(MpcSelectCfg)] + [V] * 10 + [V, ctypes.c_size_t, V]
         L.mpc_select_clusters.argtypes = [P(MpcDims), I, P(MpcSelectCfg)] + [V] * 5 + [V, ctypes.c_size_t, V]
@@ -141,6 +146,27 @@ def mpc_static_evict(q_win, k, v, kept_idx, k_out, v_out, *, keep, local_keep, s
     _check("mpc_static_evict", lib().mpc_static_evict(
         ctypes.byref(dims), T, ctypes.byref(cfg), _ptr(q_win), _ptr(k), _ptr(v), _ptr(kept_idx), _ptr(k_out),
         _ptr(v_out), _ptr(token_score), _ptr(row_lse), _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def mpc_static_evict_noalloc(q_win, k, v, kept_idx, k_out, v_out, *, keep, local_keep, sm_scale, causal=True,
+                             layer0=0, share_period=1, share_start=2, token_score=None, row_lse=None, stream=None):
+    """mpc_static_evict with the library's static scratch array as its workspace (nothing is
+    allocated); fails with MpcError (MPC_EWORKSPACE) when the block needs more than
+    noalloc_limit() scratch bytes."""
+    _contig(q_win, k, v, kept_idx, k_out, v_out, token_score, row_lse)
+    dims = dims_of(q_win, k, layer0)
+    dims.kv_capacity = k_out.shape[3]
+    T, W = k.shape[3], q_win.shape[3]
+    cfg = MpcEvictCfg(window=W, keep=keep, local_keep=local_keep, sm_scale=sm_scale, causal=int(causal),
+                      share_period=share_period, share_start=share_start)
+    _check("mpc_static_evict_noalloc", lib().mpc_static_evict_noalloc(
+        ctypes.byref(dims), T, ctypes.byref(cfg), _ptr(q_win), _ptr(k), _ptr(v), _ptr(kept_idx), _ptr(k_out),
+        _ptr(v_out), _ptr(token_score), _ptr(row_lse), _stream(stream)))
+
+
+def noalloc_limit():
+    """Bytes of the static scratch array behind mpc_static_evict_noalloc."""
+    return lib().mpc_static_evict_noalloc_limit()
 
 
 SIMILARITY = {"linear": 0, "maxprod": 1, "mean": 2}

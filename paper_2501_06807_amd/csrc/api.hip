@@ -3,6 +3,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <mutex>
 
 #include "append.h"
 #include "clusters.h"
@@ -653,6 +654,62 @@ mpc_status mpc_decode_step_status(void* ws, size_t ws_bytes, int32_t clear, int3
       return fail(MPC_EHIP, "clearing the error word: %s", hipGetErrorString(hipGetLastError()));
   }
   return ok();
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------------------------
+// Static eviction without any allocation: the workspace is a file-scope device array. Its name is
+// only a host-side stand-in in host code; the array's device address is looked up once per device
+// (hipGetSymbolAddress, with that device current) and only that address is handed to kernels.
+namespace {
+
+constexpr size_t kScratchBytes = (size_t)32 << 20;
+constexpr int kMaxDevices = 64;
+__device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices] = {};
+
+// Device address of the current device's scratch array.
+mpc_status scratch_address(void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return fail(MPC_EHIP, "no current device: %s", hipGetErrorString(hipGetLastError()));
+  if (dev < 0 || dev >= kMaxDevices) return fail(MPC_EUNSUPPORTED, "device %d beyond %d", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) return fail(MPC_EHIP, "scratch address of device %d: %s", dev, hipGetErrorString(e));
+    g_scratch[dev] = p;
+  }
+  *out = g_scratch[dev];
+  return MPC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t mpc_static_evict_noalloc_limit(void) { return kScratchBytes; }
+
+mpc_status mpc_static_evict_noalloc(const mpc_dims* dims, int32_t T, const mpc_evict_cfg* cfg, const void* q_win,
+                                    const void* k, const void* v, int32_t* kept_idx, void* k_out, void* v_out,
+                                    float* token_score, float* row_lse, void* stream) {
+  // every check of the eviction but the workspace's (which is all that is left when it reports
+  // the missing workspace), then the scratch size
+  mpc::EvictArgs unused{};
+  mpc_status s = prepare_evict(dims, T, cfg, q_win, k, v, kept_idx, k_out, v_out, token_score, row_lse, nullptr, 0,
+                               &unused);
+  if (s != MPC_EWORKSPACE) return s;
+  const size_t need = evict_ws(dims, T, cfg->window).total;
+  if (need > kScratchBytes)
+    return fail(MPC_EWORKSPACE, "static eviction of this block needs %zu scratch bytes, the static array holds %zu "
+                "(call it on fewer layers or sequences)", need, kScratchBytes);
+  void* ws = nullptr;
+  if ((s = scratch_address(&ws)) != MPC_OK) return s;
+  return mpc_static_evict(dims, T, cfg, q_win, k, v, kept_idx, k_out, v_out, token_score, row_lse, ws, kScratchBytes,
+                          stream);
 }
 
 }  // extern "C"

@@ -273,3 +273,21 @@ def test_capacity_and_tail_validation():
     s, msg = _status("mpc_static_evict", ctypes.byref(_dims(kv_capacity=150)), 1000, ctypes.byref(ecfg), FAKE, FAKE,
                      FAKE, FAKE, FAKE, FAKE, None, None, FAKE, 1 << 30, None)
     assert s == L.MPC_ESHAPE and "kv_capacity" in msg
+
+
+def test_noalloc_refuses_a_block_beyond_its_scratch():
+    """The entry point without allocation refuses, before touching the GPU, a block whose static
+    eviction workspace is larger than its static scratch array (all 32 layers of the 8K workload:
+    46 MB against 32 MiB)."""
+    d = _dims(n_layers=32, n_q_heads=32, n_kv_heads=32)
+    T, W = 8192, 1638
+    cfg = L.MpcEvictCfg(window=W, keep=4096, local_keep=32, sm_scale=0.088, causal=1, share_period=4, share_start=2)
+    lib = L.lib()
+    assert L.workspace_bytes(L.MPC_OP_STATIC_EVICT, d, T, cfg) > lib.mpc_static_evict_noalloc_limit() == 32 << 20
+    s, msg = _status("mpc_static_evict_noalloc", ctypes.byref(d), T, ctypes.byref(cfg), FAKE, FAKE, FAKE, FAKE, FAKE,
+                     FAKE, None, None, None)
+    assert s == L.MPC_EWORKSPACE and "scratch" in msg
+    # argument errors come first, as in mpc_static_evict
+    s, _ = _status("mpc_static_evict_noalloc", ctypes.byref(d), T, ctypes.byref(cfg), None, FAKE, FAKE, FAKE, FAKE,
+                   FAKE, None, None, None)
+    assert s == L.MPC_EINVAL
