@@ -17,7 +17,9 @@ DTYPE_CODE = {"fp32": 0, "fp16": 1, "bf16": 2}
 def lib():
     global _LIB
     if _LIB is None:
-        path = os.path.join(HERE, "liboracle.so")
+        # MPC_SANITIZE=1: the AddressSanitizer / UBSan build (tests/sanitize.sh)
+        san = os.environ.get("MPC_SANITIZE") == "1"
+        path = os.path.join(HERE, "liboracle_san.so" if san else "liboracle.so")
         if not os.path.exists(path):
             raise RuntimeError(f"{path} is not built; run __graft_entry__.build()")
         L = ctypes.CDLL(path)

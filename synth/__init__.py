@@ -45,7 +45,9 @@ class SynthSpec(ctypes.Structure):
 def lib():
     global _LIB
     if _LIB is None:
-        path = os.path.join(HERE, "libsynth.so")
+        # MPC_SANITIZE=1: the AddressSanitizer / UBSan build (tests/sanitize.sh)
+        san = os.environ.get("MPC_SANITIZE") == "1"
+        path = os.path.join(HERE, "libsynth_san.so" if san else "libsynth.so")
         if not os.path.exists(path):
             raise RuntimeError(f"{path} is not built; run __graft_entry__.build()")
         L = ctypes.CDLL(path)

@@ -13,15 +13,25 @@ FLAGS = [
 ]
 
 
-def build(verbose=False):
+SAN_LIB = os.path.join(HERE, "libsynth_san.so")
+# host code only: each sanitizer flag applies to the host compilation (device code is unchanged)
+SAN_FLAGS = ["-O1", "-g", "-Xarch_host", "-fsanitize=address,undefined", "-Xarch_host", "-fno-omit-frame-pointer",
+             "-shared-libsan"]
+
+
+def build(verbose=False, sanitize=False):
+    """sanitize: a separate libsynth_san.so whose host code carries AddressSanitizer and
+    UndefinedBehaviorSanitizer, loaded instead of libsynth.so when MPC_SANITIZE=1."""
     src = os.path.join(HERE, "synth.hip")
-    cmd = ["hipcc", *FLAGS, src, "-o", LIB + ".tmp"]
+    out = SAN_LIB if sanitize else LIB
+    cmd = ["hipcc", *FLAGS, *(SAN_FLAGS if sanitize else []), src, "-o", out + ".tmp"]
     if verbose:
         print(" ".join(cmd))
     subprocess.run(cmd, check=True, stderr=None if verbose else subprocess.DEVNULL)
-    os.replace(LIB + ".tmp", LIB)
-    return LIB
+    os.replace(out + ".tmp", out)
+    return out
 
 
 if __name__ == "__main__":
-    print(build(verbose=True))
+    import sys
+    print(build(verbose=True, sanitize="--sanitize" in sys.argv))
