@@ -18,8 +18,9 @@
 //     is its own rounding and that of c, both proportional to |c * (s - m)|: smallest on the
 //     terms that carry the sums.
 // The top-k is a 4-pass, 8-bit LDS radix select on the fp32 score bits followed by an ordered
-// block compaction; the gather copies kept rows with 16-byte lanes (all layers, or those whose
-// representatives are not built in the same pass).
+// block compaction, each thread's run of scores held in registers up to 32K older tokens; the
+// gather copies kept rows with 16-byte lanes (all layers, or those whose representatives are not
+// built in the same pass).
 #include "evict.h"
 
 namespace mpc {
@@ -357,6 +358,36 @@ __device__ int block_excl_scan(int v, int* wsum) {
 
 constexpr int kTopkThreads = 1024;
 
+// The radix digit (bins in descending order) at which the running count of tot[] reaches rem, by
+// the 64 lanes of wave 0 (four bins each, a wave prefix sum): writes prefix | digit << shift to
+// *s_prefix and rem minus the count of the higher bins to *s_rem. Requires sum(tot) >= rem >= 1.
+__device__ __forceinline__ void pick_digit(const uint32_t* tot, int rem, uint32_t prefix, int shift,
+                                           uint32_t* s_prefix, int* s_rem) {
+  const int lane = threadIdx.x & 63;
+  uint32_t c[4], sum = 0;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    c[u] = tot[255 - 4 * lane - u];
+    sum += c[u];
+  }
+  uint32_t x = sum;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t y = __shfl_up(x, o);
+    if (lane >= o) x += y;
+  }
+  uint32_t cum = x - sum;  // count of the bins above this lane's first
+  const uint32_t r = (uint32_t)rem;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    if (cum < r && r <= cum + c[u]) {
+      *s_prefix = prefix | ((uint32_t)(255 - 4 * lane - u) << shift);
+      *s_rem = (int)(r - cum);
+    }
+    cum += c[u];
+  }
+}
+
 __global__ __launch_bounds__(kTopkThreads) void k_topk(EvictArgs a) {
   __shared__ uint32_t hist[kTopkThreads / 64][256];
   __shared__ uint32_t tot[256];
@@ -391,16 +422,7 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(EvictArgs a) {
         tot[tid] = s;
       }
       __syncthreads();
-      if (tid == 0) {
-        uint32_t cum = 0;
-        int d = 255;
-        for (; d > 0; --d) {
-          if (cum + tot[d] >= (uint32_t)rem) break;
-          cum += tot[d];
-        }
-        s_prefix = prefix | ((uint32_t)d << shift);
-        s_rem = rem - (int)cum;
-      }
+      if (tid < 64) pick_digit(tot, rem, prefix, shift, &s_prefix, &s_rem);
       __syncthreads();
       prefix = s_prefix;
       rem = s_rem;
@@ -428,6 +450,94 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(EvictArgs a) {
       if (u > prefix || (u == prefix && taken < take)) {
         taken += u == prefix;
         out[off++] = j;
+      }
+    }
+  }
+  for (int i = tid; i < loc; i += kTopkThreads) out[n_sel + i] = n_old + i;
+}
+
+// The same selection with each thread's run of KPT scores held in registers from one read on:
+// the radix passes and the compaction read registers, not the score buffer (which otherwise is
+// re-read from memory by every pass once the heads in flight outgrow the L2).
+template <int KPT>
+__global__ __launch_bounds__(kTopkThreads) void k_topk_reg(EvictArgs a) {
+  __shared__ uint32_t hist[kTopkThreads / 64][256];
+  __shared__ uint32_t tot[256];
+  __shared__ uint32_t s_prefix;
+  __shared__ int s_rem;
+  __shared__ int wsum[16];
+
+  const int ou = blockIdx.x;  // (owner index * B + b) * Hkv + h
+  const int l = a.own.l[ou / (a.B * a.Hkv)];
+  const size_t unit = (size_t)l * a.B * a.Hkv + ou % (a.B * a.Hkv);
+  const int tid = threadIdx.x, w = tid >> 6;
+  const int loc = min(a.local_keep, a.keep);
+  const int n_old = a.T - loc, n_sel = a.keep - loc;
+  const uint32_t* key = (const uint32_t*)(a.score + (size_t)unit * a.T);
+  int32_t* out = a.kept + (size_t)unit * a.keep;
+
+  // this thread's run [j0, j0 + nv) of the older tokens' scores
+  const int j0 = tid * KPT;
+  const int nv = max(0, min(KPT, n_old - j0));
+  uint32_t kv[KPT];
+  if (nv == KPT && (((uintptr_t)(key + j0)) & 15) == 0) {
+#pragma unroll
+    for (int i = 0; i < KPT; i += 4) {
+      const uint4 v = *(const uint4*)(key + j0 + i);
+      kv[i] = v.x;
+      kv[i + 1] = v.y;
+      kv[i + 2] = v.z;
+      kv[i + 3] = v.w;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) kv[i] = i < nv ? key[j0 + i] : 0u;
+  }
+
+  // radix select: the n_sel-th largest key (non-negative floats order like their bits)
+  uint32_t prefix = 0, mask = 0;
+  int rem = n_sel;
+  if (n_sel > 0) {
+    for (int shift = 24; shift >= 0; shift -= 8) {
+      for (int i = tid; i < (kTopkThreads / 64) * 256; i += kTopkThreads) hist[i / 256][i % 256] = 0;
+      __syncthreads();
+#pragma unroll
+      for (int i = 0; i < KPT; ++i)
+        if (i < nv && (kv[i] & mask) == prefix) atomicAdd(&hist[w][(kv[i] >> shift) & 255u], 1u);
+      __syncthreads();
+      if (tid < 256) {
+        uint32_t s = 0;
+        for (int i = 0; i < kTopkThreads / 64; ++i) s += hist[i][tid];
+        tot[tid] = s;
+      }
+      __syncthreads();
+      if (tid < 64) pick_digit(tot, rem, prefix, shift, &s_prefix, &s_rem);
+      __syncthreads();
+      prefix = s_prefix;
+      rem = s_rem;
+      mask |= 255u << shift;
+      __syncthreads();
+    }
+  }
+  // ordered compaction: keys above the threshold, then the lowest-index ties up to `rem`
+  int gt = 0, eq = 0;
+  if (n_sel > 0) {
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+      gt += i < nv && kv[i] > prefix;
+      eq += i < nv && kv[i] == prefix;
+    }
+  }
+  const int eq_before = block_excl_scan(eq, wsum);
+  const int take = n_sel > 0 ? max(0, min(eq, rem - eq_before)) : 0;
+  int off = block_excl_scan(gt + take, wsum);
+  if (n_sel > 0) {
+    int taken = 0;
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+      if (i < nv && (kv[i] > prefix || (kv[i] == prefix && taken < take))) {
+        taken += kv[i] == prefix;
+        out[off++] = j0 + i;
       }
     }
   }
@@ -499,7 +609,19 @@ hipError_t launch_colsum(const EvictArgs& a, int dtype, int D, hipStream_t st) {
 }
 
 hipError_t launch_topk(const EvictArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL(k_topk, dim3(a.own.n * a.B * a.Hkv), dim3(kTopkThreads), 0, st, a);
+  // a run of up to 32 scores per thread stays in registers; longer prompts stream the scores
+  const dim3 grid(a.own.n * a.B * a.Hkv), block(kTopkThreads);
+  const int n_old = a.T - min(a.local_keep, a.keep);
+  if (n_old <= 4 * kTopkThreads)
+    hipLaunchKernelGGL(k_topk_reg<4>, grid, block, 0, st, a);
+  else if (n_old <= 8 * kTopkThreads)
+    hipLaunchKernelGGL(k_topk_reg<8>, grid, block, 0, st, a);
+  else if (n_old <= 16 * kTopkThreads)
+    hipLaunchKernelGGL(k_topk_reg<16>, grid, block, 0, st, a);
+  else if (n_old <= 32 * kTopkThreads)
+    hipLaunchKernelGGL(k_topk_reg<32>, grid, block, 0, st, a);
+  else
+    hipLaunchKernelGGL(k_topk, grid, block, 0, st, a);
   return hipGetLastError();
 }
 
