@@ -45,9 +45,10 @@ def parse():
     p.add_argument("--group", choices=("sum", "max", "head"), default="sum",
                    help="grouped q-heads: one selection per kv head scored by the sum (default) or the maximum of "
                         "its q-heads' similarities, or one selection per q-head")
-    p.add_argument("--extra", default="C3,C5",
+    p.add_argument("--extra", default="C3,C5,C5-T",
                    help="comma-separated workloads whose decode step is also measured (same pass structure, "
-                        "reported under other_workloads); '' for none")
+                        "reported under other_workloads; C5-T: the level-2 budget read against the prompt); "
+                        "'' for none")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--copy-calibration", action="store_true",
                    help="accepted for recorded profiling commands; the 1 GiB reference copy always runs")
