@@ -671,15 +671,22 @@ __device__ __align__(256) unsigned char scratch[kScratchBytes];
 std::mutex g_scratch_mu;
 void* g_scratch[kMaxDevices] = {};
 
-// Device address of the current device's scratch array.
-mpc_status scratch_address(void** out) {
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return fail(MPC_EHIP, "no current device: %s", hipGetErrorString(hipGetLastError()));
+// Device address of the scratch array on the device the stream belongs to (the current device for
+// the null stream); looked up once per device, with that device current.
+mpc_status scratch_address(hipStream_t stream, void** out) {
+  int cur = 0, dev = 0;
+  if (hipGetDevice(&cur) != hipSuccess) return fail(MPC_EHIP, "no current device: %s", hipGetErrorString(hipGetLastError()));
+  dev = cur;
+  if (stream && hipStreamGetDevice(stream, &dev) != hipSuccess)
+    return fail(MPC_EHIP, "device of the stream: %s", hipGetErrorString(hipGetLastError()));
   if (dev < 0 || dev >= kMaxDevices) return fail(MPC_EUNSUPPORTED, "device %d beyond %d", dev, kMaxDevices);
   std::lock_guard<std::mutex> lock(g_scratch_mu);
   if (!g_scratch[dev]) {
+    if (dev != cur && hipSetDevice(dev) != hipSuccess)
+      return fail(MPC_EHIP, "selecting device %d: %s", dev, hipGetErrorString(hipGetLastError()));
     void* p = nullptr;
     const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (dev != cur) (void)hipSetDevice(cur);
     if (e != hipSuccess || !p) return fail(MPC_EHIP, "scratch address of device %d: %s", dev, hipGetErrorString(e));
     g_scratch[dev] = p;
   }
@@ -707,7 +714,7 @@ mpc_status mpc_static_evict_noalloc(const mpc_dims* dims, int32_t T, const mpc_e
     return fail(MPC_EWORKSPACE, "static eviction of this block needs %zu scratch bytes, the static array holds %zu "
                 "(call it on fewer layers or sequences)", need, kScratchBytes);
   void* ws = nullptr;
-  if ((s = scratch_address(&ws)) != MPC_OK) return s;
+  if ((s = scratch_address((hipStream_t)stream, &ws)) != MPC_OK) return s;
   return mpc_static_evict(dims, T, cfg, q_win, k, v, kept_idx, k_out, v_out, token_score, row_lse, ws, kScratchBytes,
                           stream);
 }

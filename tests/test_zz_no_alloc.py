@@ -25,7 +25,7 @@ def _inputs(w):
     return bits_to_torch(np.stack(qs), dt), bits_to_torch(np.stack(ks), dt), bits_to_torch(np.stack(vs), dt)
 
 
-def _evict(M, w, q_win, k, v, noalloc):
+def _evict(M, w, q_win, k, v, noalloc, stream=None):
     L, B, Hkv, T, d = k.shape
     kept = torch.full((L, B, Hkv, w.keep), -1, dtype=torch.int32, device="cuda")
     k_out = torch.zeros((L, B, Hkv, w.keep, d), dtype=k.dtype, device="cuda")
@@ -35,7 +35,9 @@ def _evict(M, w, q_win, k, v, noalloc):
     kw = dict(keep=w.keep, local_keep=w.local_keep, sm_scale=1.0 / math.sqrt(d), share_period=w.share_period,
               share_start=w.share_start, token_score=score, row_lse=lse)
     if noalloc:
-        M.mpc_static_evict_noalloc(q_win, k, v, kept, k_out, v_out, **kw)
+        if stream is not None:  # the outputs' fills above ran on the current stream
+            stream.wait_stream(torch.cuda.current_stream())
+        M.mpc_static_evict_noalloc(q_win, k, v, kept, k_out, v_out, stream=stream, **kw)
     else:
         M.mpc_static_evict(q_win, k, v, kept, k_out, v_out, **kw)
     torch.cuda.synchronize()
@@ -55,7 +57,10 @@ def test_noalloc_static_evict_matches_the_workspace_call_twice():
     # first call: 8K prompt, four layers of 8 kv heads with sharing; second: a smaller GQA block
     first = synth.get("C3").with_(n_layers=4, n_q_heads=8, n_kv_heads=8)
     second = synth.get("C2").with_(n_layers=3)
-    for w in (first, second):
+    # the second call runs on a stream of its own (default priority): the scratch address is that
+    # of the stream's device
+    side = torch.cuda.Stream()
+    for w, stream in ((first, None), (second, side)):
         q_win, k, v = _inputs(w)
         dims = M.dims_of(q_win, k)
         cfg = M.MpcEvictCfg(window=w.window, keep=w.keep, local_keep=w.local_keep, sm_scale=1.0, causal=1,
@@ -64,7 +69,7 @@ def test_noalloc_static_evict_matches_the_workspace_call_twice():
         say(f"[noalloc] {w.name} L={w.n_layers}: workspace {need} of {limit} scratch bytes")
         assert 0 < need <= limit
         ref = _evict(M, w, q_win, k, v, noalloc=False)
-        got = _evict(M, w, q_win, k, v, noalloc=True)
+        got = _evict(M, w, q_win, k, v, noalloc=True, stream=stream)
         assert _same(ref, got), f"{w.name}: the no-allocation call differs from the workspace call"
         assert (got[0] >= 0).all()
 
