@@ -323,7 +323,7 @@ mpc_status mpc_prefill(const mpc_dims* dims, int32_t T, const mpc_evict_cfg* ecf
   mpc::BuildArgs b;
   if ((s = prepare_build(dims, ecfg->keep, scfg, k_out, cent, scent, &b)) != MPC_OK) return s;
   // the selection's owner layers gather their rows inside the build; the gather takes the rest
-  for (int i = 0; i < b.own.n; ++i) a.skip[b.own.l[i] >> 6] |= 1ull << (b.own.l[i] & 63);
+  for (int i = 0; i < b.own.n; ++i) a.skip[b.own.local(i) >> 6] |= 1ull << (b.own.local(i) & 63);
   b.g.kept = kept_idx;
   b.g.k_src = k;
   b.g.v_src = v;
@@ -531,8 +531,9 @@ mpc_status mpc_decode_step(const mpc_dims* dims, int32_t Ts, int32_t n_tail, con
   const bool per_q_head = sa.Hsel != dims->n_kv_heads;
   hipStream_t st = (hipStream_t)stream;
   clear_stale_error();
-  const mpc::FusedPlan fp = mpc::fused_plan(sa, dims->head_dim);
-  if (per_q_head || plan.splits > 1 || !mpc::fused_fits(fp, dims->head_dim, G)) {  // two kernels in sequence
+  const mpc::FusedPlan fp = mpc::fused_plan(sa, dims->head_dim, plan.splits);
+  if ((!fp.self && (per_q_head || plan.splits > 1)) || !mpc::fused_fits(fp, dims->head_dim, G)) {
+    // two kernels in sequence
     da.part = (float*)((char*)ws + lay.part);
     da.cnt = (int*)((char*)ws + lay.part + decode_ws(dims, per_q_head).cnt);
     if (sa.own.n > 0 &&

@@ -30,7 +30,7 @@ __global__ __launch_bounds__(NW* kWave) void k_build(BuildArgs a) {
 
   const int sup = a.sup0 + blockIdx.x % a.n_sup;
   const int ou = blockIdx.x / a.n_sup;  // (owner index * B + b) * Hkv + h
-  const int l = a.own.l[ou / (a.B * a.Hkv)];
+  const int l = a.own.local(ou / (a.B * a.Hkv));
   const size_t unit = (size_t)l * a.B * a.Hkv + ou % (a.B * a.Hkv);
   const int tid = threadIdx.x, lane = tid % kWave, w = tid / kWave;
   const int rg = lane / LPR, li = lane % LPR;

@@ -173,16 +173,51 @@ __host__ __device__ __forceinline__ int owner_layer(int l, int period, int start
 
 constexpr int kMaxLayers = 256;  // layers per call
 
-// Local indices of the owner layers of a block of layers, so that grids cover owner work only.
+// The owner layers of a block of layers [layer0, layer0 + n_layers), so that grids cover owner work
+// only: every layer below `start` (or every layer when period <= 1), then start + period * j for
+// j >= j0. Closed forms of a few scalars: a kernel indexing a table held in its arguments would pay
+// a dependent memory round trip per lookup.
 struct OwnerTable {
-  int n;
-  int16_t l[kMaxLayers];
+  int n;        // owner layers in the block
+  int layer0, n_layers, period, start;
+  int n_pre;    // owners below `start` (each its own owner): local layers [0, n_pre)
+  int j0;       // first shared owner: absolute layer start + period * j0
+
+  // local layer of owner o (0 <= o < n)
+  __host__ __device__ int local(int o) const {
+    return o < n_pre ? o : start + period * (j0 + o - n_pre) - layer0;
+  }
+  // owner index of local layer l, or -1 when its owner precedes the block
+  __host__ __device__ int index_of(int l) const {
+    const int abs = layer0 + l;
+    if (period <= 1 || abs < start) return l;
+    const int j = (abs - start) / period;
+    return start + period * j < layer0 ? -1 : n_pre + j - j0;
+  }
+  // end (exclusive local layer) of the layers that share owner o's selection
+  __host__ __device__ int end(int o) const {
+    if (o < n_pre) return o + 1;
+    const int e = local(o) + period;
+    return e < n_layers ? e : n_layers;
+  }
 };
 
 inline OwnerTable owner_table(int layer0, int n_layers, int period, int start) {
   OwnerTable t{};
-  for (int l = 0; l < n_layers && l < kMaxLayers; ++l)
-    if (owner_layer(layer0 + l, period, start) == layer0 + l) t.l[t.n++] = (int16_t)l;
+  t.layer0 = layer0;
+  t.n_layers = n_layers;
+  t.period = period;
+  t.start = start;
+  if (period <= 1) {
+    t.n_pre = t.n = n_layers;
+    return t;
+  }
+  const int end = layer0 + n_layers, a0 = layer0 > start ? layer0 : start;
+  t.n_pre = (end < start ? end : start) - layer0;
+  if (t.n_pre < 0) t.n_pre = 0;
+  t.j0 = (a0 - start + period - 1) / period;
+  const int n_sh = end > start ? (end - start + period - 1) / period - t.j0 : 0;
+  t.n = t.n_pre + (n_sh > 0 ? n_sh : 0);
   return t;
 }
 

@@ -29,15 +29,17 @@ __device__ __forceinline__ size_t cache_offset(const DecodeArgs& a, int unit) {
 // (they contribute nothing), then the clusters C, C + 1, ... that hold the tail rows
 // [Ts, Ts + n_tail) (Ts is a multiple of s when there is a tail). Returns the list length.
 // COH_SEL: the selection was written by another workgroup of the same launch, so it is read with
-// device-coherent loads.
+// device-coherent loads. pick: if not null, the selection computed by this workgroup (LDS).
 template <int NW, bool COH_SEL>
-__device__ __forceinline__ int load_list(const DecodeArgs& a, int unit, int32_t* s_sel) {
+__device__ __forceinline__ int load_list(const DecodeArgs& a, int unit, int32_t* s_sel, const int32_t* pick) {
   const int n_list = a.k_sel + (a.n_tail + a.s - 1) / a.s;
   for (int i = threadIdx.x; i < n_list; i += NW * kWave) {
     int c = a.C + (i - a.k_sel);
     if (i < a.k_sel) {
       const int32_t* src = a.sel + (size_t)unit * a.k_sel + i;
-      if constexpr (COH_SEL)
+      if (pick)
+        c = pick[i];
+      else if constexpr (COH_SEL)
         c = __hip_atomic_load(src, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       else
         c = *src;
@@ -118,7 +120,7 @@ __device__ __forceinline__ void finish_unit(const DecodeArgs& a, int unit, int s
 // device-coherent loads (it was written by another workgroup of the same launch). The gathered V
 // rows are loaded with the non-temporal hint; the K rows too when STREAM_K.
 template <class DT, int D, int G, int NW, int U, bool COH_SEL, bool STREAM_K>
-__device__ __forceinline__ void attend_unit(const DecodeArgs& a, int unit, int split) {
+__device__ __forceinline__ void attend_unit(const DecodeArgs& a, int unit, int split, const int32_t* pick) {
   constexpr int EPL = DT::kVec;
   constexpr int LPR = D / EPL;
   constexpr int RPW = kWave / LPR;
@@ -150,7 +152,7 @@ __device__ __forceinline__ void attend_unit(const DecodeArgs& a, int unit, int s
     }
   }
   // the cluster list after the query loads, so that both are in flight together
-  const int n_list = load_list<NW, COH_SEL>(a, unit, s_sel);
+  const int n_list = load_list<NW, COH_SEL>(a, unit, s_sel, pick);
   __syncthreads();
 
   const int n_slot = n_list * a.s, rows_end = a.Ts + a.n_tail;
@@ -325,7 +327,7 @@ __device__ __forceinline__ float wave_max(float x) {
 }
 
 template <class DT, int D, int NW, bool COH_SEL, bool STREAM_K>
-__device__ __forceinline__ void attend_unit_g4(const DecodeArgs& a, int unit, int split) {
+__device__ __forceinline__ void attend_unit_g4(const DecodeArgs& a, int unit, int split, const int32_t* pick) {
   constexpr int G = 4;
   constexpr int EPL = 8;              // 16-bit elements per 16-byte vector
   constexpr int LPR = D / EPL;        // lanes per row (row layout)
@@ -350,7 +352,7 @@ __device__ __forceinline__ void attend_unit_g4(const DecodeArgs& a, int unit, in
   for (int kk = 0; kk < KK; ++kk)
     qa[kk] = ldg16((const char*)a.q + ((q_row0 + tk % G) * D + kk * 32 + kq * 8) * DT::kElt);
   // the cluster list after the query loads, so that both are in flight together
-  const int n_list = load_list<NW, COH_SEL>(a, unit, s_sel);
+  const int n_list = load_list<NW, COH_SEL>(a, unit, s_sel, pick);
   __syncthreads();
 
   const int n_slot = n_list * a.s, rows_end = a.Ts + a.n_tail;
@@ -472,13 +474,14 @@ __device__ __forceinline__ void attend_unit_g4(const DecodeArgs& a, int unit, in
 }
 
 // The attention path of a unit: matrix-core scores for four-head groups of 16-bit rows, the VALU
-// path otherwise.
+// path otherwise. pick: the unit's selection in LDS (computed by the same workgroup), or null to
+// read it from a.sel.
 template <class DT, int D, int G, int NW, int U, bool COH_SEL, bool STREAM_K>
-__device__ __forceinline__ void attend(const DecodeArgs& a, int unit, int split) {
+__device__ __forceinline__ void attend(const DecodeArgs& a, int unit, int split, const int32_t* pick = nullptr) {
   if constexpr (G == 4 && DT::kElt == 2)
-    attend_unit_g4<DT, D, NW, COH_SEL, STREAM_K>(a, unit, split);
+    attend_unit_g4<DT, D, NW, COH_SEL, STREAM_K>(a, unit, split, pick);
   else
-    attend_unit<DT, D, G, NW, U, COH_SEL, STREAM_K>(a, unit, split);
+    attend_unit<DT, D, G, NW, U, COH_SEL, STREAM_K>(a, unit, split, pick);
 }
 
 }  // namespace dev

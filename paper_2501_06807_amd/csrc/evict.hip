@@ -101,7 +101,7 @@ __global__ __launch_bounds__(kRowThreads) void k_rowstats(EvictArgs a) {
   const int id = xcd_remap(blockIdx.x, gridDim.x);
   const int rb = id % n_rb;
   const int ou = id / n_rb;  // (owner index * B + b) * Hq + hq
-  const int l = a.own.l[ou / (a.B * a.Hq)];
+  const int l = a.own.local(ou / (a.B * a.Hq));
   const int b = (ou / a.Hq) % a.B, hq = ou % a.Hq;
   const size_t qunit = ((size_t)l * a.B + b) * a.Hq + hq;
   const int G = a.Hq / a.Hkv;
@@ -222,7 +222,7 @@ __global__ __launch_bounds__(kColThreads) void k_colsum(EvictArgs a) {
   const int id = xcd_remap(blockIdx.x, gridDim.x);
   const int kb = id % n_kb;
   const int ou = id / n_kb;  // (owner index * B + b) * Hkv + h
-  const int l = a.own.l[ou / (a.B * a.Hkv)];
+  const int l = a.own.local(ou / (a.B * a.Hkv));
   const int b = (ou / a.Hkv) % a.B, h = ou % a.Hkv;
   const size_t kvunit = ((size_t)l * a.B + b) * a.Hkv + h;
   const int G = a.Hq / a.Hkv;
@@ -396,7 +396,7 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk(EvictArgs a) {
   __shared__ int wsum[16];
 
   const int ou = blockIdx.x;  // (owner index * B + b) * Hkv + h
-  const int l = a.own.l[ou / (a.B * a.Hkv)];
+  const int l = a.own.local(ou / (a.B * a.Hkv));
   const size_t unit = (size_t)l * a.B * a.Hkv + ou % (a.B * a.Hkv);
   const int tid = threadIdx.x, w = tid >> 6;
   const int loc = min(a.local_keep, a.keep);
@@ -468,7 +468,7 @@ __global__ __launch_bounds__(kTopkThreads) void k_topk_reg(EvictArgs a) {
   __shared__ int wsum[16];
 
   const int ou = blockIdx.x;  // (owner index * B + b) * Hkv + h
-  const int l = a.own.l[ou / (a.B * a.Hkv)];
+  const int l = a.own.local(ou / (a.B * a.Hkv));
   const size_t unit = (size_t)l * a.B * a.Hkv + ou % (a.B * a.Hkv);
   const int tid = threadIdx.x, w = tid >> 6;
   const int loc = min(a.local_keep, a.keep);

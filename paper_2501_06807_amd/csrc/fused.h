@@ -23,9 +23,11 @@ struct FusedArgs {
 struct FusedPlan {
   int units;
   size_t smem;
+  bool self;  // every workgroup selects for its own unit (no waits; no workspace words used)
 };
 
-FusedPlan fused_plan(const SelectArgs& s, int D);
+// splits: workgroups per attention unit of the block's attention plan.
+FusedPlan fused_plan(const SelectArgs& s, int D, int splits);
 // Whether the selection's LDS and the attention's fit one workgroup's LDS together.
 bool fused_fits(const FusedPlan& p, int D, int G);
 hipError_t launch_decode_step(const FusedArgs& f, const FusedPlan& p, int dtype, int D, int G,

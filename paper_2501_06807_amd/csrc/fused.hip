@@ -31,8 +31,8 @@ __global__ __launch_bounds__(kFusedWaves* kWave) void k_decode_step(FusedArgs f)
   const int BH = sa.B * sa.Hkv;
   const int unit = blockIdx.x;  // (l * B + b) * Hkv + h
   const int l = unit / BH;
-  int o = -1;  // owner index of layer l (none: owned before the block, its selection is an input)
-  for (int i = 0; i < sa.own.n && sa.own.l[i] <= l; ++i) o = i;
+  const int o = sa.own.index_of(l);  // owner index of layer l (-1: owned before the block, its
+                                     // selection is an input)
   const int head = o >= 0 ? o * BH + unit % BH : -1;  // (owner index * B + b) * Hkv + h
 
   if (tid == 0) {
@@ -81,7 +81,7 @@ __global__ __launch_bounds__(kFusedWaves* kWave) void k_decode_step(FusedArgs f)
     __syncthreads();
     if (tid == 0) {
       __builtin_amdgcn_s_waitcnt(0);  // the publication above has completed
-      const int lb = sa.own.l[o], le = o + 1 < sa.own.n ? sa.own.l[o + 1] : sa.n_layers;
+      const int lb = sa.own.local(o), le = sa.own.end(o);
       const int c = __hip_atomic_fetch_add(&f.cons[head], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       if (c == le - lb - 1) {  // last consumer of the head
         __hip_atomic_store(&f.state[head], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -91,8 +91,58 @@ __global__ __launch_bounds__(kFusedWaves* kWave) void k_decode_step(FusedArgs f)
   }
 }
 
+// Self-selecting form (blocks of at most one attention unit per compute unit, attention not split):
+// every workgroup computes the selection of its unit's owner head itself and attends over it from
+// LDS. Workgroups never wait for one another; the two to four units that share an owner head
+// compute the same selection side by side, reading its representatives through one L2.
+constexpr int kDies = 8;  // compute dies (XCDs); workgroup p of a launch runs on die p % kDies
+
+// Unit of workgroup p: ranks i of the owner-major order (all units of one owner head, then the next
+// head) are dealt to the dies in contiguous runs, so the units that select alike share a die's L2.
+// Returns -1 for the padding positions of the last run.
+__device__ __forceinline__ int self_unit(const SelectArgs& s, int p) {
+  const int BH = s.B * s.Hsel, n_units = s.n_layers * BH;
+  const int per = (n_units + kDies - 1) / kDies;
+  const int i = (p % kDies) * per + p / kDies;
+  if (i >= n_units) return -1;
+  // owner group of rank i: layers [lb, le) that share one selection (or, before the first owner
+  // of the block, layers whose selection is an input); a group's ranks are [lb * BH, le * BH), so it
+  // is the group of layer i / BH
+  const int o = s.own.index_of(i / BH);
+  const int lb = o >= 0 ? s.own.local(o) : 0;
+  const int le = o >= 0 ? s.own.end(o) : (s.own.n > 0 ? s.own.local(0) : s.n_layers);
+  const int il = i - lb * BH, n = le - lb;
+  return (lb + il % n) * BH + il / n;
+}
+
+template <class DT, int D, int G, bool MP, bool GMAX, bool STREAM_K>
+__global__ __launch_bounds__(kFusedWaves* kWave) void k_decode_self(FusedArgs f) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  __shared__ int32_t s_pick[dev::kMaxSel];
+  const SelectArgs& sa = f.s;
+  const int unit = self_unit(sa, blockIdx.x);  // (l * B + b) * Hsel + h
+  if (unit < 0) return;
+  const int BH = sa.B * sa.Hsel, l = unit / BH;
+  const int o = sa.own.index_of(l);  // -1: owned before the block, its selection is an input
+  if (o >= 0) {
+    dev::select_block<DT, D, kFusedWaves, false, 2, MP, true, GMAX>(sa, o * BH + unit % BH, smem, s_pick, l);
+    __syncthreads();
+  }
+  dev::attend<DT, D, G, kFusedWaves, 4, false, STREAM_K>(f.d, unit, 0, o >= 0 ? s_pick : nullptr);
+}
+
+template <class DT, int D, int G, bool MP, bool GMAX>
+void launch_self(const FusedArgs& f, size_t smem, hipStream_t st) {
+  const int units = f.s.n_layers * f.s.B * f.s.Hsel;
+  const dim3 grid((units + kDies - 1) / kDies * kDies), block(kFusedWaves * kWave);
+  if (f.d.stream_k)
+    hipLaunchKernelGGL((k_decode_self<DT, D, G, MP, GMAX, true>), grid, block, smem, st, f);
+  else
+    hipLaunchKernelGGL((k_decode_self<DT, D, G, MP, GMAX, false>), grid, block, smem, st, f);
+}
+
 template <class DT, int D, int G>
-hipError_t launch_g(const FusedArgs& f, size_t smem, hipStream_t st) {
+hipError_t launch_claim(const FusedArgs& f, size_t smem, hipStream_t st) {
   const dim3 grid(f.s.n_layers * f.s.B * f.s.Hkv), block(kFusedWaves * kWave);
   const bool mp = f.s.similarity == MPC_SIM_MAXPROD;
   if constexpr (G > 1) {
@@ -111,45 +161,65 @@ hipError_t launch_g(const FusedArgs& f, size_t smem, hipStream_t st) {
   return hipGetLastError();
 }
 
+template <class DT, int D, int G>
+hipError_t launch_g(const FusedArgs& f, const FusedPlan& p, hipStream_t st) {
+  const size_t smem = p.smem;
+  const bool mp = f.s.similarity == MPC_SIM_MAXPROD;
+  const bool gmax = G > 1 && f.s.group == MPC_GROUP_MAX;
+  if (p.self) {
+    if constexpr (G > 1) {
+      if (gmax) {
+        mp ? launch_self<DT, D, G, true, true>(f, smem, st) : launch_self<DT, D, G, false, true>(f, smem, st);
+        return hipGetLastError();
+      }
+    }
+    mp ? launch_self<DT, D, G, true, false>(f, smem, st) : launch_self<DT, D, G, false, false>(f, smem, st);
+    return hipGetLastError();
+  }
+  return launch_claim<DT, D, G>(f, smem, st);
+}
+
 template <class DT, int D>
-hipError_t launch_d(const FusedArgs& f, int G, size_t smem, hipStream_t st) {
+hipError_t launch_d(const FusedArgs& f, int G, const FusedPlan& p, hipStream_t st) {
   switch (G) {
-    case 1: return launch_g<DT, D, 1>(f, smem, st);
-    case 2: return launch_g<DT, D, 2>(f, smem, st);
-    case 4: return launch_g<DT, D, 4>(f, smem, st);
-    case 8: return launch_g<DT, D, 8>(f, smem, st);
+    case 1: return launch_g<DT, D, 1>(f, p, st);
+    case 2: return launch_g<DT, D, 2>(f, p, st);
+    case 4: return launch_g<DT, D, 4>(f, p, st);
+    case 8: return launch_g<DT, D, 8>(f, p, st);
   }
   return hipErrorInvalidValue;
 }
 
 template <class DT>
-hipError_t launch_dt(const FusedArgs& f, int D, int G, size_t smem, hipStream_t st) {
-  if (D == 64) return launch_d<DT, 64>(f, G, smem, st);
-  if (D == 128) return launch_d<DT, 128>(f, G, smem, st);
+hipError_t launch_dt(const FusedArgs& f, int D, int G, const FusedPlan& p, hipStream_t st) {
+  if (D == 64) return launch_d<DT, 64>(f, G, p, st);
+  if (D == 128) return launch_d<DT, 128>(f, G, p, st);
   return hipErrorInvalidValue;
 }
 
 }  // namespace
 
-FusedPlan fused_plan(const SelectArgs& s, int D) {
+FusedPlan fused_plan(const SelectArgs& s, int D, int splits) {
   FusedPlan p{};
-  p.units = s.n_layers * s.B * s.Hkv;
+  p.units = s.n_layers * s.B * s.Hsel;
   p.smem = dev::select_smem_bytes_dev(D, s.S, s.NC, select_query_rows(s));
+  p.self = p.units <= kNumCU && splits == 1;
   return p;
 }
 
 bool fused_fits(const FusedPlan& p, int D, int G) {
-  // the attention's static LDS: selection ids, per-wave (m, l) and partial outputs, a few words
-  const size_t att = 4 * dev::kMaxSel + (size_t)kFusedWaves * G * (2 + D) * 4 + 64;
+  // the attention's static LDS: selection ids, per-wave (m, l) and partial outputs, a few words;
+  // the self-selecting form holds its selection ids once more
+  const size_t att = 4 * dev::kMaxSel * (p.self ? 2 : 1) + (size_t)kFusedWaves * G * (2 + D) * 4 + 64;
   return p.smem + att <= kMaxLds;
 }
 
 hipError_t launch_decode_step(const FusedArgs& f, const FusedPlan& p, int dtype, int D, int G,
                               hipStream_t st) {
   switch (dtype) {
-    case MPC_FP32: return launch_dt<F32>(f, D, G, p.smem, st);
-    case MPC_FP16: return launch_dt<F16>(f, D, G, p.smem, st);
-    case MPC_BF16: return launch_dt<BF16>(f, D, G, p.smem, st);
+    case MPC_FP32: return launch_dt<F32>(f, D, G, p, st);
+    case MPC_FP16: return launch_dt<F16>(f, D, G, p, st);
+    case MPC_BF16: return launch_dt<BF16>(f, D, G, p, st);
   }
   return hipErrorInvalidValue;
 }

@@ -25,19 +25,24 @@ struct RowTile {
   bool valid[PASS];
 };
 
-template <int D, int PASS>
-__device__ __forceinline__ void tile_load(const float* M, const int* idx, int n, int r0, RowTile<D, PASS>& t) {
+template <int D, int PASS, class RowOf>
+__device__ __forceinline__ void tile_load_fn(const float* M, RowOf row_of, int n, int r0, RowTile<D, PASS>& t) {
   constexpr int ROWS = kWave / 4;
   const int lane = threadIdx.x % kWave, rq = lane >> 2, qk = lane & 3;
 #pragma unroll
   for (int p = 0; p < PASS; ++p) {
     const int r = r0 + p * ROWS + rq;
-    const int row = r < n ? (idx ? idx[r] : r) : -1;
+    const int row = r < n ? row_of(r) : -1;
     t.valid[p] = row >= 0;
     const float* src = M + (size_t)(t.valid[p] ? row : 0) * D + qk * 4;
 #pragma unroll
     for (int c = 0; c < D / 16; ++c) t.x[p][c] = *(const float4*)(src + c * 16);
   }
+}
+
+template <int D, int PASS>
+__device__ __forceinline__ void tile_load(const float* M, const int* idx, int n, int r0, RowTile<D, PASS>& t) {
+  tile_load_fn<D, PASS>(M, [idx](int r) { return idx ? idx[r] : r; }, n, r0, t);
 }
 
 __device__ __forceinline__ uint32_t key_hi(double x);
@@ -385,26 +390,254 @@ __device__ __forceinline__ void emit_selection(const SelectArgs& a, const int* t
   }
 }
 
-// LDS carve-up of the one-workgroup-per-head selection (host and device).
+// Writes the level-2 result of a workgroup that attends one layer itself: entry top[j] (j <
+// k_clusters) goes to its ascending position of `pick` (LDS, read by the same workgroup's attention)
+// and of layer l's row of the selection output (layer l uses the selection of its owner head, which
+// the workgroup computed). Threads t0, t0 + nt, ...
+__device__ __forceinline__ void emit_pick(const SelectArgs& a, const int* top, const int* cand, const double* s2,
+                                          int l, int b, int h, int32_t* pick, int t0, int nt) {
+  const size_t o0 = (((size_t)l * a.B + b) * a.Hsel + h) * a.k_clusters;
+  for (int j = t0; j < a.k_clusters; j += nt) {
+    const int i = top[j], p = ascending_pos(top, a.k_clusters, j);
+    const int c = cand[i];
+    pick[p] = c;
+    a.sel[o0 + p] = c;
+    if (a.sel_score) a.sel_score[o0 + p] = (float)s2[i];
+  }
+}
+
+// ---------------------------------------------------------------------------------------------
+// Register ranking of the workgroup-per-head selection, for up to 64 super-clusters and up to 512
+// candidates (fewer than 64 kept when there are more than 64): one entry per lane, ranks counted
+// against LDS broadcasts of the keys, selected sets as wave ballots, ascending output positions as
+// bit counts of a ballot below the lane. No per-thread list walks and, at level 1, no barrier: every
+// wave ranks the super-clusters itself and derives its own candidate rows from the ballot.
+__host__ __device__ inline bool register_ranking(int S, int NC, int k_clusters) {
+  return S <= kWave && (NC <= kWave || (NC <= 8 * kWave && k_clusters < kWave));
+}
+
+// Exact rank (score desc, index asc) of entry i among sc[0, n) (LDS): the boundary fallback when the
+// composite keys of ranks k-1 and k share their 32-bit score image.
+__device__ __forceinline__ int exact_rank(const double* sc, int n, int i) {
+  const double si = sc[i];
+  int c = 0;
+  for (int j = 0; j < n; ++j) {
+    const double x = sc[j];
+    c += (x > si) | ((x == si) & (j < i));
+  }
+  return c;
+}
+
+// Position of the n-th (from 0) set bit of m (n below its bit count).
+__device__ __forceinline__ int nth_set_bit(unsigned long long m, int n) {
+  int pos = 0;
+  uint32_t x = (uint32_t)m;
+  int c = __popc(x);
+  if (n >= c) {
+    n -= c;
+    pos = 32;
+    x = (uint32_t)(m >> 32);
+  }
+#pragma unroll
+  for (int w = 16; w >= 1; w >>= 1) {
+    c = __popc(x & ((1u << w) - 1u));
+    if (n >= c) {
+      n -= c;
+      pos += w;
+      x >>= w;
+    }
+  }
+  return pos;
+}
+
+// Output of one selected entry: cluster c with score sc at ascending position p, to the LDS pick
+// list and layer pick_layer's row (pick set), or to every layer of [l, l_end) of the call.
+template <bool COH>
+__device__ __forceinline__ void emit_entry(const SelectArgs& a, int c, float sc, int p, int l, int l_end, int b,
+                                           int h, int32_t* pick, int pick_layer) {
+  if (pick) {
+    pick[p] = c;
+    const size_t o = (((size_t)pick_layer * a.B + b) * a.Hsel + h) * a.k_clusters + p;
+    a.sel[o] = c;
+    if (a.sel_score) a.sel_score[o] = sc;
+    return;
+  }
+  const size_t stride = (size_t)a.B * a.Hsel * a.k_clusters;
+  const size_t o0 = (((size_t)l * a.B + b) * a.Hsel + h) * a.k_clusters + p;
+  for (int l2 = l; l2 < l_end; ++l2) {
+    store_sel<COH>(a.sel + o0 + (size_t)(l2 - l) * stride, c);
+    if (a.sel_score) a.sel_score[o0 + (size_t)(l2 - l) * stride] = sc;
+  }
+}
+
+// LDS carve-up of the one-workgroup-per-head selection (host and device). The key array is padded
+// to whole 64-entry slices and the tournament list to whole 16-key batches.
 struct BlockLds {
-  size_t qsum, s1, s2, ck, img1, img2, list_k, list_i, top, cand, total;
+  size_t qsum, s1, s2, ck, img1, img2, list_k, list_i, top, cand, part, total;
 };
 __host__ __device__ inline BlockLds block_lds(int D, int S, int NC, int qrows) {
   auto al = [](size_t x) { return (x + 15) & ~(size_t)15; };
   const int m = S > NC ? S : NC;
+  const int m64 = (m + 63) / 64 * 64;
   BlockLds o;
   o.qsum = 0;
   o.s1 = al(o.qsum + (size_t)qrows * D * 8);
   o.s2 = al(o.s1 + (size_t)S * 8);
   o.ck = al(o.s2 + (size_t)NC * 8);
-  o.img1 = al(o.ck + (size_t)m * 8);
+  o.img1 = al(o.ck + (size_t)(kWave + m64) * 8);  // level 1 (register ranking: 64 keys), then level 2
   o.img2 = al(o.img1 + (size_t)S * 4);
-  o.list_k = al(o.img2 + (size_t)NC * 4);  // a tournament list is at most half its set
-  o.list_i = al(o.list_k + (size_t)m * 8);
-  o.top = al(o.list_i + (size_t)m * 4);
-  o.cand = al(o.top + (size_t)m * 4);
-  o.total = al(o.cand + (size_t)NC * 4);
+  o.list_k = al(o.img2 + (size_t)NC * 4);
+  o.list_i = al(o.list_k + (size_t)(m64 + 16) * 8);
+  o.top = al(o.list_i + (size_t)(m64 + 16) * 4);
+  o.cand = al(o.top + (size_t)(m > kWave ? m : kWave) * 4);
+  o.part = al(o.cand + (size_t)NC * 4);  // partial counts: level 1, then level 2 (8 x 64 each)
+  o.total = al(o.part + (size_t)2 * 8 * kWave * 4);
   return o;
+}
+
+// Keys of keys[base, base + KPC) above `mine`, all read before the compares.
+template <int KPC>
+__device__ __forceinline__ int count_chunk(const unsigned long long* keys, int base, unsigned long long mine) {
+  unsigned long long v[KPC];
+#pragma unroll
+  for (int u = 0; u < KPC; ++u) v[u] = keys[base + u];
+  int c = 0;
+#pragma unroll
+  for (int u = 0; u < KPC; ++u) c += v[u] > mine;
+  return c;
+}
+
+// Partial ranks of the entries of n_slice 64-entry slices of `keys` (padded to whole slices): the
+// workgroup's waves take the items (slice, chunk) of cps chunks per slice (NW for one slice, else 1),
+// and item t writes, for the entry of its slice in each lane, the number of its chunk's keys above
+// that entry to part[t * 64 + lane]. Returns cps. The rank of entry `lane` of slice sl within its
+// slice is then the sum of part[(sl * cps + c) * 64 + lane] over c < cps (after a barrier).
+template <int NW>
+__device__ __forceinline__ int slice_partials(const unsigned long long* keys, int n_slice, int* part) {
+  const int w = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  // chunks only for a single slice: with several slices the extra barrier and partial reads cost
+  // more than the compares they save (measured)
+  const int cps = n_slice > 1 ? 1 : NW >= 8 ? 8 : NW >= 4 ? 4 : NW >= 2 ? 2 : 1;
+  const int kpc = kWave / cps;
+  for (int t = w; t < n_slice * cps; t += NW) {
+    const int sl = t / cps, base = sl * kWave + (t % cps) * kpc;
+    const unsigned long long mine = keys[sl * kWave + lane];
+    int c;
+    if (kpc == 8)
+      c = count_chunk<8>(keys, base, mine);
+    else if (kpc == 16)
+      c = count_chunk<16>(keys, base, mine);
+    else if (kpc == 32)
+      c = count_chunk<32>(keys, base, mine);
+    else
+      c = count_chunk<64>(keys, base, mine);
+    part[t * kWave + lane] = c;
+  }
+  return cps;
+}
+
+// Sum of the cps partial ranks of entry `lane` of slice sl.
+__device__ __forceinline__ int slice_rank(const int* part, int sl, int cps) {
+  const int lane = threadIdx.x % kWave;
+  int r = 0;
+  for (int c = 0; c < cps; ++c) r += part[(sl * cps + c) * kWave + lane];
+  return r;
+}
+
+// The rank of every lane's entry of a 64-entry slice is exact in (score desc, index asc) unless the
+// entries of ranks k-1 and k share a score image: then every lane takes its exact rank.
+__device__ __forceinline__ int exact_at_boundary(int r, const double* sc, const uint32_t* img, int n, int k) {
+  const int lane = threadIdx.x % kWave;
+  const unsigned long long ba = __ballot(r == k - 1), bb = __ballot(r == k);
+  if (ba && bb) {
+    const int la = __ffsll((long long)ba) - 1, lb = __ffsll((long long)bb) - 1;
+    if (la < n && lb < n && img[la] == img[lb]) r = lane < n ? exact_rank(sc, n, lane) : kWave;
+  }
+  return r;
+}
+
+// Continuation of select_block once the level-1 scores are written (register ranking): level-1
+// top-k_super as a ballot in every wave, level-2 rows derived from it, level-2 ranking by 64-entry
+// slices (each keeps its local top k_clusters + 1) and a count over the survivors, output by wave 0.
+// The ranks of a single 64-entry set are counted by all waves together (partial counts over key
+// chunks).
+template <class SC, int NW, bool COH>
+__device__ void select_block_reg(const SelectArgs& a, typename SC::Tile& tile, const typename SC::Query& qr,
+                                 const float* cent, const double* s1, double* s2, unsigned long long* ck,
+                                 const uint32_t* img1, uint32_t* img2, unsigned long long* list_k, int* list_i,
+                                 int* top, int* part, int* bnd2, int l, int b, int h, int32_t* pick,
+                                 int pick_layer) {
+  constexpr int NT = NW * kWave;
+  constexpr int TILE = NW * (kWave / 4) * SC::P;
+  const int tid = threadIdx.x, w = tid / kWave, lane = tid % kWave;
+  for (int j = a.S + tid; j < kWave; j += NT) ck[j] = rank_key(0u, j);  // padding below every score
+  __syncthreads();
+  const int cps1 = slice_partials<NW>(ck, 1, part);
+  __syncthreads();
+  const unsigned long long sup =
+      __ballot(exact_at_boundary(slice_rank(part, 0, cps1), s1, img1, a.S, a.k_super) < a.k_super);
+
+  // level 2: the member clusters of the selected super-clusters, in ascending order; their keys
+  // follow the level-1 keys and their partial counts the level-1 ones, which slower waves may still
+  // be reading
+  ck += kWave;
+  part += NW * kWave;
+  const int f = a.f, C = a.C, NC = a.NC, k = a.k_clusters;
+  const int fs = (f & (f - 1)) == 0 ? __builtin_ctz(f) : -1;  // shift when f is a power of two
+  auto cand = [=](int r) {
+    const int q = fs >= 0 ? r >> fs : r / f;
+    const int c = nth_set_bit(sup, q) * f + (r - q * f);
+    return c < C ? c : -1;
+  };
+  for (int r0 = w * (TILE / NW); r0 < NC; r0 += TILE) {
+    tile_load_fn<SC::RW, SC::P>(cent, cand, NC, r0, tile);
+    SC::dot(tile, NC, r0, qr, s2, img2, ck);
+  }
+  const int n64 = (NC + kWave - 1) / kWave * kWave, n_slice = n64 / kWave;
+  for (int j = NC + tid; j < n64; j += NT) ck[j] = rank_key(0u, j);
+  if (tid < 2) bnd2[tid] = -1;
+  const int l_end = a.own.end(a.own.index_of(l));  // layers [l, l_end) of the call use this selection
+  __syncthreads();
+
+  if (n_slice == 1) {  // one slice: its ranks are final; wave 0 writes the result
+    const int cps = slice_partials<NW>(ck, 1, part);
+    __syncthreads();
+    if (w == 0) {
+      const int r = exact_at_boundary(slice_rank(part, 0, cps), s2, img2, NC, k);
+      const unsigned long long chosen = __ballot(r < k);
+      if (r < k) {
+        const int p = __popcll(chosen & ((1ull << lane) - 1ull));
+        emit_entry<COH>(a, cand(lane), (float)s2[lane], p, l, l_end, b, h, pick, pick_layer);
+      }
+    }
+    return;
+  }
+  // each slice keeps its entries of local rank <= k
+  const int per = k + 1, m = n_slice * per, m16 = (m + 15) / 16 * 16;
+  for (int sl = w; sl < n_slice; sl += NW) {
+    const int e = sl * kWave + lane;
+    const int r = count_above(ck, sl * kWave, sl * kWave + kWave, ck[e]);
+    if (r <= k) {
+      list_k[sl * per + r] = ck[e];
+      list_i[sl * per + r] = e < NC ? e : -1;
+    }
+  }
+  for (int j = m + tid; j < m16; j += NT) list_k[j] = 0ull;  // batch padding: above nothing
+  __syncthreads();
+  // a survivor's count of the survivors above it is its rank when below k + 1
+  for (int x = tid; x < m; x += NT) {
+    const int r = count_above(list_k, 0, m16, list_k[x]);
+    const int i = list_i[x];
+    if (r < k) top[r] = i;
+    if (r == k - 1) bnd2[0] = i;
+    if (r == k) bnd2[1] = i;
+  }
+  __syncthreads();
+  repair_top<NT>(s2, img2, NC, k, bnd2, top);
+  if (w == 0 && lane < k) {
+    const int i = top[lane];
+    emit_entry<COH>(a, cand(i), (float)s2[i], ascending_pos(top, k, lane), l, l_end, b, h, pick, pick_layer);
+  }
 }
 
 // Selection of owner head `ou` by one workgroup of NW waves (`smem`: block_lds().total bytes).
@@ -412,9 +645,12 @@ __host__ __device__ inline BlockLds block_lds(int D, int S, int NC, int qrows) {
 // PASS: row passes per wave in flight (registers against memory parallelism). MP: max-product
 // bound scores (two-row representatives), else dot-product scores. QREG: keep the summed query in
 // registers (faster) rather than reading it from LDS at every row (fewer registers). GMAX: the
-// unit's score is the maximum of its q-heads' similarities, not their sum.
+// unit's score is the maximum of its q-heads' similarities, not their sum. pick: if not null, the
+// selection goes to this LDS array and to layer pick_layer's output row only (emit_pick), instead
+// of every layer of the call that shares it.
 template <class DT, int D, int NW, bool COH, int PASS = 2, bool MP = false, bool QREG = true, bool GMAX = false>
-__device__ void select_block(const SelectArgs& a, int ou, unsigned char* smem) {
+__device__ void select_block(const SelectArgs& a, int ou, unsigned char* smem, int32_t* pick = nullptr,
+                             int pick_layer = -1) {
   using SC = Scoring<D, PASS, MP, QREG, GMAX>;
   constexpr int NT = NW * kWave;
   constexpr int TILE = NW * (kWave / 4) * SC::P;  // rows per workgroup pass
@@ -433,7 +669,7 @@ __device__ void select_block(const SelectArgs& a, int ou, unsigned char* smem) {
   __shared__ int bnd1[2], bnd2[2];
 
   const int BH = a.B * a.Hsel;
-  const int l = a.own.l[ou / BH], b = (ou / a.Hsel) % a.B, h = ou % a.Hsel;
+  const int l = a.own.local(ou / BH), b = (ou / a.Hsel) % a.B, h = ou % a.Hsel;
   const size_t unit = ((size_t)l * a.B + b) * a.Hkv + h / a.rep_div;  // representatives' kv head
   const int tid = threadIdx.x, w = tid / kWave;
   const float* scent = a.scent + unit * a.ss * SC::RW;
@@ -459,6 +695,11 @@ __device__ void select_block(const SelectArgs& a, int ou, unsigned char* smem) {
     tile_load<SC::RW, SC::P>(scent, nullptr, a.S, r0, tile);
     SC::dot(tile, a.S, r0, qr, s1, img1, ck);
   }
+  if (register_ranking(a.S, a.NC, a.k_clusters)) {
+    select_block_reg<SC, NW, COH>(a, tile, qr, cent, s1, s2, ck, img1, img2, list_k, list_i, top,
+                                  (int*)(smem + lay.part), bnd2, l, b, h, pick, pick_layer);
+    return;
+  }
   __syncthreads();
   block_topk<NT>(ck, a.S, a.k_super, list_k, list_i, top, bnd1);
   repair_top<NT>(s1, img1, a.S, a.k_super, bnd1, top);
@@ -479,7 +720,10 @@ __device__ void select_block(const SelectArgs& a, int ou, unsigned char* smem) {
   __syncthreads();
   block_topk<NT>(ck, a.NC, a.k_clusters, list_k, list_i, top, bnd2);
   repair_top<NT>(s2, img2, a.NC, a.k_clusters, bnd2, top);
-  emit_selection<COH>(a, top, cand, s2, l, b, h, tid, NT);
+  if (pick)
+    emit_pick(a, top, cand, s2, pick_layer, b, h, pick, tid, NT);
+  else
+    emit_selection<COH>(a, top, cand, s2, l, b, h, tid, NT);
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -536,7 +780,7 @@ __device__ void select_waves(const SelectArgs& a, int ou0, unsigned char* smem) 
   int* cand = (int*)(base + lay.cand);
   int* bnd = (int*)(base + lay.bnd);  // boundary entries of level 1 ([0], [1]) and level 2 ([2], [3])
 
-  const int l = a.own.l[ou / BH], b = (ou / a.Hsel) % a.B, h = ou % a.Hsel;
+  const int l = a.own.local(ou / BH), b = (ou / a.Hsel) % a.B, h = ou % a.Hsel;
   const size_t unit = ((size_t)l * a.B + b) * a.Hkv + h / a.rep_div;  // representatives' kv head
   const float* scent = a.scent + unit * a.ss * SC::RW;
   const float* cent = a.cent + unit * a.cs * SC::RW;

@@ -2,9 +2,11 @@
 
 The step must give bit for bit what mpc_select_clusters followed by mpc_sparse_decode_attn give,
 and both are checked against the oracle: the selection with the tie rule, the attention output
-recomputed by the oracle from the selection the GPU made. Cases are chosen so that the one-launch
-kernel runs (at least as many (layer, sequence, kv head) units as compute units) with per-head and
-per-wave selection, owners inside and before the block, and the sequential fallback of small blocks.
+recomputed by the oracle from the selection the GPU made. Cases are chosen so that both one-launch
+kernels run: the self-selecting one (at most one (layer, sequence, kv head) unit per compute unit:
+every workgroup computes its owner head's selection) and the claiming one (more units: the first
+consumer of an owner head selects, the others wait for it), with per-head and per-wave selection,
+owners inside and before the block, and the sequential fallback of small blocks.
 """
 import math
 
@@ -21,8 +23,10 @@ pytestmark = pytest.mark.gpu
 
 # name -> (workload, overrides, layer0)
 CASES = {
-    # 8 layers x 32 kv heads = 256 units; owners 0, 1, 2, 6 -> per-head selection items
+    # 8 layers x 32 kv heads = 256 units (self-selecting); owners 0, 1, 2, 6
     "C3-L8": ("C3", dict(n_layers=8), 0),
+    # 16 layers: 512 units (claiming); owners 0, 1, 2, 6, 10, 14
+    "C3-L16": ("C3", dict(n_layers=16), 0),
     # layers 3..10: layers 3-5 are owned by layer 2 (before the block) -> their selection is an input
     "C3-L8@3": ("C3", dict(n_layers=8), 3),
     # 512 owner heads -> one wave per head
@@ -142,9 +146,9 @@ def test_decode_step_unit_that_gives_up_is_reported():
     units give up after their bounded poll: the error word reports it, those units' outputs are NaN,
     every other unit matches the normal step, and the head's words are back at zero afterwards.
     Every workgroup exits normally."""
-    w, layer0, k, v, cent, scent, sim = _setup("C3-L8")
+    w, layer0, k, v, cent, scent, sim = _setup("C3-L16")  # 512 units: the claiming kernel
     import paper_2501_06807_amd as M
-    say("[step give-up] C3-L8: owner head (layer 2, b 0, h 0) marked claimed before the launch")
+    say("[step give-up] C3-L16: owner head (layer 2, b 0, h 0) marked claimed before the launch")
     dt = synth.torch_dtype(w.dtype)
     cfg = M.select_cfg(w.cluster, w.fanout, w.k_super, w.k_clusters, 0.6, w.share_period, similarity=sim)
     kd, vd = bits_to_torch(k, w.dtype), bits_to_torch(v, w.dtype)
