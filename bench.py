@@ -37,8 +37,11 @@ def parse():
     p.add_argument("--warmup", type=int, default=1)
     p.add_argument("--workload", default="C4")
     p.add_argument("--decode-steps", type=int, default=None, help="decode steps per pass (default: workload's)")
-    p.add_argument("--decode-mode", choices=("split", "fused"), default="split",
-                   help="timed decode step: selection and attention as two kernels (default) or one launch")
+    p.add_argument("--decode-mode", choices=("auto", "split", "fused"), default="auto",
+                   help="timed decode step: selection and attention as two kernels (split) or one launch of "
+                        "mpc_decode_step (fused); auto (default): one launch when the block has at most one "
+                        "(layer, sequence, kv head) unit per compute unit, where every workgroup selects for its "
+                        "own unit, else two kernels")
     p.add_argument("--similarity", choices=("linear", "maxprod", "mean"), default="linear",
                    help="cluster similarity: the paper's linear form (default), the max-product bound (Eq. 2) "
                         "or the cluster average")
@@ -58,6 +61,18 @@ def parse():
 DECODE_STEP_SOURCES = ("fused.hip", "fused.h", "decode_dev.h", "select_dev.h", "decode_attn.h", "select.h",
                        "common.h")
 SPARSE_DECODE_SOURCES = ("decode_attn.hip", "decode_attn.h", "decode_dev.h", "common.h")
+
+
+NUM_CU = 256  # compute units of an MI355X
+
+
+def resolve_mode(mode, path):
+    """The decode mode a run times: `auto` takes the one launch where mpc_decode_step runs its
+    self-selecting kernel (at most one attention unit per compute unit: faster there than two
+    kernels), and the two kernels elsewhere (faster than the claiming one-launch kernel)."""
+    if mode != "auto":
+        return mode
+    return "fused" if path.L * path.B * path.Hsel <= NUM_CU else "split"
 
 
 def source_digest(*names):
@@ -376,11 +391,13 @@ def extra_workload(name, args, M, synth, torch, dev):
     w = synth.get(name)
     q_win, k, v, qs, path = make_state(w, args, M, synth, dev)
     torch.cuda.synchronize()
-    step_fn = path.decode_fused if args.decode_mode == "fused" else path.decode
+    mode = resolve_mode(args.decode_mode, path)
+    step_fn = path.decode_fused if mode == "fused" else path.decode
     pre_ms, dec_us, _ = timed_passes(path, q_win, k, v, qs, step_fn, max(3, args.steps), max(1, args.warmup), torch)
     del q_win, k, v
     sel_us, att_us = kernel_times(path, qs, torch)
     rec = step_record(w, path, M, args, dec_us, sel_us, att_us)
+    rec["decode_mode"] = mode
     rec["prefill_ms_per_pass"] = round(sum(pre_ms) / len(pre_ms), 3)
     rec["decode_steps_per_pass"] = len(qs)
     del path, qs
@@ -426,9 +443,10 @@ def main():
     q_win, k, v, qs, path = make_state(w, args, M, synth, dev)
     torch.cuda.synchronize()
 
-    fused = args.decode_mode == "fused"
+    mode = resolve_mode(args.decode_mode, path)
+    fused = mode == "fused"
     modes = {"split": path.decode, "fused": path.decode_fused}
-    step_fn = modes[args.decode_mode]
+    step_fn = modes[mode]
     mk = lambda: torch.cuda.Event(enable_timing=True)
     mean = lambda x: sum(x) / len(x)
 
@@ -460,7 +478,7 @@ def main():
     sel_us, att_us = kernel_times(path, qs, torch)
     alt = {}
     for name, fn in modes.items():  # every mode on the same state, E steps back to back
-        if name != args.decode_mode:
+        if name != mode:
             step_time(fn)
             alt[name] = round(step_time(fn), 3)
 
@@ -516,8 +534,11 @@ def main():
     dec_gbs = step_b / (dec_us * 1e-6) / 1e9
     if fused:
         traffic = measured_traffic("decode_step", args.workload, source_digest(*DECODE_STEP_SOURCES))
-        roofline = {"kernel": "k_decode_step (two-level selection + gather + online-softmax attention, "
-                              "all layers, one launch)",
+        one = ("k_decode_self (every workgroup selects for its own unit, then gathers and attends)"
+               if path.L * path.B * path.Hsel <= NUM_CU else
+               "k_decode_step (first consumer of an owner head selects, the others wait)")
+        roofline = {"kernel": one + ": two-level selection + gather + online-softmax attention, all layers, "
+                                    "one launch",
                     "bound": "hbm", "achieved": round(dec_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                     "frac": round(dec_gbs / HBM_PEAK_GBS, 4), "traffic": traffic,
                     "algorithmic_bytes_per_launch": step_b, "avg_launch_us": round(dec_us, 3)}
@@ -552,7 +573,7 @@ def main():
                    "k_super": w.k_super, "k_clusters": w.k_clusters, "share_period": w.share_period,
                    "similarity": args.similarity, "group": args.group, "decode_steps_per_pass": E,
                    **({"planting": PLANTING} if w.n_sinks or w.hh_count else {})},
-        "decode_step": {"mode": args.decode_mode, "us": round(dec_us, 3), "algorithmic_bytes": step_b,
+        "decode_step": {"mode": mode, "us": round(dec_us, 3), "algorithmic_bytes": step_b,
                         "achieved_GBps": round(dec_gbs, 1), "frac_of_hbm_peak": round(dec_gbs / HBM_PEAK_GBS, 4)},
         "kernels": {"select_us": round(sel_us, 3), "attention_us": round(att_us, 3),
                     "attention_algorithmic_bytes": att_b, "attention_GBps": round(att_gbs, 1),
