@@ -5,10 +5,8 @@
 namespace mpc {
 
 constexpr int kNumXcd = 8;       // accelerator dies; workgroup i runs on die i % 8
-constexpr int kRowBlock = 256;  // window rows per row-statistics workgroup (8 waves x 32)
-constexpr int kColWaveKeys = 32;  // keys per wave in the column-sum pass (one MFMA column block)
-constexpr int kColWaves = 8;      // waves per column-sum workgroup (they share each staged row tile)
-constexpr int kColBlockKeys = kColWaves * kColWaveKeys;
+constexpr int kRowBlock = 256;      // window rows per row-statistics workgroup
+constexpr int kColBlockKeys = 256;  // keys per column-sum workgroup (its waves share each staged row tile)
 
 struct EvictArgs {
   const void* q_win;   // [L][B][Hq][W][d]

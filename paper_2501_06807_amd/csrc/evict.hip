@@ -88,12 +88,26 @@ struct Tile {
   static constexpr int BYTES = 32 * RS;
 };
 
-constexpr int kRowThreads = kRowBlock / 32 * kWave;  // one wave per 32 window rows
+// Shape of the two scoring passes: a workgroup covers 256 window rows (pass 1) or 256 keys
+// (pass 2) as NBK register blocks of 32 per wave and 8 / NBK waves. 16-bit inputs take two blocks
+// per wave, so that every fragment staged in LDS feeds two matrix instructions (half the LDS reads
+// and per-tile overhead per score) at three waves per SIMD; fp32 fragments take twice the
+// registers and keep one block per wave.
+template <class DT>
+struct PassShape {
+  static constexpr int NBK = DT::kElt == 2 ? 2 : 1;
+  static constexpr int WAVES = kRowBlock / 32 / NBK;
+  static constexpr int THREADS = WAVES * kWave;
+  static constexpr int MIN_WAVES = NBK == 2 ? 3 : 1;  // waves per SIMD the register budget keeps
+};
+static_assert(kRowBlock == kColBlockKeys, "both passes cover 256 rows / keys per workgroup");
 
 template <class DT, int D>
-__global__ __launch_bounds__(kRowThreads) void k_rowstats(EvictArgs a) {
+__global__ __launch_bounds__(PassShape<DT>::THREADS, PassShape<DT>::MIN_WAVES) void k_rowstats(EvictArgs a) {
   using M = Mma<DT>;
-  using TL = Tile<DT, D, kRowThreads>;
+  using PS = PassShape<DT>;
+  constexpr int NBK = PS::NBK, NT = PS::THREADS;
+  using TL = Tile<DT, D, NT>;
   constexpr int KS = D / M::K;
   __shared__ __align__(16) unsigned char s_k[2][TL::BYTES];
 
@@ -108,15 +122,19 @@ __global__ __launch_bounds__(kRowThreads) void k_rowstats(EvictArgs a) {
   const size_t kvunit = ((size_t)l * a.B + b) * a.Hkv + hq / G;
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, c32 = lane & 31, hl = lane >> 5;
 
-  const int row_w0 = rb * kRowBlock + w * 32;  // first window row of this wave
-  const int t = row_w0 + c32;
-  const bool tvalid = t < a.W;
-  const int tc = tvalid ? t : a.W - 1;
-  const int pos = a.T - a.W + tc;
-  typename M::Op qf[KS];
-  const char* qrow = (const char*)a.q_win + ((size_t)qunit * a.W + tc) * TL::RB;
+  // block u of this wave holds window rows row0 + 32 u .. + 31; lane column c32 is row t[u]
+  const int row0 = rb * kRowBlock + w * 32 * NBK;
+  int t[NBK], pos[NBK];
+  typename M::Op qf[NBK][KS];
 #pragma unroll
-  for (int ks = 0; ks < KS; ++ks) qf[ks] = M::load(qrow + (ks * M::K + hl * M::KL) * DT::kElt);
+  for (int u = 0; u < NBK; ++u) {
+    t[u] = row0 + 32 * u + c32;
+    const int tc = t[u] < a.W ? t[u] : a.W - 1;
+    pos[u] = a.T - a.W + tc;
+    const char* qrow = (const char*)a.q_win + ((size_t)qunit * a.W + tc) * TL::RB;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) qf[u][ks] = M::load(qrow + (ks * M::K + hl * M::KL) * DT::kElt);
+  }
 
   const char* kh = (const char*)a.k + kvunit * a.T * TL::RB;
   const int last_row = min(a.W - 1, rb * kRowBlock + kRowBlock - 1);
@@ -127,7 +145,7 @@ __global__ __launch_bounds__(kRowThreads) void k_rowstats(EvictArgs a) {
   auto fetch = [&](int tile) {
 #pragma unroll
     for (int i = 0; i < TL::PER; ++i) {
-      const int ch = tid + i * kRowThreads;
+      const int ch = tid + i * NT;
       const int row = ch / TL::CH, c16 = ch % TL::CH;
       const int j = tile * 32 + row;
       pre[i] = (ch < TL::CHUNKS && j < a.T) ? ldg16(kh + (size_t)j * TL::RB + c16 * 16) : make_uint4(0, 0, 0, 0);
@@ -136,87 +154,101 @@ __global__ __launch_bounds__(kRowThreads) void k_rowstats(EvictArgs a) {
   auto stash = [&](int buf) {
 #pragma unroll
     for (int i = 0; i < TL::PER; ++i) {
-      const int ch = tid + i * kRowThreads;
+      const int ch = tid + i * NT;
       if (ch < TL::CHUNKS) *(uint4*)&s_k[buf][(ch / TL::CH) * TL::RS + (ch % TL::CH) * 16] = pre[i];
     }
   };
   fetch(0);
   stash(0);
+  // the row operands are in registers before the loop, so that no wait for them lands inside it
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
 
   const float cf = a.c32;
-  float m = -INFINITY, nb = INFINITY;  // running max and its offset fp32(-c * m)
-  double ell = 0.0;                    // sum of exp2(fma(c, s, nb)) so far
+  float m[NBK], nb[NBK];  // running max and its offset fp32(-c * m), per block
+  double ell[NBK];        // sum of exp2(fma(c, s, nb)) so far
+#pragma unroll
+  for (int u = 0; u < NBK; ++u) {
+    m[u] = -INFINITY;
+    nb[u] = INFINITY;
+    ell[u] = 0.0;
+  }
   for (int it = 0; it < ntile; ++it) {
     const int buf = it & 1;
     if (it + 1 < ntile) fetch(it + 1);
-    f32x16 acc = {};
+    f32x16 acc[NBK] = {};
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       const typename M::Op af =
           M::load(&s_k[buf][c32 * TL::RS + (ks * M::K + hl * M::KL) * DT::kElt]);
-      acc = M::run(af, qf[ks], acc);
+#pragma unroll
+      for (int u = 0; u < NBK; ++u) acc[u] = M::run(af, qf[u][ks], acc[u]);
     }
     const int j0 = it * 32;
-    // a tile wholly inside the causal triangle and the key range needs no per-element mask
-    // (uniform over the wave: its smallest row bounds every row's last visible key)
-    const bool full = j0 + 31 < a.T && (!a.causal || j0 + 31 <= a.T - a.W + row_w0);
-    float tmax = -INFINITY;
-    if (full) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, acc[r]);
-    } else {
+    for (int u = 0; u < NBK; ++u) {
+      // a tile wholly inside the causal triangle and the key range needs no per-element mask
+      // (uniform over the wave: the block's smallest row bounds every row's last visible key)
+      const bool full = j0 + 31 < a.T && (!a.causal || j0 + 31 <= a.T - a.W + row0 + 32 * u);
+      float tmax = -INFINITY;
+      if (full) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int j = j0 + acc_row(r, lane);
-        if (j < a.T && (!a.causal || j <= pos)) tmax = fmaxf(tmax, acc[r]);
+        for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, acc[u][r]);
+      } else {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int j = j0 + acc_row(r, lane);
+          if (j < a.T && (!a.causal || j <= pos[u])) tmax = fmaxf(tmax, acc[u][r]);
+        }
       }
-    }
-    if (tmax > m) {
-      const float nb_new = -(cf * tmax);
-      if (ell > 0.0) ell *= exp2((double)nb_new - (double)nb);
-      m = tmax;
-      nb = nb_new;
-    }
-    float ps = 0.f;
-    if (full) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) ps += fast_exp2(fmaf(cf, acc[r], nb));
-    } else {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int j = j0 + acc_row(r, lane);
-        if (j < a.T && (!a.causal || j <= pos)) ps += fast_exp2(fmaf(cf, acc[r], nb));
+      if (tmax > m[u]) {
+        const float nb_new = -(cf * tmax);
+        if (ell[u] > 0.0) ell[u] *= exp2((double)nb_new - (double)nb[u]);
+        m[u] = tmax;
+        nb[u] = nb_new;
       }
+      float ps = 0.f;
+      if (full) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) ps += fast_exp2(fmaf(cf, acc[u][r], nb[u]));
+      } else {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int j = j0 + acc_row(r, lane);
+          if (j < a.T && (!a.causal || j <= pos[u])) ps += fast_exp2(fmaf(cf, acc[u][r], nb[u]));
+        }
+      }
+      ell[u] += (double)ps;
     }
-    ell += (double)ps;
     if (it + 1 < ntile) stash(buf ^ 1);
     __syncthreads();
   }
-  // the two half-waves' sums meet at the offset of the larger max (the smaller offset)
-  const double eo = __shfl_xor(ell, 32);
-  const float nbo = __shfl_xor(nb, 32);
-  const float nbx = fminf(nb, nbo);
-  double L = 0.0;
-  if (ell > 0.0) L += ell * exp2((double)nbx - (double)nb);
-  if (eo > 0.0) L += eo * exp2((double)nbx - (double)nbo);
-  if (hl == 0 && tvalid) {
-    a.rowstat[(size_t)qunit * a.W + t] = make_float2(nbx, (float)(1.0 / L));
-    // log-sum-exp of the scaled scores: log2 of sum exp2(c * s) = log2(L) - offset
-    if (a.row_lse) a.row_lse[(size_t)qunit * a.W + t] = (float)((log2(L) - (double)nbx) * 0.69314718055994531);
+#pragma unroll
+  for (int u = 0; u < NBK; ++u) {
+    // the two half-waves' sums meet at the offset of the larger max (the smaller offset)
+    const double eo = __shfl_xor(ell[u], 32);
+    const float nbo = __shfl_xor(nb[u], 32);
+    const float nbx = fminf(nb[u], nbo);
+    double L = 0.0;
+    if (ell[u] > 0.0) L += ell[u] * exp2((double)nbx - (double)nb[u]);
+    if (eo > 0.0) L += eo * exp2((double)nbx - (double)nbo);
+    if (hl == 0 && t[u] < a.W) {
+      a.rowstat[(size_t)qunit * a.W + t[u]] = make_float2(nbx, (float)(1.0 / L));
+      // log-sum-exp of the scaled scores: log2 of sum exp2(c * s) = log2(L) - offset
+      if (a.row_lse) a.row_lse[(size_t)qunit * a.W + t[u]] = (float)((log2(L) - (double)nbx) * 0.69314718055994531);
+    }
   }
 }
 
-constexpr int kColThreads = kColWaves * kWave;
-
 template <class DT, int D>
-__global__ __launch_bounds__(kColThreads) void k_colsum(EvictArgs a) {
+__global__ __launch_bounds__(PassShape<DT>::THREADS, PassShape<DT>::MIN_WAVES) void k_colsum(EvictArgs a) {
   using M = Mma<DT>;
-  using TL = Tile<DT, D, kColThreads>;
+  using PS = PassShape<DT>;
+  constexpr int NBK = PS::NBK, NT = PS::THREADS;
+  using TL = Tile<DT, D, NT>;
   constexpr int KS = D / M::K;
-  constexpr int NB = kColWaveKeys / 32;
   __shared__ __align__(16) unsigned char s_q[2][TL::BYTES];
-  __shared__ float s_nb[2][32], s_il[2][32];  // offset and 1 / sum of the staged rows
+  __shared__ __align__(16) float s_nb[2][32], s_il[2][32];  // offset and 1 / sum of the staged rows
 
   const int n_kb = (a.T + kColBlockKeys - 1) / kColBlockKeys;
   const int id = xcd_remap(blockIdx.x, gridDim.x);
@@ -228,16 +260,17 @@ __global__ __launch_bounds__(kColThreads) void k_colsum(EvictArgs a) {
   const int G = a.Hq / a.Hkv;
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, c32 = lane & 31, hl = lane >> 5;
 
-  const int jw = kb * kColBlockKeys + w * kColWaveKeys;
+  // block u of this wave holds keys jw + 32 u .. + 31; lane column c32 is key jw + 32 u + c32
+  const int jw = kb * kColBlockKeys + w * 32 * NBK;
   const float cf = a.c32;
   const char* kh = (const char*)a.k + (size_t)kvunit * a.T * TL::RB;
-  typename M::Op kf[NB][KS];
+  typename M::Op kf[NBK][KS];
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    const int j = min(jw + nb * 32 + c32, a.T - 1);
+  for (int u = 0; u < NBK; ++u) {
+    const int j = min(jw + 32 * u + c32, a.T - 1);
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
-      kf[nb][ks] = M::load(kh + (size_t)j * TL::RB + (ks * M::K + hl * M::KL) * DT::kElt);
+      kf[u][ks] = M::load(kh + (size_t)j * TL::RB + (ks * M::K + hl * M::KL) * DT::kElt);
   }
 
   const int j_lo = kb * kColBlockKeys;
@@ -253,7 +286,7 @@ __global__ __launch_bounds__(kColThreads) void k_colsum(EvictArgs a) {
     const char* qb = (const char*)a.q_win + ((qunit0 + g) * a.W) * TL::RB;
 #pragma unroll
     for (int i = 0; i < TL::PER; ++i) {
-      const int ch = tid + i * kColThreads;
+      const int ch = tid + i * NT;
       const int row = ch / TL::CH, c16 = ch % TL::CH;
       const int t = t0 + row;
       pre[i] = (ch < TL::CHUNKS && t < a.W) ? ldg16(qb + (size_t)t * TL::RB + c16 * 16) : make_uint4(0, 0, 0, 0);
@@ -266,7 +299,7 @@ __global__ __launch_bounds__(kColThreads) void k_colsum(EvictArgs a) {
   auto stash = [&](int buf) {
 #pragma unroll
     for (int i = 0; i < TL::PER; ++i) {
-      const int ch = tid + i * kColThreads;
+      const int ch = tid + i * NT;
       if (ch < TL::CHUNKS) *(uint4*)&s_q[buf][(ch / TL::CH) * TL::RS + (ch % TL::CH) * 16] = pre[i];
     }
     if (tid < 32) {
@@ -276,56 +309,67 @@ __global__ __launch_bounds__(kColThreads) void k_colsum(EvictArgs a) {
   };
   fetch(0);
   stash(0);
+  // the key operands are in registers before the loop, so that no wait for them lands inside it
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
 
-  double cacc[NB];
+  double cacc[NBK];
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) cacc[nb] = 0.0;
+  for (int u = 0; u < NBK; ++u) cacc[u] = 0.0;
   for (int it = 0; it < ntile; ++it) {
     const int buf = it & 1;
     if (it + 1 < ntile) fetch(it + 1);
     const int t0 = t_start + (it % n_t) * 32;
-    float nbr[16], ilr[16];
-    int trow[16];
+    f32x16 acc[NBK] = {};
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int rr = acc_row(r, lane);
-      trow[r] = t0 + rr;
-      nbr[r] = s_nb[buf][rr];
-      ilr[r] = s_il[buf][rr];
+    for (int ks = 0; ks < KS; ++ks) {
+      const typename M::Op af =
+          M::load(&s_q[buf][c32 * TL::RS + (ks * M::K + hl * M::KL) * DT::kElt]);
+#pragma unroll
+      for (int u = 0; u < NBK; ++u) acc[u] = M::run(af, kf[u][ks], acc[u]);
     }
+    // every row of the tile valid and every key of the wave's last block visible to its first row
+    const bool full = t0 + 31 < a.W && (!a.causal || jw + 32 * NBK - 1 <= a.T - a.W + t0);
+    float ps[NBK];
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      f32x16 acc = {};
+    for (int u = 0; u < NBK; ++u) ps[u] = 0.f;
+    if (full) {
+      // the tile's rows of this lane: 8 g + 4 hl + (0..3), g = 0..3, read four at a time
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const typename M::Op af =
-            M::load(&s_q[buf][c32 * TL::RS + (ks * M::K + hl * M::KL) * DT::kElt]);
-        acc = M::run(af, kf[nb][ks], acc);
-      }
-      const int j = jw + nb * 32 + c32;
-      // every row of the tile valid and every key of the wave visible to its first row
-      const bool full = t0 + 31 < a.W && (!a.causal || jw + nb * 32 + 31 <= a.T - a.W + t0);
-      float ps = 0.f;
-      if (full) {
+      for (int g4 = 0; g4 < 4; ++g4) {
+        const float4 nb4 = *(const float4*)&s_nb[buf][8 * g4 + 4 * hl];
+        const float4 il4 = *(const float4*)&s_il[buf][8 * g4 + 4 * hl];
+        const float nbv[4] = {nb4.x, nb4.y, nb4.z, nb4.w}, ilv[4] = {il4.x, il4.y, il4.z, il4.w};
 #pragma unroll
-        for (int r = 0; r < 16; ++r) ps = fmaf(fast_exp2(fmaf(cf, acc[r], nbr[r])), ilr[r], ps);
-      } else {
+        for (int q = 0; q < 4; ++q) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          if (trow[r] < a.W && (!a.causal || j <= a.T - a.W + trow[r]))
-            ps = fmaf(fast_exp2(fmaf(cf, acc[r], nbr[r])), ilr[r], ps);
+          for (int u = 0; u < NBK; ++u)
+            ps[u] = fmaf(fast_exp2(fmaf(cf, acc[u][4 * g4 + q], nbv[q])), ilv[q], ps[u]);
         }
       }
-      cacc[nb] += (double)ps;
+    } else {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int rr = acc_row(r, lane);
+        const int trow = t0 + rr;
+        if (trow >= a.W) continue;
+        const float nbv = s_nb[buf][rr], ilv = s_il[buf][rr];
+#pragma unroll
+        for (int u = 0; u < NBK; ++u) {
+          const int j = jw + 32 * u + c32;
+          if (!a.causal || j <= a.T - a.W + trow) ps[u] = fmaf(fast_exp2(fmaf(cf, acc[u][r], nbv)), ilv, ps[u]);
+        }
+      }
     }
+#pragma unroll
+    for (int u = 0; u < NBK; ++u) cacc[u] += (double)ps[u];
     if (it + 1 < ntile) stash(buf ^ 1);
     __syncthreads();
   }
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    const double tot = cacc[nb] + __shfl_xor(cacc[nb], 32);
-    const int j = jw + nb * 32 + c32;
+  for (int u = 0; u < NBK; ++u) {
+    const double tot = cacc[u] + __shfl_xor(cacc[u], 32);
+    const int j = jw + 32 * u + c32;
     if (hl == 0 && j < a.T) a.score[(size_t)kvunit * a.T + j] = (float)tot;
   }
 }
@@ -574,10 +618,10 @@ template <class DT, int D>
 hipError_t launch_pass(const EvictArgs& a, bool rows, hipStream_t st) {
   if (rows) {
     const int n_rb = (a.W + kRowBlock - 1) / kRowBlock;
-    hipLaunchKernelGGL((k_rowstats<DT, D>), dim3(a.own.n * a.B * a.Hq * n_rb), dim3(kRowThreads), 0, st, a);
+    hipLaunchKernelGGL((k_rowstats<DT, D>), dim3(a.own.n * a.B * a.Hq * n_rb), dim3(PassShape<DT>::THREADS), 0, st, a);
   } else {
     const int n_kb = (a.T + kColBlockKeys - 1) / kColBlockKeys;
-    hipLaunchKernelGGL((k_colsum<DT, D>), dim3(a.own.n * a.B * a.Hkv * n_kb), dim3(kColThreads), 0, st, a);
+    hipLaunchKernelGGL((k_colsum<DT, D>), dim3(a.own.n * a.B * a.Hkv * n_kb), dim3(PassShape<DT>::THREADS), 0, st, a);
   }
   return hipGetLastError();
 }
