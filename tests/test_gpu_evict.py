@@ -116,6 +116,33 @@ def test_static_evict_matches_oracle(name):
     say(f"  tie swaps {swaps}, worst score relative error {worst:.2e}")
 
 
+# Edges of the scoring passes' register blocks (a wave holds two blocks of 32 window rows in the
+# row pass and two blocks of 32 keys in the column pass; a workgroup covers 256 rows / keys): windows
+# that end inside a wave's first or second row block or just past a workgroup, key ranges that end
+# inside a wave's second key block, both element sizes and head dims, grouped heads.
+EDGE_CASES = {
+    "W20-T1000": dict(base="C3", n_q_heads=4, n_kv_heads=1, T=1000, window=20, keep=512),
+    "W33-T993-fp16": dict(base="C3", n_q_heads=2, n_kv_heads=2, dtype="fp16", T=993, window=33, keep=480),
+    "W64-T1088": dict(base="C3", n_q_heads=4, n_kv_heads=2, T=1088, window=64, keep=544),
+    "W65-T1057-d64": dict(base="C2", n_layers=1, n_q_heads=4, n_kv_heads=4, dtype="bf16", T=1057, window=65, keep=528),
+    "W257-T1285": dict(base="C3", n_q_heads=2, n_kv_heads=1, T=1285, window=257, keep=640),
+    "W100-T700-fp32": dict(base="C3", n_q_heads=2, n_kv_heads=2, dtype="fp32", T=700, window=100, keep=352),
+}
+
+
+@pytest.mark.parametrize("name", list(EDGE_CASES))
+def test_static_evict_block_edges(name):
+    o = dict(EDGE_CASES[name])
+    w = synth.get(o.pop("base")).with_(n_layers=o.pop("n_layers", 1), **o)
+    say(f"[evict edge] {name} Hq={w.n_q_heads} Hkv={w.n_kv_heads} d={w.head_dim} T={w.T} W={w.window} "
+        f"keep={w.keep} {w.dtype}")
+    qw, k, v = _prefill(w)
+    got = _run_gpu(w, qw, k, v)
+    swaps, worst = _check(w, qw, k, v, got)
+    _row_lse_check(w, qw, k, got[4], rows=16)
+    say(f"  tie swaps {swaps}, worst score relative error {worst:.2e}")
+
+
 def test_static_evict_block_whose_first_owner_precedes_it():
     w = synth.get("C2").with_(n_layers=3, T=700, window=140, keep=320, n_q_heads=4, n_kv_heads=4)
     say("[evict] layer block starting at 3 (layer 3 follows layer 2)")
