@@ -8,7 +8,8 @@ sparse attention over all layers). The reported metric is the decode step's late
 (select + attention), measured with HIP events on the stream the kernels run on, with its
 effective HBM bandwidth against the 8 TB/s peak. Prefill figures are reported beside it, and so is
 the decode step in the other mode (two kernels, or one launch of mpc_decode_step). Measured
-ceilings give the fractions a scale: a random-order chunk read (the attention's access pattern), a
+ceilings give the fractions a scale: a random-order chunk read (the attention's access pattern) over
+2 GiB and over exactly the attention's bytes of each workload (one launch, fixed costs included), a
 matrix-core throughput kernel, a device copy; the CPU oracle is timed on a bounded sample, on all
 host threads and on one.
 
@@ -151,6 +152,53 @@ def measure_read_ceiling(dev, chunk_bytes=16384, per_wg=24, total=2 << 30):
     return {"GBps": round(gbs, 1), "frac_of_peak": round(gbs / HBM_PEAK_GBS, 4),
             "note": "every 16 KB chunk of 2 GiB read once in random order, 16-byte non-temporal loads (the "
                     "sparse attention's pattern)"}
+
+
+def measure_read_time(dev, nbytes, chunk_bytes=16384, total=2 << 30):
+    """Time of the same chunk-read kernel reading about `nbytes` (a decode step's attention bytes)
+    as 16 KB chunks in random order, the best of three grid shapes (1024 / 2560 / 5120 workgroups
+    of four waves), each the per-launch average of five back-to-back launches: what one launch that
+    only reads this many bytes the attention's way takes on this GPU, fixed costs included."""
+    import ctypes
+
+    import torch
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2501_06807_amd", "libmpc_ceiling.so"))
+    lib.mpc_read_ceiling.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_void_p, ctypes.c_int,
+                                     ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+    n_chunks = total // chunk_bytes
+    want = max(1, min(n_chunks, round(nbytes / chunk_bytes)))
+    buf = torch.empty(total, dtype=torch.uint8, device=dev).fill_(3)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(11)
+    perm = torch.randperm(n_chunks, generator=gen, device=dev, dtype=torch.int32)
+    st = torch.cuda.current_stream(dev)
+    best = None
+    for g in (1024, 2560, 5120):
+        per_wg = max(1, want // g)
+        grid = max(1, want // per_wg)
+        order = perm[:grid * per_wg].contiguous()
+        sink = torch.empty(grid * 256, dtype=torch.int32, device=dev)
+
+        def launch():
+            rc = lib.mpc_read_ceiling(buf.data_ptr(), n_chunks, chunk_bytes, order.data_ptr(), grid, per_wg,
+                                      sink.data_ptr(), st.cuda_stream)
+            if rc != 0:
+                raise RuntimeError(f"read kernel failed to launch ({rc})")
+
+        launch()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(st)
+        for _ in range(5):
+            launch()
+        b.record(st)
+        torch.cuda.synchronize()
+        us = a.elapsed_time(b) * 1e3 / 5
+        nb = grid * per_wg * chunk_bytes
+        if best is None or nb / us > best[0] / best[1]:
+            best = (nb, us, grid)
+    del buf, perm
+    nb, us, grid = best
+    return {"bytes": nb, "us": round(us, 3), "GBps": round(nb / us / 1e3, 1), "workgroups": grid}
 
 
 def measure_mfma_ceiling(dev, grid=2048, iters=2048):
@@ -397,6 +445,8 @@ def extra_workload(name, args, M, synth, torch, dev):
     del q_win, k, v
     sel_us, att_us = kernel_times(path, qs, torch)
     rec = step_record(w, path, M, args, dec_us, sel_us, att_us)
+    rec["read_same_bytes"] = measure_read_time(dev, rec["attention_algorithmic_bytes"])
+    rec["attention_us_over_read_us"] = round(att_us / rec["read_same_bytes"]["us"], 4)
     rec["decode_mode"] = mode
     rec["prefill_ms_per_pass"] = round(sum(pre_ms) / len(pre_ms), 3)
     rec["decode_steps_per_pass"] = len(qs)
@@ -553,6 +603,7 @@ def main():
                                    "us": round(dec_us, 3)}}
     fl = prefill_flops(w, len(owners))
     pre_tflops = fl / (mean(pre_ms) * 1e-3) / 1e12
+    read_same = measure_read_time(dev, att_b)
 
     rec = {
         "metric": METRIC,
@@ -578,8 +629,12 @@ def main():
         "kernels": {"select_us": round(sel_us, 3), "attention_us": round(att_us, 3),
                     "attention_algorithmic_bytes": att_b, "attention_GBps": round(att_gbs, 1),
                     "attention_frac_of_hbm_peak": round(att_gbs / HBM_PEAK_GBS, 4),
+                    "read_same_bytes": read_same,
+                    "attention_us_over_read_us": round(att_us / read_same["us"], 4),
                     "note": "each kernel launched once per decode step, back to back, between two HIP "
-                            "events; per-launch average (attention reads each step's own selection)"},
+                            "events; per-launch average (attention reads each step's own selection); "
+                            "read_same_bytes: one launch of the read-ceiling kernel reading the attention's "
+                            "bytes as 16 KB chunks in random order, best of three grid shapes"},
         "decode_step_other_modes": alt,
         "decode_step_cache": cache,
         "selection_quality": quality,

@@ -102,14 +102,30 @@ __device__ __forceinline__ void finish_unit(const DecodeArgs& a, int unit, int s
     const int g = t / D, dim = t % D;
     const float* p0 = a.part + ((size_t)unit * a.splits * G + g) * (D + 2);
     const size_t stride = (size_t)G * (D + 2);
+    // every split's (m, l, o) is requested before any is used: one memory round trip for the
+    // merge instead of one per split and pass (these loads bypass the per-die caches)
+    float mv[kMaxSplits], lv[kMaxSplits], ov[kMaxSplits];
+#pragma unroll
+    for (int i = 0; i < kMaxSplits; ++i) {
+      if (i < a.splits) {
+        const float* p = p0 + i * stride;
+        mv[i] = ld_coherent(p + D);
+        lv[i] = ld_coherent(p + D + 1);
+        ov[i] = ld_coherent(p + dim);
+      }
+    }
     float M = -1e30f;
-    for (int i = 0; i < a.splits; ++i) M = fmaxf(M, ld_coherent(p0 + i * stride + D));
+#pragma unroll
+    for (int i = 0; i < kMaxSplits; ++i)
+      if (i < a.splits) M = fmaxf(M, mv[i]);
     float L = 0.f, O = 0.f;
-    for (int i = 0; i < a.splits; ++i) {
-      const float* p = p0 + i * stride;
-      const float r = fast_exp2(ld_coherent(p + D) - M);
-      L += ld_coherent(p + D + 1) * r;
-      O += ld_coherent(p + dim) * r;
+#pragma unroll
+    for (int i = 0; i < kMaxSplits; ++i) {
+      if (i < a.splits) {
+        const float r = fast_exp2(mv[i] - M);
+        L += lv[i] * r;
+        O += ov[i] * r;
+      }
     }
     store_elt<DT>(a.out, (q_row0 + g) * D + dim, O / L);
     if (dim == 0 && a.lse) a.lse[q_row0 + g] = (M + __log2f(L)) * 0.69314718055994531f;
