@@ -19,7 +19,7 @@ import torch
 
 import oracle
 import synth
-from gpu_util import assert_out_close, bits_to_torch, boundary_score, say
+from gpu_util import assert_out_close, bits_to_torch, boundary_score, say, torch_to_bits
 
 pytestmark = pytest.mark.gpu
 
@@ -158,3 +158,99 @@ def test_random_shape_decode_path(i):
     assert torch.equal(sel1, sel), "one-launch selection differs from mpc_select_clusters"
     assert torch.equal(out1.view(torch.uint8), out.view(torch.uint8)), "one-launch output differs"
     say(f"  tie swaps {swaps}, worst attention relative error {worst:.2e}")
+
+
+N_EVICT_CASES = 16
+
+
+def _draw_evict(i):
+    """Shape of static-eviction case i: element type, head dim, grouped heads, sequences, layer block
+    and sharing, prompt length, window rows (ending anywhere inside the scoring passes' register
+    blocks), kept and recent counts."""
+    rng = np.random.default_rng(0xE71C0000 + i)
+    d = int(rng.choice([64, 128]))
+    dtype = str(rng.choice(["bf16", "fp16", "fp32"]))
+    G = int(rng.choice([1, 2, 4]))
+    Hkv = int(rng.integers(1, 3))
+    B = int(rng.integers(1, 3))
+    L = int(rng.integers(1, 5))
+    layer0 = int(rng.integers(0, 4))
+    period = int(rng.choice([1, 2, 4]))
+    start = int(rng.choice([0, 2]))
+    T = int(rng.integers(64, 1400))
+    W = int(rng.integers(1, min(T, 300) + 1))
+    local = int(rng.integers(0, 65))
+    keep = int(rng.integers(max(local, 1), T + 1))
+    s = int(rng.choice([4, 8, 16, 32]))
+    f = int(rng.choice([2, 4, 8]))
+    sim = str(rng.choice(["linear", "maxprod", "mean"]))
+    base = "C2" if d == 64 else "C3"
+    w = synth.get(base).with_(n_layers=L, batch=B, n_q_heads=G * Hkv, n_kv_heads=Hkv, head_dim=d, dtype=dtype, T=T,
+                              window=W, keep=keep, local_keep=local, cluster=s, fanout=f, share_period=period,
+                              share_start=start, seed=synth.workloads.SEED_BASE + 200 + i)
+    return w, layer0, sim
+
+
+@pytest.mark.parametrize("i", range(N_EVICT_CASES))
+def test_random_shape_static_eviction_and_prefill(i):
+    """Static eviction against the oracle (token scores within 2e-5, kept sets equal up to boundary
+    ties, gathered rows a bit copy, row log-sum-exp sampled) and the one-call prefill equal to
+    eviction followed by the cluster build, bit for bit."""
+    import paper_2501_06807_amd as M
+    from test_gpu_evict import _check, _row_lse_check
+    w, layer0, sim = _draw_evict(i)
+    say(f"[random evict {i}] {w.dtype} d={w.head_dim} L={w.n_layers}@{layer0} B={w.batch} Hq={w.n_q_heads} "
+        f"Hkv={w.n_kv_heads} P={w.share_period}/{w.share_start} T={w.T} W={w.window} keep={w.keep} "
+        f"local={w.local_keep} s={w.cluster} f={w.fanout} {sim}")
+    parts = [synth.prefill_host(w, layer0 + l) for l in range(w.n_layers)]
+    qw, k, v = (np.stack([p[j] for p in parts]) for j in range(3))
+    # layers owned before the block arrive with their kept set
+    kept_in = np.zeros((w.n_layers, w.batch, w.n_kv_heads, w.keep), dtype=np.int32)
+    given = [l for l in range(w.n_layers) if oracle.owner_layer(layer0 + l, w.share_period, w.share_start) < layer0]
+    loc = min(w.local_keep, w.keep)
+    for l in given:  # a kept set of the method's form: older tokens, then the recent window
+        older = np.sort(np.random.default_rng(i).choice(w.T - loc, w.keep - loc, replace=False))
+        kept_in[l] = np.concatenate([older, np.arange(w.T - loc, w.T)]).astype(np.int32)
+    dt = w.dtype
+    qd, kd, vd = bits_to_torch(qw, dt), bits_to_torch(k, dt), bits_to_torch(v, dt)
+    R = 2 if sim == "maxprod" else 1
+    C = -(-w.keep // w.cluster)
+    S = -(-C // w.fanout)
+    cfg = M.select_cfg(w.cluster, w.fanout, 1, 1, 0.6, w.share_period, w.share_start, sim)
+    sm = 1.0 / math.sqrt(w.head_dim)
+
+    def run(fused):
+        kept = torch.from_numpy(kept_in).cuda()
+        k_out = torch.zeros((w.n_layers, w.batch, w.n_kv_heads, w.keep, w.head_dim), dtype=synth.torch_dtype(dt),
+                            device="cuda")
+        v_out = torch.zeros_like(k_out)
+        cent = torch.zeros((w.n_layers, w.batch, w.n_kv_heads, C, R, w.head_dim), dtype=torch.float32, device="cuda")
+        scent = torch.zeros((w.n_layers, w.batch, w.n_kv_heads, S, R, w.head_dim), dtype=torch.float32,
+                            device="cuda")
+        score = torch.zeros((w.n_layers, w.batch, w.n_kv_heads, w.T), dtype=torch.float32, device="cuda")
+        lse = torch.zeros((w.n_layers, w.batch, w.n_q_heads, w.window), dtype=torch.float32, device="cuda")
+        kw = dict(keep=w.keep, local_keep=w.local_keep, sm_scale=sm, layer0=layer0, share_period=w.share_period,
+                  share_start=w.share_start, token_score=score, row_lse=lse)
+        if fused:
+            M.mpc_prefill(qd, kd, vd, kept, k_out, v_out, cent, scent, cfg, **kw)
+        else:
+            M.mpc_static_evict(qd, kd, vd, kept, k_out, v_out, **kw)
+            M.mpc_build_clusters(k_out, cent, scent, cfg, Ts=w.keep, layer0=layer0)
+        torch.cuda.synchronize()
+        return [kept.cpu().numpy(), torch_to_bits(k_out, dt), torch_to_bits(v_out, dt), score.cpu().numpy(),
+                lse.cpu().numpy(), cent.cpu().numpy(), scent.cpu().numpy()]
+
+    two = run(False)
+    one = run(True)
+    for a, b, name in zip(two, one, ["kept", "k_out", "v_out", "token_score", "row_lse", "cent", "scent"]):
+        if name == "cent" or name == "scent":  # representatives exist for the selection's owner layers
+            owners = [l for l in range(w.n_layers)
+                      if oracle.owner_layer(layer0 + l, w.share_period, w.share_start) == layer0 + l]
+            a, b = a[owners], b[owners]
+        assert np.array_equal(a, b), f"one-call prefill differs from the two calls in {name}"
+    for l in given:
+        np.testing.assert_array_equal(two[0][l], kept_in[l])
+    # scores and kept sets of the layers owned inside the block; every layer's gathered rows
+    swaps, worst = _check(w, qw, k, v, two[:5], layer0=layer0)
+    _row_lse_check(w, qw, k, two[4], layer0=layer0, rows=6)
+    say(f"  tie swaps {swaps}, worst score relative error {worst:.2e}")
