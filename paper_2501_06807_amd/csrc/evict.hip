@@ -88,6 +88,26 @@ struct Tile {
   static constexpr int BYTES = 32 * RS;
 };
 
+// The PER 16-byte chunks a thread stages from each 32-row tile: chunk i is row row[i] of the
+// tile, at byte mem[i] from the tile's first row in memory and byte lds[i] of an LDS buffer. The
+// offsets are the same for every tile, so they are computed once per thread.
+template <class TL, int NT>
+struct TileChunks {
+  unsigned row[TL::PER], mem[TL::PER], lds[TL::PER];
+  int tid;
+  __device__ explicit TileChunks(int t) : tid(t) {
+#pragma unroll
+    for (int i = 0; i < TL::PER; ++i) {
+      const int ch = t + i * NT;
+      row[i] = ch / TL::CH;
+      mem[i] = row[i] * TL::RB + (ch % TL::CH) * 16;
+      lds[i] = row[i] * TL::RS + (ch % TL::CH) * 16;
+    }
+  }
+  // whether chunk i exists (always, when the threads cover the tile's chunks exactly)
+  __device__ bool ok(int i) const { return (i + 1) * NT <= TL::CHUNKS || tid + i * NT < TL::CHUNKS; }
+};
+
 // Shape of the two scoring passes: a workgroup covers 256 window rows (pass 1) or 256 keys
 // (pass 2) as NBK register blocks of 32 per wave and 8 / NBK waves. 16-bit inputs take two blocks
 // per wave, so that every fragment staged in LDS feeds two matrix instructions (half the LDS reads
@@ -141,22 +161,25 @@ __global__ __launch_bounds__(PassShape<DT>::THREADS, PassShape<DT>::MIN_WAVES) v
   const int jend = a.causal ? min(a.T, a.T - a.W + last_row + 1) : a.T;
   const int ntile = (jend + 31) / 32;
 
+  const TileChunks<TL, NT> tc(tid);
   uint4 pre[TL::PER];
+  // key tiles lying wholly inside the cache load without per-chunk row tests or zero fills
   auto fetch = [&](int tile) {
+    const char* tb = kh + (size_t)tile * (32 * TL::RB);
+    if (tile * 32 + 32 <= a.T) {
 #pragma unroll
-    for (int i = 0; i < TL::PER; ++i) {
-      const int ch = tid + i * NT;
-      const int row = ch / TL::CH, c16 = ch % TL::CH;
-      const int j = tile * 32 + row;
-      pre[i] = (ch < TL::CHUNKS && j < a.T) ? ldg16(kh + (size_t)j * TL::RB + c16 * 16) : make_uint4(0, 0, 0, 0);
+      for (int i = 0; i < TL::PER; ++i)
+        if (tc.ok(i)) pre[i] = ldg16(tb + tc.mem[i]);
+    } else {
+#pragma unroll
+      for (int i = 0; i < TL::PER; ++i)
+        pre[i] = tc.ok(i) && tile * 32 + (int)tc.row[i] < a.T ? ldg16(tb + tc.mem[i]) : make_uint4(0, 0, 0, 0);
     }
   };
   auto stash = [&](int buf) {
 #pragma unroll
-    for (int i = 0; i < TL::PER; ++i) {
-      const int ch = tid + i * NT;
-      if (ch < TL::CHUNKS) *(uint4*)&s_k[buf][(ch / TL::CH) * TL::RS + (ch % TL::CH) * 16] = pre[i];
-    }
+    for (int i = 0; i < TL::PER; ++i)
+      if (tc.ok(i)) *(uint4*)&s_k[buf][tc.lds[i]] = pre[i];
   };
   fetch(0);
   stash(0);
@@ -279,35 +302,42 @@ __global__ __launch_bounds__(PassShape<DT>::THREADS, PassShape<DT>::MIN_WAVES) v
   const int ntile = G * n_t;
   const size_t qunit0 = ((size_t)l * a.B + b) * a.Hq + (size_t)h * G;
 
+  const TileChunks<TL, NT> tc(tid);
   uint4 pre[TL::PER];
   float2 pre_b = make_float2(0.f, 0.f);
-  auto fetch = [&](int tile) {
-    const int g = tile / n_t, t0 = t_start + (tile % n_t) * 32;
-    const char* qb = (const char*)a.q_win + ((qunit0 + g) * a.W) * TL::RB;
+  // tiles run through the group's heads, each from row t_start to t_end; the next one to fetch is
+  // head fg's rows ft0 .. ft0 + 31 (a counter, not a division per tile)
+  const int t_end = t_start + n_t * 32;
+  int fg = 0, ft0 = t_start;
+  auto fetch = [&]() {
+    const size_t r0 = (qunit0 + fg) * a.W + ft0;
+    const char* tb = (const char*)a.q_win + r0 * TL::RB;
+    if (ft0 + 32 <= a.W) {
 #pragma unroll
-    for (int i = 0; i < TL::PER; ++i) {
-      const int ch = tid + i * NT;
-      const int row = ch / TL::CH, c16 = ch % TL::CH;
-      const int t = t0 + row;
-      pre[i] = (ch < TL::CHUNKS && t < a.W) ? ldg16(qb + (size_t)t * TL::RB + c16 * 16) : make_uint4(0, 0, 0, 0);
+      for (int i = 0; i < TL::PER; ++i)
+        if (tc.ok(i)) pre[i] = ldg16(tb + tc.mem[i]);
+    } else {
+#pragma unroll
+      for (int i = 0; i < TL::PER; ++i)
+        pre[i] = tc.ok(i) && ft0 + (int)tc.row[i] < a.W ? ldg16(tb + tc.mem[i]) : make_uint4(0, 0, 0, 0);
     }
-    if (tid < 32) {
-      const int t = t0 + tid;
-      pre_b = t < a.W ? a.rowstat[(qunit0 + g) * a.W + t] : make_float2(0.f, 0.f);
+    if (tid < 32) pre_b = ft0 + tid < a.W ? a.rowstat[r0 + tid] : make_float2(0.f, 0.f);
+    ft0 += 32;
+    if (ft0 == t_end) {
+      ft0 = t_start;
+      ++fg;
     }
   };
   auto stash = [&](int buf) {
 #pragma unroll
-    for (int i = 0; i < TL::PER; ++i) {
-      const int ch = tid + i * NT;
-      if (ch < TL::CHUNKS) *(uint4*)&s_q[buf][(ch / TL::CH) * TL::RS + (ch % TL::CH) * 16] = pre[i];
-    }
+    for (int i = 0; i < TL::PER; ++i)
+      if (tc.ok(i)) *(uint4*)&s_q[buf][tc.lds[i]] = pre[i];
     if (tid < 32) {
       s_nb[buf][tid] = pre_b.x;
       s_il[buf][tid] = pre_b.y;
     }
   };
-  fetch(0);
+  fetch();
   stash(0);
   // the key operands are in registers before the loop, so that no wait for them lands inside it
   __builtin_amdgcn_s_waitcnt(0);
@@ -316,10 +346,10 @@ __global__ __launch_bounds__(PassShape<DT>::THREADS, PassShape<DT>::MIN_WAVES) v
   double cacc[NBK];
 #pragma unroll
   for (int u = 0; u < NBK; ++u) cacc[u] = 0.0;
+  int t0 = t_start;  // first window row of the tile being scored
   for (int it = 0; it < ntile; ++it) {
     const int buf = it & 1;
-    if (it + 1 < ntile) fetch(it + 1);
-    const int t0 = t_start + (it % n_t) * 32;
+    if (it + 1 < ntile) fetch();
     f32x16 acc[NBK] = {};
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
@@ -364,6 +394,7 @@ __global__ __launch_bounds__(PassShape<DT>::THREADS, PassShape<DT>::MIN_WAVES) v
 #pragma unroll
     for (int u = 0; u < NBK; ++u) cacc[u] += (double)ps[u];
     if (it + 1 < ntile) stash(buf ^ 1);
+    t0 = t0 + 32 == t_end ? t_start : t0 + 32;
     __syncthreads();
   }
 #pragma unroll
