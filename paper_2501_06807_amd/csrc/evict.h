@@ -16,7 +16,7 @@ struct EvictArgs {
   void* k_out;         // [L][B][Hkv][out_rows][d], rows [0, keep) written
   void* v_out;
   float* score;        // [L][B][Hkv][T] accumulated attention (token_score or workspace)
-  float2* rowstat;     // [L][B][Hq][W]: (b = fp32(-c * max score), 1 / sum of exp2(fma(c, score, b)))
+  float2* rowstat;     // [L][B][Hq][W]: (b = -ceil(c * max score), 1 / sum of exp2(fma(c, score, b)))
   float* row_lse;      // [L][B][Hq][W] natural log-sum-exp, optional
   int B, layer0, n_layers, Hq, Hkv, T, W, keep, local_keep, causal, period, start;
   int out_rows;        // row capacity of k_out / v_out per (layer, sequence, kv head)

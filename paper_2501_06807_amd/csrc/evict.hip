@@ -6,17 +6,18 @@
 // (v_mfma_f32_32x32x{16,16,2}_{bf16,f16,f32}):
 //   pass 1 (k_rowstats): window rows stay in registers as the B operand, key tiles stream
 //     through LDS as the A operand; each lane owns one query column of the 32x32 output, so the
-//     row max and row sum are in-lane reductions. Output per row: the offset b = fp32(-c * m) of
-//     the row max m and 1 / sum of exp2(fma(c, s, b)), c = fp32(sm_scale * log2(e)).
+//     row max and row sum are in-lane reductions. Output per row: the whole-number offset
+//     b = -ceil(fp32(c * m)) of the row max m and 1 / sum of exp2(fma(c, s, b)),
+//     c = fp32(sm_scale * log2(e)).
 //   pass 2 (k_colsum): keys stay in registers as the B operand, window-row tiles (all query heads
 //     of the group) stream through LDS as the A operand; each lane owns one key column, so the
 //     column sum is in-lane. p = exp2(fma(c, s, b)) / sum, summed over 16 rows in fp32 and
 //     accumulated across tiles in fp64. Both passes form the exponent with one fused multiply-add
-//     against the same fp32 offset, so the offset's rounding is a common factor of a row's terms
-//     and of its sum and cancels in p; when the running max moves, pass 1 rebases its fp64 sum by
-//     exp2(b_new - b_old), exact from the two fp32 offsets. The remaining error of each exponent
-//     is its own rounding and that of c, both proportional to |c * (s - m)|: smallest on the
-//     terms that carry the sums.
+//     against the same offset, so the offset is a common factor of a row's terms and of its sum
+//     and cancels in p; it only has to keep every exponent at or below about 0. Being a whole
+//     number, a move of the running max rescales pass 1's fp64 sum by an exact power of two
+//     (ldexp). The exponents of the terms near the max lie in (-1, 0], so their rounding, and that
+//     of c (proportional to |c * (s - m)|), stay smallest on the terms that carry the sums.
 // The top-k is a 4-pass, 8-bit LDS radix select on the fp32 score bits followed by an ordered
 // block compaction, each thread's run of scores held in registers up to 32K older tokens; the
 // gather copies kept rows with 16-byte lanes (all layers, or those whose representatives are not
@@ -188,7 +189,7 @@ __global__ __launch_bounds__(PassShape<DT>::THREADS, PassShape<DT>::MIN_WAVES) v
   __syncthreads();
 
   const float cf = a.c32;
-  float m[NBK], nb[NBK];  // running max and its offset fp32(-c * m), per block
+  float m[NBK], nb[NBK];  // running max and its whole-number offset -ceil(c * m), per block
   double ell[NBK];        // sum of exp2(fma(c, s, nb)) so far
 #pragma unroll
   for (int u = 0; u < NBK; ++u) {
@@ -225,8 +226,9 @@ __global__ __launch_bounds__(PassShape<DT>::THREADS, PassShape<DT>::MIN_WAVES) v
         }
       }
       if (tmax > m[u]) {
-        const float nb_new = -(cf * tmax);
-        if (ell[u] > 0.0) ell[u] *= exp2((double)nb_new - (double)nb[u]);
+        // offsets are whole numbers, so moving one rescales the sum by a power of two (exact)
+        const float nb_new = -ceilf(cf * tmax);
+        if (ell[u] > 0.0 && nb_new != nb[u]) ell[u] = ldexp(ell[u], (int)(nb_new - nb[u]));
         m[u] = tmax;
         nb[u] = nb_new;
       }
@@ -253,8 +255,8 @@ __global__ __launch_bounds__(PassShape<DT>::THREADS, PassShape<DT>::MIN_WAVES) v
     const float nbo = __shfl_xor(nb[u], 32);
     const float nbx = fminf(nb[u], nbo);
     double L = 0.0;
-    if (ell[u] > 0.0) L += ell[u] * exp2((double)nbx - (double)nb[u]);
-    if (eo > 0.0) L += eo * exp2((double)nbx - (double)nbo);
+    if (ell[u] > 0.0) L += ldexp(ell[u], (int)(nbx - nb[u]));
+    if (eo > 0.0) L += ldexp(eo, (int)(nbx - nbo));
     if (hl == 0 && t[u] < a.W) {
       a.rowstat[(size_t)qunit * a.W + t[u]] = make_float2(nbx, (float)(1.0 / L));
       // log-sum-exp of the scaled scores: log2 of sum exp2(c * s) = log2(L) - offset
