@@ -95,23 +95,6 @@ __device__ __forceinline__ float load_elt<F16>(const void* base, size_t i) {
   return f16_to_f32(((const uint16_t*)base)[i]);
 }
 
-// Four consecutive elements starting at element i (8-byte aligned for 16-bit types).
-template <class DT>
-__device__ __forceinline__ void load4(const void* base, size_t i, float* out) {
-  if constexpr (DT::kElt == 4) {
-    const float4 v = *(const float4*)((const float*)base + i);
-    out[0] = v.x;
-    out[1] = v.y;
-    out[2] = v.z;
-    out[3] = v.w;
-  } else {
-    const uint2 v = *(const uint2*)((const uint16_t*)base + i);
-    out[0] = load_elt<DT>(&v, 0);
-    out[1] = load_elt<DT>(&v, 1);
-    out[2] = load_elt<DT>(&v, 2);
-    out[3] = load_elt<DT>(&v, 3);
-  }
-}
 
 template <class DT>
 __device__ __forceinline__ void store_elt(void* base, size_t i, float x);
