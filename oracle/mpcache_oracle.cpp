@@ -80,7 +80,7 @@ int32_t ceil_div(int32_t a, int32_t b) { return (a + b - 1) / b; }
 // ------------------------------------------------------------------------------------ rules
 
 // Static eviction scores only the last 20% of the prompt's queries, and 10% once the prompt is
-// longer than 24k tokens (Sec. 3.2; App. F "Static eviction"). Reading: 24k = 24 * 1024 tokens,
+// longer than 24k tokens (Sec. 3.2; App. F, static-eviction setting). Reading: 24k = 24 * 1024 tokens,
 // the row count is rounded down, and at least one row is used.
 int32_t mpcref_window_rows(int32_t T) {
   if (T <= 0) return 0;
@@ -227,7 +227,7 @@ int mpcref_cluster_bounds(int32_t n_tok, int32_t d, int32_t dtype, const void* k
 }
 
 // Average of a cluster's keys, the naive representative the paper compares against (Sec. 3.3
-// opening; App. "comparison with average-based similarity"): the fp64 sum over the cluster's
+// opening; the appendix that compares it with the paper's similarity): the fp64 sum over the cluster's
 // tokens in token order divided by their count. Reading: the score is the dot product with this
 // average (like the other representatives), and it is stored rounded to fp32.
 int mpcref_cluster_mean(int32_t n_tok, int32_t d, int32_t dtype, const void* k, int32_t first,

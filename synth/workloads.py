@@ -109,7 +109,7 @@ WORKLOADS = {
 
 
 # Level-2 budgets with the dynamic ratio read against the prompt length T instead of the kept cache
-# (the Fig. 9 caption's "final KV cache budget"): floor(eta * T / s) clusters, at most the
+# (the Fig. 9 caption speaks of the final budget of the KV cache): floor(eta * T / s) clusters, at most the
 # candidates. The tiny workload states its budget (8 clusters) outright, so it keeps it.
 K_CLUSTERS_OF_PROMPT = {"C1": 8, "C2": 16, "C3": 25, "C4": 51, "C5": 40, "X1": 25}
 

@@ -46,7 +46,7 @@ def test_workload_integers_follow_the_rules(name):
 
 
 def test_level2_budget_of_the_prompt_reading():
-    # The Fig. 9 caption's "final KV cache budget" reads eta against the prompt: at the GPT-2 workload
+    # The Fig. 9 caption, which calls eta the final budget of the KV cache, reads it against the prompt: at the GPT-2 workload
     # (T = 2048, static ratio 50%, eta = 12.5%, s = 16) that is 2048 / 8 / 16 = 16 clusters, twice
     # the 8 clusters of the post-eviction reading.
     w = synth.get("C2")
