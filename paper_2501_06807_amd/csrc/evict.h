@@ -7,6 +7,7 @@ namespace mpc {
 constexpr int kNumXcd = 8;       // accelerator dies; workgroup i runs on die i % 8
 constexpr int kRowBlock = 256;      // window rows per row-statistics workgroup
 constexpr int kColBlockKeys = 256;  // keys per column-sum workgroup (its waves share each staged row tile)
+constexpr int kColThreads16 = 256;  // column-sum workgroup for 16-bit inputs: 4 waves of 64 keys
 
 struct EvictArgs {
   const void* q_win;   // [L][B][Hq][W][d]

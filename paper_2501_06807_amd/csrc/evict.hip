@@ -9,10 +9,12 @@
 //     row max and row sum are in-lane reductions. Output per row: the whole-number offset
 //     b = -ceil(fp32(c * m)) of the row max m and 1 / sum of exp2(fma(c, s, b)),
 //     c = fp32(sm_scale * log2(e)).
-//   pass 2 (k_colsum): keys stay in registers as the B operand, window-row tiles (all query heads
-//     of the group) stream through LDS as the A operand; each lane owns one key column, so the
-//     column sum is in-lane. p = exp2(fma(c, s, b)) / sum, summed over 16 rows in fp32 and
-//     accumulated across tiles in fp64. Both passes form the exponent with one fused multiply-add
+//   pass 2 (k_colsum16 for 16-bit inputs, k_colsum for fp32): keys stay in registers as the B
+//     operand, window-row tiles (all query heads of the group) stream through LDS as the A
+//     operand; each lane owns one key column, so the column sum needs no exchange within a tile.
+//     p = exp2(fma(c, s, b)) / sum, summed over a lane's rows of a tile in fp32 and accumulated
+//     across tiles in fp64. 16-bit inputs use 16x16x32 blocks, so that each block's exponentials
+//     overlap the next block's matrix chain. Both passes form the exponent with one fused multiply-add
 //     against the same offset, so the offset is a common factor of a row's terms and of its sum
 //     and cancels in p; it only has to keep every exponent at or below about 0. Being a whole
 //     number, a move of the running max rescales pass 1's fp64 sum by an exact power of two
@@ -23,6 +25,8 @@
 // gather copies kept rows with 16-byte lanes (all layers, or those whose representatives are not
 // built in the same pass).
 #include "evict.h"
+
+#include <type_traits>
 
 namespace mpc {
 namespace {
@@ -63,6 +67,21 @@ struct Mma<F32> {
   }
   __device__ static Op load(const void* p) { return *(const float*)p; }
 };
+
+// 16x16x32 matrix-core operation for 16-bit inputs: lane l feeds row (l % 16) of A / column
+// (l % 16) of B with the k-slice [(l / 16) * 8, + 8) of each 32-wide step, and receives the output
+// rows 4 (l / 16) + r, r = 0..3, of column l % 16.
+typedef float f32x4 __attribute__((__vector_size__(4 * sizeof(float))));
+template <class DT>
+__device__ __forceinline__ f32x4 mma16(uint4 a, uint4 b, f32x4 c);
+template <>
+__device__ __forceinline__ f32x4 mma16<BF16>(uint4 a, uint4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+template <>
+__device__ __forceinline__ f32x4 mma16<F16>(uint4 a, uint4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
+}
 
 // Row of the 32x32 output held in accumulator register r of `lane` (the column is lane % 32).
 __device__ __forceinline__ int acc_row(int r, int lane) {
@@ -109,11 +128,11 @@ struct TileChunks {
   __device__ bool ok(int i) const { return (i + 1) * NT <= TL::CHUNKS || tid + i * NT < TL::CHUNKS; }
 };
 
-// Shape of the two scoring passes: a workgroup covers 256 window rows (pass 1) or 256 keys
-// (pass 2) as NBK register blocks of 32 per wave and 8 / NBK waves. 16-bit inputs take two blocks
-// per wave, so that every fragment staged in LDS feeds two matrix instructions (half the LDS reads
-// and per-tile overhead per score) at three waves per SIMD; fp32 fragments take twice the
-// registers and keep one block per wave.
+// Shape of the 32x32 scoring passes (pass 1; pass 2 for fp32 inputs): a workgroup covers 256
+// window rows (pass 1) or 256 keys (pass 2) as NBK register blocks of 32 per wave and 8 / NBK
+// waves. 16-bit inputs take two blocks per wave, so that every fragment staged in LDS feeds two
+// matrix instructions (half the LDS reads and per-tile overhead per score) at three waves per
+// SIMD; fp32 fragments take twice the registers and keep one block per wave.
 template <class DT>
 struct PassShape {
   static constexpr int NBK = DT::kElt == 2 ? 2 : 1;
@@ -265,6 +284,7 @@ __global__ __launch_bounds__(PassShape<DT>::THREADS, PassShape<DT>::MIN_WAVES) v
   }
 }
 
+// Column pass on 32x32 matrix instructions (fp32 inputs; 16-bit inputs take k_colsum16 below).
 template <class DT, int D>
 __global__ __launch_bounds__(PassShape<DT>::THREADS, PassShape<DT>::MIN_WAVES) void k_colsum(EvictArgs a) {
   using M = Mma<DT>;
@@ -404,6 +424,148 @@ __global__ __launch_bounds__(PassShape<DT>::THREADS, PassShape<DT>::MIN_WAVES) v
     const double tot = cacc[u] + __shfl_xor(cacc[u], 32);
     const int j = jw + 32 * u + c32;
     if (hl == 0 && j < a.T) a.score[(size_t)kvunit * a.T + j] = (float)tot;
+  }
+}
+
+// Column pass for 16-bit inputs on 16x16x32 matrix instructions. A wave holds 64 keys in
+// registers as four 16-key B operands and takes each 32-row window tile from LDS as two 16-row A
+// operands, so a tile is eight 16x16 blocks of four accumulators each; every block's exponentials
+// and sums run while the next block's four matrix instructions execute (a block's vector work,
+// twelve instructions, matches its matrix work), with no second accumulator set. A lane holds rows
+// 4 (lane / 16) + r of one key per block; its fp32 sum over a tile's eight rows goes into an fp64
+// total, and the four lanes of a key meet once at the end.
+template <class DT, int D>
+__global__ __launch_bounds__(kColThreads16, 3) void k_colsum16(EvictArgs a) {
+  constexpr int NT = kColThreads16;
+  using TL = Tile<DT, D, NT>;
+  constexpr int KS = D / 32;
+  static_assert(DT::kElt == 2, "16-bit inputs");
+  static_assert(NT / kWave * 64 == kColBlockKeys, "four waves of 64 keys");
+  __shared__ __align__(16) unsigned char s_q[2][TL::BYTES];
+  __shared__ __align__(16) float s_nb[2][32], s_il[2][32];  // offset and 1 / sum of the staged rows
+
+  const int n_kb = (a.T + kColBlockKeys - 1) / kColBlockKeys;
+  const int id = xcd_remap(blockIdx.x, gridDim.x);
+  const int kb = id % n_kb;
+  const int ou = id / n_kb;  // (owner index * B + b) * Hkv + h
+  const int l = a.own.local(ou / (a.B * a.Hkv));
+  const int b = (ou / a.Hkv) % a.B, h = ou % a.Hkv;
+  const size_t kvunit = ((size_t)l * a.B + b) * a.Hkv + h;
+  const int G = a.Hq / a.Hkv;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, c16 = lane & 15, q4 = lane >> 4;
+
+  // key group g of this wave holds keys jw + 16 g + lane % 16
+  const int jw = kb * kColBlockKeys + w * 64;
+  const float cf = a.c32;
+  const char* kh = (const char*)a.k + (size_t)kvunit * a.T * TL::RB;
+  uint4 kf[4][KS];
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    const int j = min(jw + 16 * g + c16, a.T - 1);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) kf[g][ks] = ldg16(kh + (size_t)j * TL::RB + (ks * 32 + q4 * 8) * DT::kElt);
+  }
+
+  const int j_lo = kb * kColBlockKeys;
+  const int t_start = a.causal ? (max(0, j_lo - (a.T - a.W)) & ~31) : 0;
+  const int n_t = (a.W - t_start + 31) / 32;
+  const int ntile = G * n_t;
+  const size_t qunit0 = ((size_t)l * a.B + b) * a.Hq + (size_t)h * G;
+
+  const TileChunks<TL, NT> tc(tid);
+  uint4 pre[TL::PER];
+  float2 pre_b = make_float2(0.f, 0.f);
+  // tiles run through the group's heads, each from row t_start to t_end; the next one to fetch is
+  // head fg's rows ft0 .. ft0 + 31
+  const int t_end = t_start + n_t * 32;
+  int fg = 0, ft0 = t_start;
+  auto fetch = [&]() {
+    const size_t r0 = (qunit0 + fg) * a.W + ft0;
+    const char* tb = (const char*)a.q_win + r0 * TL::RB;
+    if (ft0 + 32 <= a.W) {
+#pragma unroll
+      for (int i = 0; i < TL::PER; ++i)
+        if (tc.ok(i)) pre[i] = ldg16(tb + tc.mem[i]);
+    } else {
+#pragma unroll
+      for (int i = 0; i < TL::PER; ++i)
+        pre[i] = tc.ok(i) && ft0 + (int)tc.row[i] < a.W ? ldg16(tb + tc.mem[i]) : make_uint4(0, 0, 0, 0);
+    }
+    if (tid < 32) pre_b = ft0 + tid < a.W ? a.rowstat[r0 + tid] : make_float2(0.f, 0.f);
+    ft0 += 32;
+    if (ft0 == t_end) {
+      ft0 = t_start;
+      ++fg;
+    }
+  };
+  auto stash = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < TL::PER; ++i)
+      if (tc.ok(i)) *(uint4*)&s_q[buf][tc.lds[i]] = pre[i];
+    if (tid < 32) {
+      s_nb[buf][tid] = pre_b.x;
+      s_il[buf][tid] = pre_b.y;
+    }
+  };
+  fetch();
+  stash(0);
+  // the key operands are in registers before the loop, so that no wait for them lands inside it
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+
+  double cacc[4] = {0.0, 0.0, 0.0, 0.0};
+  int t0 = t_start;  // first window row of the tile being scored
+  // one tile; FULL: every row valid and every key of the wave visible to the tile's first row
+  auto tile = [&](auto full_tag, int buf) {
+    constexpr bool FULL = decltype(full_tag)::value;
+    float ps[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int rh = 0; rh < 2; ++rh) {
+      // this lane's rows of the half: t0 + 16 rh + 4 (lane / 16) + r
+      const float4 nb4 = *(const float4*)&s_nb[buf][16 * rh + 4 * q4];
+      const float4 il4 = *(const float4*)&s_il[buf][16 * rh + 4 * q4];
+      const float nbv[4] = {nb4.x, nb4.y, nb4.z, nb4.w}, ilv[4] = {il4.x, il4.y, il4.z, il4.w};
+      uint4 af[KS];
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+        af[ks] = *(const uint4*)&s_q[buf][(16 * rh + c16) * TL::RS + (ks * 32 + q4 * 8) * DT::kElt];
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        f32x4 c = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) c = mma16<DT>(af[ks], kf[g][ks], c);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          if constexpr (FULL) {
+            ps[g] = fmaf(fast_exp2(fmaf(cf, c[r], nbv[r])), ilv[r], ps[g]);
+          } else {
+            const int t = t0 + 16 * rh + 4 * q4 + r, j = jw + 16 * g + c16;
+            if (t < a.W && (!a.causal || j <= a.T - a.W + t))
+              ps[g] = fmaf(fast_exp2(fmaf(cf, c[r], nbv[r])), ilv[r], ps[g]);
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int g = 0; g < 4; ++g) cacc[g] += (double)ps[g];
+  };
+  for (int it = 0; it < ntile; ++it) {
+    const int buf = it & 1;
+    if (it + 1 < ntile) fetch();
+    if (t0 + 31 < a.W && (!a.causal || jw + 63 <= a.T - a.W + t0))
+      tile(std::true_type{}, buf);
+    else
+      tile(std::false_type{}, buf);
+    if (it + 1 < ntile) stash(buf ^ 1);
+    t0 = t0 + 32 == t_end ? t_start : t0 + 32;
+    __syncthreads();
+  }
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    double tot = cacc[g] + __shfl_xor(cacc[g], 16);
+    tot += __shfl_xor(tot, 32);
+    const int j = jw + 16 * g + c16;
+    if (q4 == 0 && j < a.T) a.score[(size_t)kvunit * a.T + j] = (float)tot;
   }
 }
 
@@ -654,7 +816,10 @@ hipError_t launch_pass(const EvictArgs& a, bool rows, hipStream_t st) {
     hipLaunchKernelGGL((k_rowstats<DT, D>), dim3(a.own.n * a.B * a.Hq * n_rb), dim3(PassShape<DT>::THREADS), 0, st, a);
   } else {
     const int n_kb = (a.T + kColBlockKeys - 1) / kColBlockKeys;
-    hipLaunchKernelGGL((k_colsum<DT, D>), dim3(a.own.n * a.B * a.Hkv * n_kb), dim3(PassShape<DT>::THREADS), 0, st, a);
+    if constexpr (DT::kElt == 2)
+      hipLaunchKernelGGL((k_colsum16<DT, D>), dim3(a.own.n * a.B * a.Hkv * n_kb), dim3(kColThreads16), 0, st, a);
+    else
+      hipLaunchKernelGGL((k_colsum<DT, D>), dim3(a.own.n * a.B * a.Hkv * n_kb), dim3(PassShape<DT>::THREADS), 0, st, a);
   }
   return hipGetLastError();
 }
