@@ -96,19 +96,19 @@ __device__ __forceinline__ int xcd_remap(int bid, int n) {
   return x < r ? x * (q + 1) + slot : r * (q + 1) + (x - r) * q + slot;
 }
 
-// 32-row tiles of a [rows][D] matrix staged through LDS with 16-byte chunks; the row stride is
-// padded by 16 bytes to spread the 32 rows of a fragment read over the LDS banks.
-template <class DT, int D, int NT = 256>
+// Tiles of ROWS rows of a [rows][D] matrix staged through LDS with 16-byte chunks; the row stride
+// is padded by 16 bytes to spread the rows of a fragment read over the LDS banks.
+template <class DT, int D, int NT = 256, int ROWS = 32>
 struct Tile {
   static constexpr int RB = D * DT::kElt;
   static constexpr int RS = RB + 16;
   static constexpr int CH = RB / 16;
-  static constexpr int CHUNKS = 32 * CH;
+  static constexpr int CHUNKS = ROWS * CH;
   static constexpr int PER = (CHUNKS + NT - 1) / NT;  // chunks per thread (NT threads)
-  static constexpr int BYTES = 32 * RS;
+  static constexpr int BYTES = ROWS * RS;
 };
 
-// The PER 16-byte chunks a thread stages from each 32-row tile: chunk i is row row[i] of the
+// The PER 16-byte chunks a thread stages from each tile: chunk i is row row[i] of the
 // tile, at byte mem[i] from the tile's first row in memory and byte lds[i] of an LDS buffer. The
 // offsets are the same for every tile, so they are computed once per thread.
 template <class TL, int NT>
@@ -428,21 +428,23 @@ __global__ __launch_bounds__(PassShape<DT>::THREADS, PassShape<DT>::MIN_WAVES) v
 }
 
 // Column pass for 16-bit inputs on 16x16x32 matrix instructions. A wave holds 64 keys in
-// registers as four 16-key B operands and takes each 32-row window tile from LDS as two 16-row A
-// operands, so a tile is eight 16x16 blocks of four accumulators each; every block's exponentials
-// and sums run while the next block's four matrix instructions execute (a block's vector work,
-// twelve instructions, matches its matrix work), with no second accumulator set. A lane holds rows
-// 4 (lane / 16) + r of one key per block; its fp32 sum over a tile's eight rows goes into an fp64
+// registers as four 16-key B operands and takes each 64-row window tile from LDS as four 16-row A
+// operands, so a tile is sixteen 16x16 blocks of four accumulators each; every block's
+// exponentials and sums run while the next block's four matrix instructions execute (a block's
+// vector work, twelve instructions, matches its matrix work), with no second accumulator set, and
+// a barrier, a tile load and a row-statistics stash serve 64 rows. A lane holds rows
+// 4 (lane / 16) + r of one key per block; its fp32 sum over a tile's sixteen rows goes into an fp64
 // total, and the four lanes of a key meet once at the end.
 template <class DT, int D>
 __global__ __launch_bounds__(kColThreads16, 3) void k_colsum16(EvictArgs a) {
   constexpr int NT = kColThreads16;
-  using TL = Tile<DT, D, NT>;
+  constexpr int RT = 64;  // window rows per staged tile
+  using TL = Tile<DT, D, NT, RT>;
   constexpr int KS = D / 32;
   static_assert(DT::kElt == 2, "16-bit inputs");
   static_assert(NT / kWave * 64 == kColBlockKeys, "four waves of 64 keys");
   __shared__ __align__(16) unsigned char s_q[2][TL::BYTES];
-  __shared__ __align__(16) float s_nb[2][32], s_il[2][32];  // offset and 1 / sum of the staged rows
+  __shared__ __align__(16) float s_nb[2][RT], s_il[2][RT];  // offset and 1 / sum of the staged rows
 
   const int n_kb = (a.T + kColBlockKeys - 1) / kColBlockKeys;
   const int id = xcd_remap(blockIdx.x, gridDim.x);
@@ -468,7 +470,7 @@ __global__ __launch_bounds__(kColThreads16, 3) void k_colsum16(EvictArgs a) {
 
   const int j_lo = kb * kColBlockKeys;
   const int t_start = a.causal ? (max(0, j_lo - (a.T - a.W)) & ~31) : 0;
-  const int n_t = (a.W - t_start + 31) / 32;
+  const int n_t = (a.W - t_start + RT - 1) / RT;
   const int ntile = G * n_t;
   const size_t qunit0 = ((size_t)l * a.B + b) * a.Hq + (size_t)h * G;
 
@@ -476,13 +478,13 @@ __global__ __launch_bounds__(kColThreads16, 3) void k_colsum16(EvictArgs a) {
   uint4 pre[TL::PER];
   float2 pre_b = make_float2(0.f, 0.f);
   // tiles run through the group's heads, each from row t_start to t_end; the next one to fetch is
-  // head fg's rows ft0 .. ft0 + 31
-  const int t_end = t_start + n_t * 32;
+  // head fg's rows ft0 .. ft0 + RT - 1
+  const int t_end = t_start + n_t * RT;
   int fg = 0, ft0 = t_start;
   auto fetch = [&]() {
     const size_t r0 = (qunit0 + fg) * a.W + ft0;
     const char* tb = (const char*)a.q_win + r0 * TL::RB;
-    if (ft0 + 32 <= a.W) {
+    if (ft0 + RT <= a.W) {
 #pragma unroll
       for (int i = 0; i < TL::PER; ++i)
         if (tc.ok(i)) pre[i] = ldg16(tb + tc.mem[i]);
@@ -491,8 +493,8 @@ __global__ __launch_bounds__(kColThreads16, 3) void k_colsum16(EvictArgs a) {
       for (int i = 0; i < TL::PER; ++i)
         pre[i] = tc.ok(i) && ft0 + (int)tc.row[i] < a.W ? ldg16(tb + tc.mem[i]) : make_uint4(0, 0, 0, 0);
     }
-    if (tid < 32) pre_b = ft0 + tid < a.W ? a.rowstat[r0 + tid] : make_float2(0.f, 0.f);
-    ft0 += 32;
+    if (tid < RT) pre_b = ft0 + tid < a.W ? a.rowstat[r0 + tid] : make_float2(0.f, 0.f);
+    ft0 += RT;
     if (ft0 == t_end) {
       ft0 = t_start;
       ++fg;
@@ -502,7 +504,7 @@ __global__ __launch_bounds__(kColThreads16, 3) void k_colsum16(EvictArgs a) {
 #pragma unroll
     for (int i = 0; i < TL::PER; ++i)
       if (tc.ok(i)) *(uint4*)&s_q[buf][tc.lds[i]] = pre[i];
-    if (tid < 32) {
+    if (tid < RT) {
       s_nb[buf][tid] = pre_b.x;
       s_il[buf][tid] = pre_b.y;
     }
@@ -520,8 +522,8 @@ __global__ __launch_bounds__(kColThreads16, 3) void k_colsum16(EvictArgs a) {
     constexpr bool FULL = decltype(full_tag)::value;
     float ps[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int rh = 0; rh < 2; ++rh) {
-      // this lane's rows of the half: t0 + 16 rh + 4 (lane / 16) + r
+    for (int rh = 0; rh < RT / 16; ++rh) {
+      // this lane's rows of the quarter: t0 + 16 rh + 4 (lane / 16) + r
       const float4 nb4 = *(const float4*)&s_nb[buf][16 * rh + 4 * q4];
       const float4 il4 = *(const float4*)&s_il[buf][16 * rh + 4 * q4];
       const float nbv[4] = {nb4.x, nb4.y, nb4.z, nb4.w}, ilv[4] = {il4.x, il4.y, il4.z, il4.w};
@@ -552,12 +554,12 @@ __global__ __launch_bounds__(kColThreads16, 3) void k_colsum16(EvictArgs a) {
   for (int it = 0; it < ntile; ++it) {
     const int buf = it & 1;
     if (it + 1 < ntile) fetch();
-    if (t0 + 31 < a.W && (!a.causal || jw + 63 <= a.T - a.W + t0))
+    if (t0 + RT - 1 < a.W && (!a.causal || jw + 63 <= a.T - a.W + t0))
       tile(std::true_type{}, buf);
     else
       tile(std::false_type{}, buf);
     if (it + 1 < ntile) stash(buf ^ 1);
-    t0 = t0 + 32 == t_end ? t_start : t0 + 32;
+    t0 = t0 + RT == t_end ? t_start : t0 + RT;
     __syncthreads();
   }
 #pragma unroll
