@@ -3,7 +3,7 @@
 // The accumulated attention of key j is A[j] = sum over the group's window rows t of
 // softmax_j(sm_scale * q_t . k_j). It needs every row's normaliser before any column can be
 // summed, so it takes two passes over the scores, both on the matrix cores
-// (v_mfma_f32_32x32x{16,16,2}_{bf16,f16,f32}):
+// (v_mfma_f32_32x32x{16,16,2}_{bf16,f16,f32}; the column pass of 16-bit inputs 16x16x32):
 //   pass 1 (k_rowstats): window rows stay in registers as the B operand, key tiles stream
 //     through LDS as the A operand; each lane owns one query column of the 32x32 output, so the
 //     row max and row sum are in-lane reductions. Output per row: the whole-number offset
@@ -13,8 +13,9 @@
 //     operand, window-row tiles (all query heads of the group) stream through LDS as the A
 //     operand; each lane owns one key column, so the column sum needs no exchange within a tile.
 //     p = exp2(fma(c, s, b)) / sum, summed over a lane's rows of a tile in fp32 and accumulated
-//     across tiles in fp64. 16-bit inputs use 16x16x32 blocks, so that each block's exponentials
-//     overlap the next block's matrix chain. Both passes form the exponent with one fused multiply-add
+//     across tiles in fp64. 16-bit inputs use 16x16x32 blocks and 64-row tiles, so that each
+//     block's exponentials overlap the next block's matrix chain within the wave and a barrier
+//     serves 64 rows. Both passes form the exponent with one fused multiply-add
 //     against the same offset, so the offset is a common factor of a row's terms and of its sum
 //     and cancels in p; it only has to keep every exponent at or below about 0. Being a whole
 //     number, a move of the running max rescales pass 1's fp64 sum by an exact power of two
