@@ -8,6 +8,7 @@ constexpr int kNumXcd = 8;       // accelerator dies; workgroup i runs on die i 
 constexpr int kRowBlock = 256;      // window rows per row-statistics workgroup
 constexpr int kColBlockKeys = 256;  // keys per column-sum workgroup (its waves share each staged row tile)
 constexpr int kColThreads16 = 256;  // column-sum workgroup for 16-bit inputs: 4 waves of 64 keys
+constexpr int kRowThreads16 = 256;  // row-statistics workgroup for 16-bit inputs: 4 waves of 64 rows
 
 struct EvictArgs {
   const void* q_win;   // [L][B][Hq][W][d]
@@ -17,7 +18,7 @@ struct EvictArgs {
   void* k_out;         // [L][B][Hkv][out_rows][d], rows [0, keep) written
   void* v_out;
   float* score;        // [L][B][Hkv][T] accumulated attention (token_score or workspace)
-  float2* rowstat;     // [L][B][Hq][W]: (b = -ceil(c * max score), 1 / sum of exp2(fma(c, score, b)))
+  float2* rowstat;     // [L][B][Hq][W]: (whole-number offset b, every fma(c, score, b) <= 1; 1 / sum of exp2(fma(c, score, b)))
   float* row_lse;      // [L][B][Hq][W] natural log-sum-exp, optional
   int B, layer0, n_layers, Hq, Hkv, T, W, keep, local_keep, causal, period, start;
   int out_rows;        // row capacity of k_out / v_out per (layer, sequence, kv head)

@@ -2,25 +2,26 @@
 //
 // The accumulated attention of key j is A[j] = sum over the group's window rows t of
 // softmax_j(sm_scale * q_t . k_j). It needs every row's normaliser before any column can be
-// summed, so it takes two passes over the scores, both on the matrix cores
-// (v_mfma_f32_32x32x{16,16,2}_{bf16,f16,f32}; the column pass of 16-bit inputs 16x16x32):
-//   pass 1 (k_rowstats): window rows stay in registers as the B operand, key tiles stream
-//     through LDS as the A operand; each lane owns one query column of the 32x32 output, so the
-//     row max and row sum are in-lane reductions. Output per row: the whole-number offset
-//     b = -ceil(fp32(c * m)) of the row max m and 1 / sum of exp2(fma(c, s, b)),
+// summed, so it takes two passes over the scores, both on the matrix cores (16-bit inputs:
+// v_mfma_f32_16x16x32_{bf16,f16} blocks; fp32 inputs: v_mfma_f32_32x32x2f32):
+//   pass 1 (k_rowstats16, k_rowstats for fp32): window rows stay in registers as the B operand,
+//     key tiles stream through LDS as the A operand; each lane owns one query column of its
+//     blocks, so a row's sum needs no exchange until the end. Output per row: a whole-number
+//     offset b >= -ceil(fp32(c * m)) for the row max m with every exponent fma(c, s, b) at most 1
+//     (b = -ceil(fp32(c * m)) for fp32 inputs), and 1 / sum of exp2(fma(c, s, b)),
 //     c = fp32(sm_scale * log2(e)).
 //   pass 2 (k_colsum16 for 16-bit inputs, k_colsum for fp32): keys stay in registers as the B
 //     operand, window-row tiles (all query heads of the group) stream through LDS as the A
 //     operand; each lane owns one key column, so the column sum needs no exchange within a tile.
 //     p = exp2(fma(c, s, b)) / sum, summed over a lane's rows of a tile in fp32 and accumulated
-//     across tiles in fp64. 16-bit inputs use 16x16x32 blocks and 64-row tiles, so that each
-//     block's exponentials overlap the next block's matrix chain within the wave and a barrier
-//     serves 64 rows. Both passes form the exponent with one fused multiply-add
+//     across tiles in fp64. For 16-bit inputs both passes use 16x16 blocks and 64-row (64-key)
+//     tiles, so that each block's exponentials overlap the next block's matrix chain within the
+//     wave and a barrier serves 64 rows. Both passes form the exponent with one fused multiply-add
 //     against the same offset, so the offset is a common factor of a row's terms and of its sum
-//     and cancels in p; it only has to keep every exponent at or below about 0. Being a whole
-//     number, a move of the running max rescales pass 1's fp64 sum by an exact power of two
-//     (ldexp). The exponents of the terms near the max lie in (-1, 0], so their rounding, and that
-//     of c (proportional to |c * (s - m)|), stay smallest on the terms that carry the sums.
+//     and cancels in p; it only has to keep every exponent at or below about 1. Being a whole
+//     number, a move of the offset rescales pass 1's sums by an exact power of two (ldexp). The
+//     exponents of the terms near the max lie in (-1, 1], so their rounding, and that of c
+//     (proportional to |c * (s - m)|), stay smallest on the terms that carry the sums.
 // The top-k is a 4-pass, 8-bit LDS radix select on the fp32 score bits followed by an ordered
 // block compaction, each thread's run of scores held in registers up to 32K older tokens; the
 // gather copies kept rows with 16-byte lanes (all layers, or those whose representatives are not
@@ -129,20 +130,21 @@ struct TileChunks {
   __device__ bool ok(int i) const { return (i + 1) * NT <= TL::CHUNKS || tid + i * NT < TL::CHUNKS; }
 };
 
-// Shape of the 32x32 scoring passes (pass 1; pass 2 for fp32 inputs): a workgroup covers 256
-// window rows (pass 1) or 256 keys (pass 2) as NBK register blocks of 32 per wave and 8 / NBK
-// waves. 16-bit inputs take two blocks per wave, so that every fragment staged in LDS feeds two
-// matrix instructions (half the LDS reads and per-tile overhead per score) at three waves per
-// SIMD; fp32 fragments take twice the registers and keep one block per wave.
+// Shape of the 32x32 scoring passes (fp32 inputs; 16-bit inputs take the 16x16 kernels): a
+// workgroup covers 256 window rows (pass 1) or 256 keys (pass 2) as NBK register blocks of 32 per
+// wave and 8 / NBK waves; fp32 fragments keep one block per wave.
 template <class DT>
 struct PassShape {
-  static constexpr int NBK = DT::kElt == 2 ? 2 : 1;
+  static_assert(DT::kElt == 4, "16-bit inputs take k_rowstats16 / k_colsum16");
+  static constexpr int NBK = 1;
   static constexpr int WAVES = kRowBlock / 32 / NBK;
   static constexpr int THREADS = WAVES * kWave;
-  static constexpr int MIN_WAVES = NBK == 2 ? 3 : 1;  // waves per SIMD the register budget keeps
+  static constexpr int MIN_WAVES = 1;  // waves per SIMD the register budget keeps
 };
 static_assert(kRowBlock == kColBlockKeys, "both passes cover 256 rows / keys per workgroup");
 
+// Row pass on 32x32 matrix instructions (fp32 inputs; 16-bit inputs take k_rowstats16 below):
+// the offset follows the running max, so every exponent is at most 0.
 template <class DT, int D>
 __global__ __launch_bounds__(PassShape<DT>::THREADS, PassShape<DT>::MIN_WAVES) void k_rowstats(EvictArgs a) {
   using M = Mma<DT>;
@@ -425,6 +427,184 @@ __global__ __launch_bounds__(PassShape<DT>::THREADS, PassShape<DT>::MIN_WAVES) v
     const double tot = cacc[u] + __shfl_xor(cacc[u], 32);
     const int j = jw + 32 * u + c32;
     if (hl == 0 && j < a.T) a.score[(size_t)kvunit * a.T + j] = (float)tot;
+  }
+}
+
+// Row pass for 16-bit inputs on 16x16x32 matrix instructions. A wave holds 64 window rows in
+// registers as four 16-row B operands (query groups) and takes each 64-key tile from LDS as four
+// 16-key A operands, so a tile is sixteen 16x16 blocks; a lane holds keys 4 (lane / 16) + r of one
+// row per block. Each block's exponentials are taken against the row's current offset, with no
+// running max, beside the next block's matrix chain (one basic block, so the two interleave). A
+// block whose four terms sum to at most 2 has every exponent at most 1, as accurate as an offset
+// at the max; a larger sum takes the slow path: the offset moves to the block's max if that is
+// higher (the running sums rescaled by an exact power of two) and the block is summed again. The
+// four lanes of a row meet once at the end at the smallest offset, so no exponent of pass 2 exceeds 1.
+template <class DT, int D>
+__global__ __launch_bounds__(kRowThreads16, 3) void k_rowstats16(EvictArgs a) {
+  constexpr int NT = kRowThreads16;
+  constexpr int KT = 64;  // keys per staged tile
+  using TL = Tile<DT, D, NT, KT>;
+  constexpr int KS = D / 32;
+  static_assert(DT::kElt == 2, "16-bit inputs");
+  static_assert(NT / kWave * 64 == kRowBlock, "four waves of 64 rows");
+  __shared__ __align__(16) unsigned char s_k[2][TL::BYTES];
+
+  const int n_rb = (a.W + kRowBlock - 1) / kRowBlock;
+  const int id = xcd_remap(blockIdx.x, gridDim.x);
+  const int rb = id % n_rb;
+  const int ou = id / n_rb;  // (owner index * B + b) * Hq + hq
+  const int l = a.own.local(ou / (a.B * a.Hq));
+  const int b = (ou / a.Hq) % a.B, hq = ou % a.Hq;
+  const size_t qunit = ((size_t)l * a.B + b) * a.Hq + hq;
+  const int G = a.Hq / a.Hkv;
+  const size_t kvunit = ((size_t)l * a.B + b) * a.Hkv + hq / G;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, c16 = lane & 15, q4 = lane >> 4;
+
+  // query group g of this wave holds window rows row0 + 16 g + lane % 16
+  const int row0 = rb * kRowBlock + w * 64;
+  int t[4], pos[4];
+  uint4 qf[4][KS];
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    t[g] = row0 + 16 * g + c16;
+    const int tc = t[g] < a.W ? t[g] : a.W - 1;
+    pos[g] = a.T - a.W + tc;
+    const char* qrow = (const char*)a.q_win + ((size_t)qunit * a.W + tc) * TL::RB;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) qf[g][ks] = ldg16(qrow + (ks * 32 + q4 * 8) * DT::kElt);
+  }
+
+  const char* kh = (const char*)a.k + kvunit * a.T * TL::RB;
+  const int last_row = min(a.W - 1, rb * kRowBlock + kRowBlock - 1);
+  const int jend = a.causal ? min(a.T, a.T - a.W + last_row + 1) : a.T;
+  const int ntile = (jend + KT - 1) / KT;
+
+  const TileChunks<TL, NT> tc(tid);
+  uint4 pre[TL::PER];
+  // key tiles lying wholly inside the cache load without per-chunk row tests or zero fills
+  auto fetch = [&](int tile) {
+    const char* tb = kh + (size_t)tile * (KT * TL::RB);
+    if (tile * KT + KT <= a.T) {
+#pragma unroll
+      for (int i = 0; i < TL::PER; ++i)
+        if (tc.ok(i)) pre[i] = ldg16(tb + tc.mem[i]);
+    } else {
+#pragma unroll
+      for (int i = 0; i < TL::PER; ++i)
+        pre[i] = tc.ok(i) && tile * KT + (int)tc.row[i] < a.T ? ldg16(tb + tc.mem[i]) : make_uint4(0, 0, 0, 0);
+    }
+  };
+  auto stash = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < TL::PER; ++i)
+      if (tc.ok(i)) *(uint4*)&s_k[buf][tc.lds[i]] = pre[i];
+  };
+  fetch(0);
+  stash(0);
+  // the row operands are in registers before the loop, so that no wait for them lands inside it
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+
+  const float cf = a.c32;
+  float nb[4];    // whole-number offset of each query group's row (this lane's keys)
+  double ell[4];  // sum of exp2(fma(c, s, nb)) so far
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    nb[g] = INFINITY;
+    ell[g] = 0.0;
+  }
+  // one tile; block b = (key quarter b / 4, query group b % 4). FULL: every key of the tile visible
+  // to every row of the wave
+  auto tile = [&](auto full_tag, int buf, int j0) {
+    constexpr bool FULL = decltype(full_tag)::value;
+    float psg[4] = {0.f, 0.f, 0.f, 0.f};
+    uint4 af[KS];
+    auto load_af = [&](int kq) {
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+        af[ks] = *(const uint4*)&s_k[buf][(16 * kq + c16) * TL::RS + (ks * 32 + q4 * 8) * DT::kElt];
+    };
+    auto chain = [&](int g) {
+      f32x4 c = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) c = mma16<DT>(af[ks], qf[g][ks], c);
+      return c;
+    };
+    auto visible = [&](int kq, int g, int r) {
+      if constexpr (FULL) return true;
+      const int j = j0 + 16 * kq + 4 * q4 + r;
+      return j < a.T && (!a.causal || j <= pos[g]);
+    };
+    auto sum4 = [&](const f32x4& c, int kq, int g) {
+      float ps = 0.f;
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        if (visible(kq, g, r)) ps += fast_exp2(fmaf(cf, c[r], nb[g]));
+      return ps;
+    };
+    auto finish = [&](const f32x4& c, int kq, int g, float ps) {
+      if (ps > 2.f) {  // an exponent may exceed 1 (or the row's first terms): offset at the max
+        float tmax = -INFINITY;
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (visible(kq, g, r)) tmax = fmaxf(tmax, c[r]);
+        const float nb_new = -ceilf(cf * tmax);
+        if (nb_new < nb[g]) {
+          const int d = (int)(nb_new - nb[g]);
+          if (ell[g] > 0.0) ell[g] = ldexp(ell[g], d);
+          if (psg[g] > 0.f) psg[g] = ldexpf(psg[g], d);
+          nb[g] = nb_new;
+        }
+        ps = sum4(c, kq, g);
+      }
+      psg[g] += ps;
+    };
+    load_af(0);
+    f32x4 cp = chain(0);
+#pragma unroll
+    for (int bb = 1; bb < 4 * (KT / 16); ++bb) {
+      if ((bb & 3) == 0) load_af(bb >> 2);
+      const f32x4 cc = chain(bb & 3);
+      const int kp = (bb - 1) >> 2, gp = (bb - 1) & 3;
+      finish(cp, kp, gp, sum4(cp, kp, gp));
+      cp = cc;
+    }
+    finish(cp, KT / 16 - 1, 3, sum4(cp, KT / 16 - 1, 3));
+#pragma unroll
+    for (int g = 0; g < 4; ++g) ell[g] += (double)psg[g];
+  };
+  for (int it = 0; it < ntile; ++it) {
+    const int buf = it & 1;
+    if (it + 1 < ntile) fetch(it + 1);
+    const int j0 = it * KT;
+    if (j0 + KT - 1 < a.T && (!a.causal || j0 + KT - 1 <= a.T - a.W + row0))
+      tile(std::true_type{}, buf, j0);
+    else
+      tile(std::false_type{}, buf, j0);
+    if (it + 1 < ntile) stash(buf ^ 1);
+    __syncthreads();
+  }
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    // the four lanes of a row (lane % 16 equal) meet at the smallest offset, in two pairwise steps
+    double e = ell[g];
+    float o = nb[g];
+#pragma unroll
+    for (int x = 16; x <= 32; x <<= 1) {
+      const double eo = __shfl_xor(e, x);
+      const float oo = __shfl_xor(o, x);
+      const float ox = fminf(o, oo);
+      double L = 0.0;
+      if (e > 0.0) L += ldexp(e, (int)(ox - o));
+      if (eo > 0.0) L += ldexp(eo, (int)(ox - oo));
+      e = L;
+      o = ox;
+    }
+    if (q4 == 0 && t[g] < a.W) {
+      a.rowstat[(size_t)qunit * a.W + t[g]] = make_float2(o, (float)(1.0 / e));
+      // log-sum-exp of the scaled scores: log2 of sum exp2(c * s) = log2(L) - offset
+      if (a.row_lse) a.row_lse[(size_t)qunit * a.W + t[g]] = (float)((log2(e) - (double)o) * 0.69314718055994531);
+    }
   }
 }
 
@@ -816,7 +996,10 @@ template <class DT, int D>
 hipError_t launch_pass(const EvictArgs& a, bool rows, hipStream_t st) {
   if (rows) {
     const int n_rb = (a.W + kRowBlock - 1) / kRowBlock;
-    hipLaunchKernelGGL((k_rowstats<DT, D>), dim3(a.own.n * a.B * a.Hq * n_rb), dim3(PassShape<DT>::THREADS), 0, st, a);
+    if constexpr (DT::kElt == 2)
+      hipLaunchKernelGGL((k_rowstats16<DT, D>), dim3(a.own.n * a.B * a.Hq * n_rb), dim3(kRowThreads16), 0, st, a);
+    else
+      hipLaunchKernelGGL((k_rowstats<DT, D>), dim3(a.own.n * a.B * a.Hq * n_rb), dim3(PassShape<DT>::THREADS), 0, st, a);
   } else {
     const int n_kb = (a.T + kColBlockKeys - 1) / kColBlockKeys;
     if constexpr (DT::kElt == 2)
