@@ -116,10 +116,11 @@ def test_static_evict_matches_oracle(name):
     say(f"  tie swaps {swaps}, worst score relative error {worst:.2e}")
 
 
-# Edges of the scoring passes' register blocks (a wave holds two blocks of 32 window rows in the
-# row pass and two blocks of 32 keys in the column pass; a workgroup covers 256 rows / keys): windows
-# that end inside a wave's first or second row block or just past a workgroup, key ranges that end
-# inside a wave's second key block, both element sizes and head dims, grouped heads.
+# Edges of the scoring passes' register blocks (for 16-bit inputs a wave holds 64 window rows in the
+# row pass and 64 keys in the column pass as four groups of 16, tiles of 64 keys / rows are staged
+# per barrier, and a workgroup covers 256 rows / keys; fp32 inputs use one 32-row block per wave):
+# windows that end inside a wave's groups or just past a workgroup, key ranges that end inside a
+# staged tile, both element sizes and head dims, grouped heads.
 EDGE_CASES = {
     "W20-T1000": dict(base="C3", n_q_heads=4, n_kv_heads=1, T=1000, window=20, keep=512),
     "W33-T993-fp16": dict(base="C3", n_q_heads=2, n_kv_heads=2, dtype="fp16", T=993, window=33, keep=480),
@@ -141,6 +142,39 @@ def test_static_evict_block_edges(name):
     swaps, worst = _check(w, qw, k, v, got)
     _row_lse_check(w, qw, k, got[4], rows=16)
     say(f"  tie swaps {swaps}, worst score relative error {worst:.2e}")
+
+
+# All-zero window queries: every score is 0, so every block of the row pass sums four terms of
+# exactly 1 and goes through its offset check's slow path, and the accumulated attention has a
+# closed form: key j receives 1 / (T - W + t + 1) from every window row t that sees it, once per
+# query head of its group, and row t's log-sum-exp is ln(T - W + t + 1). Most older tokens tie.
+EQUAL_CASES = {
+    "bf16-d128": dict(base="C3", n_q_heads=4, n_kv_heads=2, T=1100, window=200, keep=560),
+    "fp16-d64": dict(base="C2", n_q_heads=4, n_kv_heads=2, dtype="fp16", T=777, window=150, keep=400),
+}
+
+
+@pytest.mark.parametrize("name", list(EQUAL_CASES))
+def test_static_evict_equal_scores(name):
+    o = dict(EQUAL_CASES[name])
+    w = synth.get(o.pop("base")).with_(n_layers=1, **o)
+    say(f"[evict equal scores] {name} Hq={w.n_q_heads} Hkv={w.n_kv_heads} d={w.head_dim} T={w.T} "
+        f"W={w.window} keep={w.keep} {w.dtype}")
+    qw, k, v = _prefill(w)
+    qw = np.zeros_like(qw)
+    got = _run_gpu(w, qw, k, v)
+    T, W = w.T, w.window
+    seen = T - W + np.arange(W) + 1                       # keys row t attends
+    tail = np.cumsum((1.0 / seen)[::-1])[::-1]            # tail[t] = sum over rows t' >= t of 1 / seen
+    first = np.clip(np.arange(T) - (T - W), 0, None)      # first window row that sees key j
+    exact = w.group * tail[first]
+    for b in range(w.batch):
+        for h in range(w.n_kv_heads):
+            np.testing.assert_allclose(got[3][0, b, h], exact, rtol=1e-6)
+        for hq in range(w.n_q_heads):
+            np.testing.assert_allclose(got[4][0, b, hq], np.log(seen), rtol=1e-6)
+    swaps, worst = _check(w, qw, k, v, got)
+    say(f"  closed form ok; tie swaps {swaps}, worst score relative error {worst:.2e}")
 
 
 def test_static_evict_block_whose_first_owner_precedes_it():
