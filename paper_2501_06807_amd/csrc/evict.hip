@@ -573,14 +573,19 @@ __global__ __launch_bounds__(kRowThreads16, 3) void k_rowstats16(EvictArgs a) {
 #pragma unroll
     for (int g = 0; g < 4; ++g) ell[g] += (double)psg[g];
   };
+  // a wave whose rows all lie past the window (the last workgroup of a ragged window) only helps
+  // stage the tiles
+  const bool rows_live = row0 < a.W;
   for (int it = 0; it < ntile; ++it) {
     const int buf = it & 1;
     if (it + 1 < ntile) fetch(it + 1);
     const int j0 = it * KT;
-    if (j0 + KT - 1 < a.T && (!a.causal || j0 + KT - 1 <= a.T - a.W + row0))
-      tile(std::true_type{}, buf, j0);
-    else
-      tile(std::false_type{}, buf, j0);
+    if (rows_live) {
+      if (j0 + KT - 1 < a.T && (!a.causal || j0 + KT - 1 <= a.T - a.W + row0))
+        tile(std::true_type{}, buf, j0);
+      else
+        tile(std::false_type{}, buf, j0);
+    }
     if (it + 1 < ntile) stash(buf ^ 1);
     __syncthreads();
   }
