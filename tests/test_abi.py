@@ -291,3 +291,32 @@ def test_noalloc_refuses_a_block_beyond_its_scratch():
     s, _ = _status("mpc_static_evict_noalloc", ctypes.byref(d), T, ctypes.byref(cfg), None, FAKE, FAKE, FAKE, FAKE,
                    FAKE, None, None, None)
     assert s == L.MPC_EINVAL
+
+
+def test_layer_block_limit():
+    """Calls whose layers share kept sets or selections take at most 256 layers (the owner tables and
+    the prefill's per-layer masks are sized for that); a block of 257 is refused before anything runs."""
+    d = _dims(n_layers=257, n_q_heads=2, n_kv_heads=1, head_dim=64)
+    dc = _dims(n_layers=257, n_q_heads=2, n_kv_heads=1, head_dim=64, kv_capacity=512)
+    ecfg = L.MpcEvictCfg(window=32, keep=64, local_keep=8, sm_scale=0.125, causal=1, share_period=3,
+                         share_start=2)
+    scfg = L.select_cfg(16, 4, 2, 4, share_period=3)
+    ws = 1 << 40  # any workspace size passes: the layer count is refused first
+    calls = {
+        "mpc_static_evict": ("mpc_static_evict", ctypes.byref(d), 160, ctypes.byref(ecfg), FAKE, FAKE, FAKE, FAKE,
+                             FAKE, FAKE, None, None, FAKE, ws, None),
+        "mpc_static_evict_noalloc": ("mpc_static_evict_noalloc", ctypes.byref(d), 160, ctypes.byref(ecfg), FAKE,
+                                     FAKE, FAKE, FAKE, FAKE, FAKE, None, None, None),
+        "mpc_build_clusters": ("mpc_build_clusters", ctypes.byref(d), 256, ctypes.byref(scfg), FAKE, FAKE, FAKE, None),
+        "mpc_prefill": ("mpc_prefill", ctypes.byref(d), 160, ctypes.byref(ecfg), ctypes.byref(scfg), FAKE, FAKE, FAKE,
+                        FAKE, FAKE, FAKE, FAKE, FAKE, None, None, FAKE, ws, None),
+        "mpc_select_clusters": ("mpc_select_clusters", ctypes.byref(d), 256, ctypes.byref(scfg), FAKE, FAKE, FAKE,
+                                FAKE, None, FAKE, ws, None),
+        "mpc_decode_step": ("mpc_decode_step", ctypes.byref(d), 256, 0, ctypes.byref(scfg), FAKE, FAKE, FAKE, FAKE,
+                            FAKE, 0.125, FAKE, None, FAKE, None, FAKE, ws, None),
+        "mpc_append_kv": ("mpc_append_kv", ctypes.byref(dc), 256, 3, ctypes.byref(scfg), FAKE, FAKE, FAKE, FAKE,
+                          FAKE, FAKE, None, None, None),
+    }
+    for name, args in calls.items():
+        s, msg = _status(*args)
+        assert s == L.MPC_EUNSUPPORTED and "256" in msg, (name, s, msg)

@@ -101,6 +101,8 @@ CASES = {
     "C3-fp16": dict(n_layers=1, n_q_heads=4, n_kv_heads=2, dtype="fp16", T=2000, window=400, keep=1024),
     "C3-fp32": dict(n_layers=1, n_q_heads=2, n_kv_heads=2, dtype="fp32", T=1500, window=300, keep=768),
     "C2-bf16": dict(n_layers=2, n_q_heads=4, n_kv_heads=2, dtype="bf16", T=1300, window=260, keep=640),
+    # the most layers one call takes (256): owners on both sides of every 64-layer boundary
+    "C2-L256": dict(n_layers=256, n_q_heads=2, n_kv_heads=1, T=160, window=32, keep=80, share_period=3),
 }
 
 
