@@ -68,6 +68,8 @@ CASES = {
     # the block's first layer is owned by a layer before it: its kept set arrives in place
     "C2-owner-before": ("C2", dict(n_layers=3, T=700, window=140, keep=320, n_q_heads=4, n_kv_heads=4),
                         "linear", 3, 0, None),
+    # every token kept, the window the whole prompt, no recent tokens kept by rule
+    "C2-keep-all": ("C2", dict(n_layers=3, T=300, window=300, keep=300, local_keep=0), "maxprod", 0, 0, None),
     # the most layers one call takes (256): the gather's mask of layers left to the build spans four
     # 64-layer words; kept sets shared by threes, representatives by fives
     "C2-L256": ("C2", dict(n_layers=256, n_q_heads=2, n_kv_heads=1, T=160, window=32, keep=80, share_period=3),
