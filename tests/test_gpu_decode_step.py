@@ -43,6 +43,10 @@ CASES = {
     "X1-L8": ("X1", dict(n_layers=8), 0),
     # the dynamic ratio read against the prompt length (40 clusters per selection)
     "C5-T-L32": ("C5-T", dict(keep=8192, k_super=8), 0),
+    # degenerate budgets: one partial cluster of 10 tokens (one super-cluster, three of its four
+    # member slots empty); every cluster of every super-cluster selected (256 units, self-selecting)
+    "C2-one-cluster": ("C2", dict(keep=10, k_super=1, k_clusters=1), 0),
+    "C2-all-selected": ("C2", dict(n_layers=32, n_q_heads=8, n_kv_heads=8, keep=512, k_super=8, k_clusters=32), 0),
     # the most layers one call takes (256): one kv head -> 256 units (self-selecting); two kv heads
     # from layer 5 -> 512 units (claiming), layer 5 owned by layer 4 before the block
     "C2-L256": ("C2", dict(n_layers=256, n_q_heads=1, n_kv_heads=1, keep=512), 0),
