@@ -37,6 +37,9 @@
  *     returned status covers argument validation and launch errors only; it never waits for the
  *     GPU. A validation failure (MPC_EINVAL / ESHAPE / EUNSUPPORTED / EWORKSPACE) enqueues
  *     nothing; after MPC_EHIP, kernels launched before the failing one may have been enqueued.
+ *   - Apart from mpc_decode_step_status (a blocking read), no call allocates, sets memory, waits on
+ *     the host or uses a stream other than `stream`. So calls can be captured into a HIP graph,
+ *     whose replays rerun the same kernels on the same pointers and sizes.
  *   - Supported: d in {64, 128}; G in {1, 2, 4, 8}; dtype fp32 / fp16 / bf16.
  */
 #ifndef MPCACHE_H

@@ -136,6 +136,17 @@ class MPCachePath:
         self.attend(q, stream)
         return self.out
 
+    def capture(self, fn, *args):
+        """A HIP graph (torch.cuda.CUDAGraph) of fn(*args), e.g. capture(self.decode, q_buf) or
+        capture(self.prefill, q_win, k, v). Replaying it reruns the same kernels on the same buffers,
+        so the caller refills the input buffers between replays. The entry points only enqueue kernels
+        (no allocation, memset or host wait), so capture needs nothing else from them. A graph keeps
+        the cache state (Ts, n_tail) it was captured with: capture again after append()."""
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            fn(*args)
+        return g
+
     def decode_fused(self, q, stream=None):
         st = L._stream(stream)
         L._check("mpc_decode_step",
