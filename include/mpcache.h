@@ -133,11 +133,12 @@ size_t mpc_workspace_bytes(int32_t op, const mpc_dims* dims, int32_t T_or_Ts, co
  *   ws          workspace of mpc_workspace_bytes(MPC_OP_STATIC_EVICT, dims, T, cfg) bytes.
  * Accumulation: fp32 matrix-core dot products; each exponent is one fp32 fused multiply-add
  * against a per-row whole-number offset that keeps every exponent at most 1, shared by the row sum
- * and the column sums; sums of 16 terms in fp32, accumulated across tiles in fp64. token_score matches the exact (fp64)
- * scores within a relative 2e-5 (the bound the tests hold it to; the largest error measured over
- * every token of the tested cases is 1.8e-6, and 3.3e-7 to 7.3e-7 at the 8K-32K workloads, where
- * tokens near the keep boundary are within 3e-7, as they are at 128K), so a kept set can differ
- * from the exact one only between tokens whose exact scores tie within about 1e-6. */
+ * and the column sums; sums of at most 16 terms in fp32, accumulated across tiles in fp64.
+ * token_score matches the exact (fp64) scores within a relative 2e-5 (the bound the tests hold it
+ * to; the largest error measured over every token of the tested cases is 1.8e-6, and 3.3e-7 to
+ * 7.3e-7 at the 8K-32K workloads, where tokens near the keep boundary are within 3e-7, as they are
+ * at 128K), so a kept set can differ from the exact one only between tokens whose exact scores tie
+ * within about 1e-6. */
 mpc_status mpc_static_evict(const mpc_dims* dims, int32_t T, const mpc_evict_cfg* cfg,
                             const void* q_win, const void* k, const void* v, int32_t* kept_idx,
                             void* k_out, void* v_out, float* token_score, float* row_lse,
