@@ -98,3 +98,49 @@ def test_prefill_graph_replays_equal_eager(case):
             assert torch.equal(_bits(t) if t.dtype != torch.int32 else t, _bits(r) if r.dtype != torch.int32 else r), \
                 (rep, n)
     say("  3 replays equal to the eager prefill")
+
+
+def test_noalloc_eviction_graph_replays_equal_eager():
+    """The static eviction without allocation, captured as a graph (its scratch address is looked
+    up by an eager call first): every replay equals the eager workspace call."""
+    import math
+    import paper_2501_06807_amd as M
+    w = synth.get("C2").with_(n_layers=4)
+    say(f"[graph noalloc] C2 L={w.n_layers} T={w.T} W={w.window} keep={w.keep}")
+    q_win, k, v, _ = _inputs(w, steps=1)
+    L, B, Hkv = w.n_layers, w.batch, w.n_kv_heads
+    dt = synth.torch_dtype(w.dtype)
+    kw = dict(keep=w.keep, local_keep=w.local_keep, sm_scale=1.0 / math.sqrt(w.head_dim), share_period=w.share_period,
+              share_start=w.share_start)
+
+    def buffers():
+        return dict(kept=torch.zeros((L, B, Hkv, w.keep), dtype=torch.int32, device="cuda"),
+                    k_out=torch.zeros((L, B, Hkv, w.keep, w.head_dim), dtype=dt, device="cuda"),
+                    v_out=torch.zeros((L, B, Hkv, w.keep, w.head_dim), dtype=dt, device="cuda"),
+                    score=torch.zeros((L, B, Hkv, w.T), dtype=torch.float32, device="cuda"),
+                    lse=torch.zeros((L, B, w.n_q_heads, w.window), dtype=torch.float32, device="cuda"))
+
+    def call(o, noalloc):
+        fn = M.mpc_static_evict_noalloc if noalloc else M.mpc_static_evict
+        fn(q_win, k, v, o["kept"], o["k_out"], o["v_out"], token_score=o["score"], row_lse=o["lse"], **kw)
+
+    ref = buffers()
+    call(ref, False)
+    got = buffers()
+    call(got, True)  # eager: the scratch address of this device is looked up here
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        call(got, True)
+    for rep in range(3):
+        for t in got.values():
+            t.zero_()
+        call(buffers(), False)  # eager work of the program between replays
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for n in ref:
+            a, b = got[n], ref[n]
+            assert torch.equal(a if a.dtype == torch.int32 else _bits(a), b if b.dtype == torch.int32 else _bits(b)), \
+                (rep, n)
+    say("  3 replays equal to the eager workspace call")
